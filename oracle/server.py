@@ -1,0 +1,232 @@
+"""Sequential ASGD parameter server, written plainly (test infrastructure).
+
+Only the tests, the smoke check and the benchmark's CPU-baseline leg use this
+module; the product path never imports it.
+
+What it follows (GaDei, arXiv 1611.06213):
+  * Sec. 2.1, Fig. "design_base": learners push gradients to the server and
+    pull weights from it; they never talk to each other.
+  * Eq. "asgd" with the step of Eq. "gd": each received gradient is applied on
+    its own, in the order it was received.
+  * Sec. 2.1: the server's scalar timestamp grows by one per update; the
+    staleness of a gradient is the server timestamp minus the timestamp of
+    the weights the learner held.
+  * Sec. 4.1 and Lemma 1 / Theorem 2 (Sec. 4.2): gradients wait in a FIFO with
+    a fixed number of slots; a full queue refuses the pusher; each queued
+    gradient is applied exactly once.
+  * Sec. 4.1: a pull is skipped when the learner's copy already carries the
+    server's timestamp.
+
+Readings where the paper is silent (each also listed in the design notes):
+  * one global FIFO in push-call order stands in for the per-learner queues;
+  * a batch of K pending gradients is applied as K sequential steps, each over
+    the whole vector, oldest first;
+  * a full queue returns EFULL instead of blocking;
+  * momentum, when non-zero, is heavy-ball kept on the server (v0 = +0);
+  * the staleness of a push uses the timestamp the learner held when it
+    pushed; every learner starts holding w0 at timestamp 0;
+  * a pull is skipped iff the same learner pulls into the same buffer with
+    the same dtype and the timestamp has not moved since its last pull.
+
+The oracle can be run on any coordinate range [lo, hi) of a workload: every
+step is per coordinate (Eq. "gd" is written for the k-th parameter), so the
+range run is exactly the full run restricted to those coordinates.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, List, Optional, Tuple
+
+import numpy as np
+
+OK = 0
+EINVAL = -1
+EFULL = -2
+ESTATE = -5
+
+F32 = 0
+BF16 = 1
+
+MAX_DEPTH = 64
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_lib = None
+
+
+def lib():
+    """Load oracle/liboracle.so, compiling it with gcc if it is not built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    path = os.path.join(_HERE, "liboracle.so")
+    src = os.path.join(_HERE, "asgd_oracle.c")
+    if not os.path.exists(path) or os.path.getmtime(path) < os.path.getmtime(src):
+        from . import build
+        build.build()
+    L = ctypes.CDLL(path)
+    fp = ctypes.POINTER(ctypes.c_float)
+    up = ctypes.POINTER(ctypes.c_uint16)
+    sz = ctypes.c_size_t
+    fl = ctypes.c_float
+    L.orc_step_f32.argtypes = [fp, fp, sz, fl]
+    L.orc_step_mom_f32.argtypes = [fp, fp, fp, sz, fl, fl]
+    L.orc_step_bf16.argtypes = [fp, up, sz, fl]
+    L.orc_step_mom_bf16.argtypes = [fp, fp, up, sz, fl, fl]
+    L.orc_pull_f32.argtypes = [fp, fp, sz]
+    L.orc_pull_bf16.argtypes = [up, fp, sz]
+    L.orc_widen_bf16.argtypes = [fp, up, sz]
+    L.orc_widen_bf16.restype = None
+    L.orc_bf16_to_f32.argtypes = [ctypes.c_uint16]
+    L.orc_bf16_to_f32.restype = ctypes.c_float
+    L.orc_f32_to_bf16.argtypes = [ctypes.c_float]
+    L.orc_f32_to_bf16.restype = ctypes.c_uint16
+    for f in ("orc_step_f32", "orc_step_mom_f32", "orc_step_bf16", "orc_step_mom_bf16",
+              "orc_pull_f32", "orc_pull_bf16"):
+        getattr(L, f).restype = None
+    _lib = L
+    return L
+
+
+def _fp(a: np.ndarray):
+    assert a.dtype == np.float32 and a.flags.c_contiguous
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
+
+
+def _up(a: np.ndarray):
+    assert a.dtype == np.uint16 and a.flags.c_contiguous
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_uint16))
+
+
+# ------------------------------------------------------------ single steps
+
+def step(w: np.ndarray, g: np.ndarray, lr: float, v: Optional[np.ndarray] = None,
+         momentum: float = 0.0) -> None:
+    """One ASGD step in place on w (and v). g is float32, or uint16 holding
+    bf16 bit patterns. With v given, the momentum form is used."""
+    L = lib()
+    n = w.size
+    assert g.size == n
+    if v is None:
+        if g.dtype == np.uint16:
+            L.orc_step_bf16(_fp(w), _up(g), n, lr)
+        else:
+            L.orc_step_f32(_fp(w), _fp(g), n, lr)
+    else:
+        if g.dtype == np.uint16:
+            L.orc_step_mom_bf16(_fp(w), _fp(v), _up(g), n, lr, momentum)
+        else:
+            L.orc_step_mom_f32(_fp(w), _fp(v), _fp(g), n, lr, momentum)
+
+
+def pull_copy(w: np.ndarray, dtype: int) -> np.ndarray:
+    """The replica a pull writes: w itself (fp32) or w rounded to bf16 bits."""
+    L = lib()
+    if dtype == F32:
+        out = np.empty_like(w)
+        L.orc_pull_f32(_fp(out), _fp(w), w.size)
+    else:
+        out = np.empty(w.size, np.uint16)
+        L.orc_pull_bf16(_up(out), _fp(w), w.size)
+    return out
+
+
+def f32_to_bf16(x: np.ndarray) -> np.ndarray:
+    return pull_copy(np.ascontiguousarray(x, dtype=np.float32), BF16)
+
+
+def bf16_to_f32(b: np.ndarray) -> np.ndarray:
+    b = np.ascontiguousarray(b, dtype=np.uint16)
+    out = np.empty(b.size, np.float32)
+    lib().orc_widen_bf16(_fp(out), _up(b), b.size)
+    return out
+
+
+# ------------------------------------------------------------ the server
+
+class OracleServer:
+    """Single-threaded sequential ASGD server over a coordinate range."""
+
+    def __init__(self, w0: np.ndarray, lr: float, momentum: float = 0.0, depth: int = 32,
+                 pull_skip: bool = True):
+        self.w = np.array(w0, dtype=np.float32, copy=True)
+        self.lr = float(np.float32(lr))
+        self.momentum = float(np.float32(momentum))
+        self.v = np.zeros_like(self.w) if self.momentum != 0.0 else None
+        if not 1 <= depth <= MAX_DEPTH:
+            raise ValueError("depth")
+        self.depth = depth
+        self.pull_skip = pull_skip
+        self.ts = 0
+        self.queue: List[Tuple[int, np.ndarray, int]] = []   # (learner, grad, learner ts)
+        self.learner_ts: Dict[int, int] = {}
+        self.last_pull: Dict[int, Tuple[object, int, int]] = {}
+        self.replicas: Dict[object, np.ndarray] = {}
+        self.staleness: List[int] = []        # one entry per applied push, in order
+        self.applied_order: List[int] = []    # learner of each applied push
+        self.pulls = 0
+        self.pulls_skipped = 0
+
+    def pending(self) -> int:
+        return len(self.queue)
+
+    def push(self, learner: int, grad: np.ndarray) -> int:
+        if learner < 0:
+            return EINVAL
+        if len(self.queue) == self.depth:
+            return EFULL
+        self.queue.append((learner, grad, self.learner_ts.get(learner, 0)))
+        return OK
+
+    def apply_pending(self) -> int:
+        for learner, g, lts in self.queue:
+            self.staleness.append(self.ts - lts)
+            self.applied_order.append(learner)
+            step(self.w, g, self.lr, self.v, self.momentum)
+            self.ts += 1
+        self.queue = []
+        return OK
+
+    def pull(self, learner: int, dst_key, dtype: int = F32) -> bool:
+        """Refresh replica `dst_key` for `learner`. Returns False if skipped."""
+        self.pulls += 1
+        key = (dst_key, dtype, self.ts)
+        if self.pull_skip and self.last_pull.get(learner) == key:
+            self.pulls_skipped += 1
+            return False
+        self.replicas[dst_key] = pull_copy(self.w, dtype)
+        self.last_pull[learner] = key
+        self.learner_ts[learner] = self.ts
+        return True
+
+    def set_depth(self, depth: int) -> int:
+        if not 1 <= depth <= MAX_DEPTH:
+            return EINVAL
+        if depth < len(self.queue):
+            return ESTATE
+        self.depth = depth
+        return OK
+
+
+def replay(server: OracleServer, events, grads, pull_dtype: int = F32, on_pull=None):
+    """Drive `server` through a workload schedule.
+
+    grads(buf) returns the gradient slice of pool buffer `buf`; learner r
+    pulls into replica key r. on_pull(learners, server) is called after each
+    pull event (the caller may snapshot replicas there)."""
+    for ev in events:
+        kind = type(ev).__name__
+        if kind == "Push":
+            rc = server.push(ev.learner, grads(ev.buf))
+            if rc != OK:
+                raise RuntimeError(f"oracle push failed: {rc}")
+        elif kind == "Apply":
+            server.apply_pending()
+        elif kind == "Pull":
+            for l in ev.learners:
+                server.pull(l, l, pull_dtype)
+            if on_pull is not None:
+                on_pull(ev.learners, server)
+        else:
+            raise ValueError(kind)
+    return server

@@ -1,0 +1,401 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+Each test checks the oracle against something other than itself: closed forms
+of Eq. "gd"/"asgd" (Sec. 2.1), an exact-rational evaluator of binary32
+round-to-nearest-even, the hand-worked protocol script (Sec. 2.1 staleness,
+Sec. 4.1 pull skip, Lemma 1 / Theorem 2), and torch's bfloat16 conversions.
+"""
+import itertools
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from oracle import server as orc
+from tests import golden_script
+
+F = Fraction
+
+
+# ------------------------------------------------ exact binary32 evaluator
+
+def rne32(x: Fraction) -> Fraction:
+    """Round an exact rational to the nearest binary32, ties to even
+    (normals and subnormals; the tests stay far from overflow)."""
+    if x == 0:
+        return F(0)
+    s = -1 if x < 0 else 1
+    a = -x if x < 0 else x
+    e = a.numerator.bit_length() - a.denominator.bit_length()
+    while F(2) ** e > a:
+        e -= 1
+    while F(2) ** (e + 1) <= a:
+        e += 1
+    e = max(e, -126)
+    q = F(2) ** (e - 23)
+    m = a / q
+    fl = m.numerator // m.denominator
+    rem = m - fl
+    if rem > F(1, 2) or (rem == F(1, 2) and fl % 2 == 1):
+        fl += 1
+    assert F(fl) * q < F(2) ** 128
+    return s * F(fl) * q
+
+
+def exact_run(w0, grads, lr, m=None):
+    """Reference evaluation of sequential steps, each operation rounded."""
+    lr = F(float(np.float32(lr)))
+    w = [F(float(x)) for x in w0]
+    v = [F(0)] * len(w) if m is not None else None
+    mm = F(float(np.float32(m))) if m is not None else None
+    for g in grads:
+        for i in range(len(w)):
+            gi = F(float(g[i]))
+            if v is None:
+                p = rne32(lr * gi)
+            else:
+                t = rne32(mm * v[i])
+                v[i] = rne32(t + gi)
+                p = rne32(lr * v[i])
+            w[i] = rne32(w[i] - p)
+    return np.array([float(x) for x in w], np.float32), (
+        None if v is None else np.array([float(x) for x in v], np.float32))
+
+
+def bits(a):
+    return np.asarray(a, np.float32).view(np.uint32)
+
+
+def same_bits(a, b):
+    """Bitwise equality, with +0 and -0 treated alike (rationals carry no
+    sign of zero)."""
+    a = np.asarray(a, np.float32)
+    b = np.asarray(b, np.float32)
+    zero = (a == 0) & (b == 0)
+    return bool(np.all((bits(a) == bits(b)) | zero))
+
+
+def rand_f32(rng, n, scale):
+    return (rng.standard_normal(n) * scale).astype(np.float32)
+
+
+def run_oracle(w0, grads, lr, m=0.0, depth=None):
+    depth = depth or max(1, len(grads))
+    s = orc.OracleServer(w0, lr, m, depth=min(depth, 64))
+    for j, g in enumerate(grads):
+        if s.pending() == s.depth:
+            s.apply_pending()
+        assert s.push(j % 7, g) == orc.OK
+    s.apply_pending()
+    return s
+
+
+# ------------------------------------------------ closed forms
+
+@pytest.mark.parametrize("T", [1, 2, 7, 100, 4096, 65536])
+def test_constant_gradient_closed_form_dyadic(T):
+    """Eq. "gd" T times with a constant gradient: w_T = w0 - T*lr*g.
+    Dyadic w0, lr, g make every intermediate exact, so the check is bitwise."""
+    w0 = np.array([1.0, 0.75, -0.5, 0.625, 0.5 + 2 ** -10], np.float32)
+    g = np.array([2 ** -10, -2 ** -10, 2 ** -12, 3 * 2 ** -11, 2 ** -9], np.float32)
+    lr = 2.0 ** -7
+    n_steps = T
+    s = orc.OracleServer(w0, lr, 0.0, depth=64)
+    done = 0
+    while done < n_steps:
+        k = min(64, n_steps - done)
+        for _ in range(k):
+            s.push(0, g)
+        s.apply_pending()
+        done += k
+    expect = np.array([float(F(float(a)) - T * F(lr) * F(float(b))) for a, b in zip(w0, g)])
+    assert np.array_equal(s.w, expect.astype(np.float32))
+    assert np.array_equal(s.w.astype(np.float64), expect)   # exactly representable
+    assert s.ts == T
+
+
+def test_constant_gradient_closed_form_general():
+    """General values: |w_T - (w0 - T*lr*g)| is within the rounding bound
+    T * 2^-24 * (max|w| + |lr*g|) (one half-ulp per operation)."""
+    rng = np.random.default_rng(1)
+    n, T, lr = 4096, 300, 0.01
+    w0 = rng.uniform(-0.05, 0.05, n).astype(np.float32)
+    g = rand_f32(rng, n, 0.01)
+    s = run_oracle(w0, [g] * T, lr, depth=64)
+    lr32 = np.float64(np.float32(lr))
+    exact = w0.astype(np.float64) - T * lr32 * g.astype(np.float64)
+    maxw = np.maximum(np.abs(w0), np.abs(exact)) + T * np.abs(lr32 * g)
+    bound = T * 2.0 ** -24 * (maxw + np.abs(lr32 * g)) * 1.0001
+    assert np.all(np.abs(s.w.astype(np.float64) - exact) <= bound)
+    # and the error is not trivially zero: rounding really happens
+    assert np.any(s.w.astype(np.float64) != exact)
+
+
+@pytest.mark.parametrize("m", [0.0, 0.9])
+def test_zero_gradient_leaves_weights_bitwise(m):
+    """A zero gradient is a no-op step (w - lr*0 = w), also with momentum
+    starting from v0 = +0."""
+    rng = np.random.default_rng(2)
+    w0 = rng.uniform(-0.05, 0.05, 1000).astype(np.float32)
+    w0[:3] = [0.0, -0.0, 1e-40]          # signed zeros and a subnormal survive too
+    z = np.zeros(1000, np.float32)
+    s = run_oracle(w0, [z] * 10, 0.01, m=m)
+    assert np.array_equal(bits(s.w), bits(w0))
+    if m:
+        assert np.array_equal(bits(s.v), bits(z))
+
+
+@pytest.mark.parametrize("T", [1, 2, 5, 8])
+def test_momentum_closed_form_dyadic(T):
+    """Heavy-ball with constant g: v_t = g(1-m^t)/(1-m) and
+    w_T = w0 - lr*g/(1-m) * (T - m(1-m^T)/(1-m)). With m = 1/2, lr = 2^-7,
+    g = 2^-10, w0 = 1 every term is dyadic and representable: bitwise."""
+    m, lr, g0, w00 = F(1, 2), F(1, 2 ** 7), F(1, 2 ** 10), F(1)
+    w0 = np.array([1.0, 1.0], np.float32)
+    g = np.array([2 ** -10, -2 ** -10], np.float32)
+    s = run_oracle(w0, [g] * T, float(lr), m=float(m), depth=8)
+    v_T = g0 * (1 - m ** T) / (1 - m)
+    w_T = w00 - lr * g0 / (1 - m) * (T - m * (1 - m ** T) / (1 - m))
+    assert s.v[0] == float(v_T) and s.v[1] == -float(v_T)
+    assert s.w[0] == float(w_T) and s.w[1] == float(2 * w00 - w_T)
+
+
+def test_momentum_closed_form_general():
+    """m = 0.9 constant gradient: within a rounding tolerance of the closed
+    form evaluated in double."""
+    rng = np.random.default_rng(3)
+    n, T = 2048, 64
+    w0 = rng.uniform(-0.05, 0.05, n).astype(np.float32)
+    g = rand_f32(rng, n, 1e-3)
+    lr, m = np.float32(0.001), np.float32(0.9)
+    s = run_oracle(w0, [g] * T, float(lr), m=float(m), depth=64)
+    lr64, m64, g64 = float(lr), float(m), g.astype(np.float64)
+    wT = w0 - lr64 * g64 / (1 - m64) * (T - m64 * (1 - m64 ** T) / (1 - m64))
+    vT = g64 * (1 - m64 ** T) / (1 - m64)
+    assert np.allclose(s.v, vT, rtol=2e-5, atol=1e-12)
+    assert np.max(np.abs(s.w - wT)) < 4 * T * 2.0 ** -24 * 0.06
+
+
+# ------------------------------------------------ exact-rational brute force
+
+@pytest.mark.parametrize("m", [None, 0.9])
+def test_brute_force_every_permutation(m):
+    """N <= 8, 5 pushes, every arrival order: the oracle equals an exact-
+    rational evaluation of the same sequence with binary32 RNE after each
+    operation (so a fused multiply-add, a dropped term, a swapped operand or
+    a reordering would show)."""
+    rng = np.random.default_rng(4)
+    n = 8
+    w0 = rng.uniform(-0.05, 0.05, n).astype(np.float32)
+    grads = [rand_f32(rng, n, 0.01) for _ in range(5)]
+    lr = 0.0123
+    for perm in itertools.permutations(range(5)):
+        seq = [grads[p] for p in perm]
+        s = run_oracle(w0, seq, lr, m=(m or 0.0), depth=5)
+        ew, ev = exact_run(w0, seq, lr, m)
+        assert same_bits(s.w, ew), perm
+        if m is not None:
+            assert same_bits(s.v, ev), perm
+
+
+def test_brute_force_detects_contraction():
+    """Sanity of the evaluator itself: a fused multiply-add (single rounding)
+    differs from the two-rounding result on these inputs, so the brute-force
+    test above would catch a contracted oracle."""
+    rng = np.random.default_rng(5)
+    w = rng.uniform(-0.05, 0.05, 200).astype(np.float32)
+    g = rand_f32(rng, 200, 0.01)
+    lr = F(float(np.float32(0.0123)))
+    two = [rne32(F(float(a)) - rne32(lr * F(float(b)))) for a, b in zip(w, g)]
+    fused = [rne32(F(float(a)) - lr * F(float(b))) for a, b in zip(w, g)]
+    assert any(x != y for x, y in zip(two, fused))
+
+
+def test_permutations_within_real_sum_bound():
+    """m = 0: the exact real result w0 - lr*sum(g) does not depend on arrival
+    order (addition in R commutes), so every order lands within the rounding
+    bound of it."""
+    rng = np.random.default_rng(6)
+    n, P = 64, 6
+    w0 = rng.uniform(-0.05, 0.05, n).astype(np.float32)
+    grads = [rand_f32(rng, n, 0.01) for _ in range(P)]
+    lr = np.float32(0.01)
+    exact = w0.astype(np.float64) - float(lr) * np.sum([g.astype(np.float64) for g in grads], axis=0)
+    bound = P * 2.0 ** -24 * (np.abs(w0) + 0.05 + 0.01 * 0.05) * 2
+    for perm in itertools.permutations(range(P)):
+        s = run_oracle(w0, [grads[p] for p in perm], float(lr), depth=P)
+        assert np.all(np.abs(s.w - exact) <= bound)
+
+
+# ------------------------------------------------ batching invariant
+
+@pytest.mark.parametrize("m", [0.0, 0.9])
+@pytest.mark.parametrize("K", [1, 3, 8, 32])
+def test_batched_equals_sequential(K, m):
+    """K pushes folded by one apply give the bits of K applies of one push."""
+    rng = np.random.default_rng(7 + K)
+    n = 1000
+    w0 = rng.uniform(-0.05, 0.05, n).astype(np.float32)
+    grads = [rand_f32(rng, n, 1e-3) for _ in range(2 * K + 1)]
+    a = run_oracle(w0, grads, 0.005, m=m, depth=K)
+    b = run_oracle(w0, grads, 0.005, m=m, depth=1)
+    assert np.array_equal(bits(a.w), bits(b.w))
+    if m:
+        assert np.array_equal(bits(a.v), bits(b.v))
+
+
+def test_bf16_gradient_step_matches_widened_f32():
+    """A bf16 gradient is the fp32 gradient of its widened value: the bf16
+    step equals the fp32 step on torch's widening of the same bits."""
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(8)
+    n = 4096
+    w0 = rng.uniform(-0.05, 0.05, n).astype(np.float32)
+    x = torch.from_numpy(rand_f32(rng, n, 1e-3))
+    gb = x.to(torch.bfloat16)
+    gbits = gb.view(torch.int16).numpy().view(np.uint16).copy()
+    gw = gb.float().numpy().copy()
+    for m in (0.0, 0.9):
+        a = run_oracle(w0, [gbits, gbits], 0.001, m=m)
+        b = run_oracle(w0, [gw, gw], 0.001, m=m)
+        assert np.array_equal(bits(a.w), bits(b.w))
+
+
+# ------------------------------------------------ bf16 conversions
+
+def test_bf16_widening_exhaustive():
+    """All 65,536 bf16 patterns widen to the fp32 value torch gives them."""
+    torch = pytest.importorskip("torch")
+    pats = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    ref = torch.from_numpy(pats.view(np.int16)).view(torch.bfloat16).float().numpy()
+    got = orc.bf16_to_f32(pats)
+    assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
+
+
+def test_bf16_rne_against_torch():
+    """fp32 -> bf16 round-to-nearest-even equals torch's cast on random
+    values, exact ties (both parities), values that carry into the exponent,
+    the largest finite values, subnormals and signed zeros."""
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(9)
+    special = np.array([
+        0x3F808000,  # 1 + 2^-8: tie, last kept bit even -> down
+        0x3F818000,  # tie, last kept bit odd -> up
+        0x3F808001, 0x3F807FFF, 0x3FFFFFFF, 0x3FFF8000,  # above/below half; carry
+        0x7F7FFFFF, 0x7F7F8000, 0x7F7F7FFF,              # max finite: to inf / stay
+        0xFF7FFFFF, 0x00000001, 0x00008000, 0x00018000, 0x807FFFFF,
+        0x00000000, 0x80000000, 0x7F800000, 0xFF800000,
+    ], np.uint32)
+    r = rng.integers(0, 2 ** 32, 200000, dtype=np.uint64).astype(np.uint32)
+    r = r[(r & 0x7F800000) != 0x7F800000]     # no NaN/inf in the random part
+    x = np.concatenate([special, r]).view(np.float32)
+    ref = torch.from_numpy(x.copy()).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    got = orc.f32_to_bf16(x)
+    assert np.array_equal(got, ref)
+
+
+def test_bf16_rne_ties_by_hand():
+    """Hand-derived ties-to-even cases (tests/golden/bf16_rne.txt)."""
+    import os
+    path = os.path.join(golden_script.GOLDEN, "bf16_rne.txt")
+    rows = []
+    for line in open(path):
+        line = line.split("#", 1)[0].strip()
+        if line:
+            a, b = line.split()
+            rows.append((int(a, 16), int(b, 16)))
+    x = np.array([a for a, _ in rows], np.uint32).view(np.float32)
+    got = orc.f32_to_bf16(x)
+    assert [int(v) for v in got] == [b for _, b in rows]
+
+
+def test_bf16_nan_stays_quiet_nan():
+    x = np.array([0x7F800001, 0xFFC00000, 0x7FBFFFFF], np.uint32).view(np.float32)
+    got = orc.f32_to_bf16(x).astype(np.uint32)
+    assert np.all((got & 0x7F80) == 0x7F80) and np.all(got & 0x0040)
+    assert list(got >> 15) == [0, 1, 0]
+
+
+# ------------------------------------------------ pulls
+
+def test_pull_replicas():
+    """A fp32 pull is w itself; a bf16 pull is RNE(w). With skip on or off the
+    replica bits are the same (skipping is an optimisation only)."""
+    rng = np.random.default_rng(10)
+    w0 = rng.uniform(-0.05, 0.05, 3000).astype(np.float32)
+    g = rand_f32(rng, 3000, 0.01)
+    torch = pytest.importorskip("torch")
+    for skip in (True, False):
+        s = orc.OracleServer(w0, 0.01, 0.0, depth=4, pull_skip=skip)
+        s.push(0, g)
+        s.apply_pending()
+        assert s.pull(0, "a", orc.F32)
+        assert s.pull(0, "b", orc.BF16)
+        assert s.pull(0, "b", orc.BF16) is (not skip)
+        assert np.array_equal(bits(s.replicas["a"]), bits(s.w))
+        ref = torch.from_numpy(s.w.copy()).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+        assert np.array_equal(s.replicas["b"], ref)
+
+
+# ------------------------------------------------ protocol
+
+def test_golden_staleness_script():
+    """The hand-worked schedule of tests/golden/staleness_k2.txt."""
+    depth, ops, expect = golden_script.load("staleness_k2.txt")
+    g = np.full(4, 0.5, np.float32)
+    s = orc.OracleServer(np.zeros(4, np.float32), 2.0 ** -4, 0.0, depth=depth)
+    rejected = 0
+    for op, l, outcome in ops:
+        if op == "push":
+            rc = s.push(l, g)
+            assert rc == {"ok": orc.OK, "full": orc.EFULL}[outcome]
+            rejected += rc == orc.EFULL
+        elif op == "apply":
+            s.apply_pending()
+        elif op == "pull":
+            assert s.pull(l, ("dst", l), orc.F32) == (outcome == "pulled")
+        assert 0 <= s.pending() <= depth          # Lemma 1
+    assert s.staleness == expect["staleness"]
+    assert s.applied_order == expect["order"]
+    assert s.ts == expect["ts"][0]
+    assert (s.pulls, s.pulls_skipped, rejected) == (expect["pulls"], expect["skipped"], expect["rejected"])
+    # 7 accepted pushes of 0.5 at lr 1/16: each step subtracts exactly 1/32
+    assert np.all(s.w == -7 / 32)
+
+
+def test_queue_exactly_once_fifo_random():
+    """Theorem 2: over a random push/apply interleaving with a bounded queue,
+    every accepted gradient is applied exactly once, in push order, a full
+    queue refuses without changing state, and ts counts accepted pushes."""
+    rng = np.random.default_rng(11)
+    for depth in (1, 2, 5, 64):
+        s = orc.OracleServer(np.zeros(1, np.float32), 1.0, 0.0, depth=depth)
+        accepted = []
+        for step in range(600):
+            if rng.random() < 0.7:
+                tag = np.array([float(step)], np.float32)
+                before = (s.pending(), s.ts)
+                rc = s.push(int(rng.integers(0, 5)), tag)
+                if rc == orc.OK:
+                    accepted.append(step)
+                else:
+                    assert rc == orc.EFULL and before == (s.pending(), s.ts) and before[0] == depth
+            else:
+                order = [int(g[0]) for _, g, _ in s.queue]
+                n_before = len(s.applied_order)
+                s.apply_pending()
+                assert len(s.applied_order) - n_before == len(order)
+            assert 0 <= s.pending() <= depth
+        s.apply_pending()
+        assert s.ts == len(accepted)
+        # w = -sum(tags) exactly (small integers), and every tag was used once
+        assert s.w[0] == -float(sum(accepted))
+
+
+def test_set_depth_rules():
+    s = orc.OracleServer(np.zeros(2, np.float32), 0.1, depth=4)
+    assert s.set_depth(0) == orc.EINVAL and s.set_depth(65) == orc.EINVAL
+    for _ in range(3):
+        s.push(0, np.zeros(2, np.float32))
+    assert s.set_depth(2) == orc.ESTATE
+    assert s.set_depth(3) == orc.OK
