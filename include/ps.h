@@ -1,0 +1,184 @@
+/*
+ * ps.h -- C ABI of an ASGD parameter server held in one gfx950 GPU's memory.
+ *
+ * Model (GaDei, arXiv 1611.06213):
+ *   - Learners push gradients to the server and pull weights from it; they
+ *     never talk to each other (Sec. 2.1, Fig. "design_base"; Sec. 4.1).
+ *   - Asynchronous SGD: the server applies every gradient it receives, in the
+ *     order received, each as one step theta <- theta - alpha * grad
+ *     (Eq. "asgd" with the step of Eq. "gd", Sec. 2.1).
+ *   - The server's weights carry a scalar timestamp that grows by one per
+ *     applied gradient; the staleness of a gradient is the server timestamp
+ *     when it is applied minus the timestamp of the weights its learner held
+ *     (Sec. 2.1).
+ *   - Gradients wait in a producer-consumer queue with a fixed number of
+ *     slots; each is applied exactly once and a full queue refuses the
+ *     producer (Sec. 4.1; Lemma 1 and Theorem 2, Sec. 4.2).
+ *   - A learner whose copy already carries the server's timestamp skips its
+ *     pull (Sec. 4.1).
+ *
+ * Design on one GPU:
+ *   - The library owns the fp32 weights w[n] (and, with momentum, the fp32
+ *     velocity v[n]) in device memory.
+ *   - ps_push only records a descriptor; it copies nothing. The gradient
+ *     stays in the caller's device buffer until the apply that consumes it.
+ *   - ps_apply_pending folds all pending gradients into w in one pass over
+ *     memory: for each coordinate, the K gradients are applied one after the
+ *     other, oldest first, with the same roundings as K separate steps.
+ *   - All device work is enqueued, asynchronously, on one HIP stream in call
+ *     order (the stream set by ps_set_stream; the null stream by default).
+ *     A pull therefore sees every gradient applied by earlier calls and no
+ *     gradient still pending.
+ *
+ * Arithmetic per coordinate and per applied gradient g (binary32, each
+ * operation rounded to nearest even, no fused multiply-add):
+ *   momentum == 0:  p = lr*g;  w = w - p
+ *   momentum != 0:  t = m*v;  v = t + g;  p = lr*v;  w = w - p   (v starts +0)
+ * A bf16 gradient is widened exactly to fp32 first. A bf16 pull writes w
+ * rounded to nearest even bf16.
+ *
+ * Threading: calls on one handle must not overlap (one thread at a time).
+ * Distinct handles are independent.
+ *
+ * Pointers named "device" must point to device memory (hipMalloc or torch
+ * CUDA tensors) on the device that was current at ps_create. Any alignment is
+ * accepted; 16-byte-aligned fp32 buffers and 8-byte-aligned bf16 buffers take
+ * the vector path, others a scalar path with identical results.
+ *
+ * Status codes: every int-returning call returns PS_OK (0) or a negative
+ * PS_E* code; ps_last_error() then describes the failure (per thread).
+ */
+#ifndef GADEI_PS_H
+#define GADEI_PS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ps_server ps_server;
+
+enum {
+    PS_OK = 0,
+    PS_EINVAL = -1,  /* bad handle, id, pointer, dtype or size              */
+    PS_EFULL = -2,   /* push on a full queue; nothing was enqueued          */
+    PS_ENOMEM = -3,  /* device or host allocation failed                    */
+    PS_EHIP = -4,    /* a HIP runtime call or kernel launch failed          */
+    PS_ESTATE = -5   /* call not allowed in the current state               */
+};
+
+enum { PS_F32 = 0, PS_BF16 = 1 };
+
+#define PS_MAX_QUEUE_DEPTH 64   /* K: gradients folded by one apply         */
+#define PS_MAX_REPLICAS 64      /* replica buffers written by one pull call */
+#define PS_MAX_LEARNERS 65536   /* learner ids are 0 .. PS_MAX_LEARNERS-1   */
+#define PS_STALENESS_BINS 64    /* histogram bins; the last one is ">= 63"  */
+
+typedef struct ps_stats {
+    uint64_t timestamp;        /* applied gradients so far (Sec. 2.1)       */
+    uint64_t pushes_accepted;
+    uint64_t pushes_rejected;  /* PS_EFULL returns                          */
+    uint64_t pushes_applied;
+    uint64_t applies;          /* apply calls that launched device work     */
+    uint64_t pulls;            /* replica refreshes requested               */
+    uint64_t pulls_skipped;    /* ... of which skipped as already current   */
+    uint64_t staleness_max;
+    uint64_t staleness_sum;
+    uint64_t staleness_hist[PS_STALENESS_BINS];
+} ps_stats;
+
+/* Create a server for n_params fp32 weights with learning rate lr (alpha in
+ * Eq. "gd") and heavy-ball momentum (0 disables it and allocates no v).
+ * Allocates w (and v) on the current device; w starts at zero, v at +0,
+ * timestamp 0, queue depth PS_MAX_QUEUE_DEPTH / 2 = 32, pull skipping on.
+ * Returns NULL on failure (n_params == 0, lr or momentum not finite,
+ * allocation failure); see ps_last_error(). */
+ps_server *ps_create(size_t n_params, float lr, float momentum);
+
+/* Wait for the server's stream, then free w and v and the handle. NULL is a
+ * no-op. Pending (unapplied) gradients are dropped. */
+void ps_destroy(ps_server *ps);
+
+/* Push the fp32 gradient grad[n_params] (device pointer) of learner
+ * learner_id (Sec. 2.1, Eq. "asgd"). Records it at the tail of the FIFO; no
+ * data moves. The buffer is borrowed: the caller must not write or free it
+ * until the apply that consumes it has completed on the server's stream.
+ * Returns PS_EFULL, with nothing enqueued, when the queue holds its depth of
+ * gradients (Sec. 4.1, Theorem 2): apply, then push again. */
+int ps_push(ps_server *ps, int learner_id, const void *grad);
+
+/* ps_push for a gradient of the given dtype (PS_F32 or PS_BF16; a bf16
+ * gradient holds n_params 16-bit values). */
+int ps_push_dtype(ps_server *ps, int learner_id, const void *grad, int dtype);
+
+/* Apply every pending gradient, oldest first, each as one step of Eq.
+ * "asgd", then empty the queue. Enqueues one kernel per run of equal-dtype
+ * gradients (one in the usual case) on the server's stream; returns without
+ * waiting. The timestamp grows by the number applied; staleness of each is
+ * recorded (ps_last_staleness, ps_get_stats). An empty queue is a no-op. */
+int ps_apply_pending(ps_server *ps);
+
+/* Pull: write the current weights into the learner's replica buffer
+ * dst[n_params] (device, fp32). Asynchronous on the server's stream; the copy
+ * sees every apply issued before it. Skipped (no device work) when the same
+ * learner last pulled into the same buffer with the same dtype at the current
+ * timestamp (Sec. 4.1). dst must not overlap w or a pending gradient. */
+int ps_pull(ps_server *ps, int learner_id, void *dst);
+
+/* Pull for n learners at once: learner_ids[i] into dsts[i], all in dst_dtype
+ * (PS_F32, or PS_BF16 = round to nearest even). One fan-out kernel reads w
+ * once and writes every replica that is not skipped. 0 <= n <=
+ * PS_MAX_REPLICAS; the buffers that are written must be distinct. */
+int ps_pull_many(ps_server *ps, int n, const int *learner_ids, void *const *dsts, int dst_dtype);
+
+/* ps_apply_pending followed by ps_pull_many, fused: the replicas are written
+ * from the same pass that updates w, so w is not read again. The result is
+ * identical to the two calls in sequence. */
+int ps_apply_pull(ps_server *ps, int n, const int *learner_ids, void *const *dsts, int dst_dtype);
+
+/* Use hip_stream (a hipStream_t; NULL = the null stream) for all later device
+ * work. The caller orders it against work already on the previous stream. */
+int ps_set_stream(ps_server *ps, void *hip_stream);
+
+/* Queue depth K, 1..PS_MAX_QUEUE_DEPTH. PS_ESTATE if more gradients are
+ * pending than the new depth. */
+int ps_set_queue_depth(ps_server *ps, int depth);
+
+/* Enable (1) or disable (0) skipping of pulls that are already current. */
+int ps_set_pull_skip(ps_server *ps, int enabled);
+
+/* Reset the server to start from src[n_params] (device, fp32): w := src,
+ * v := +0, timestamp := 0, every learner holds timestamp 0, pull history and
+ * statistics cleared. PS_ESTATE if gradients are pending. Asynchronous. */
+int ps_set_weights(ps_server *ps, const float *src);
+
+/* Device pointers to w[n_params] and v[n_params] (NULL without momentum).
+ * Owned by the server; valid until ps_destroy. Reading them is ordered by the
+ * server's stream. */
+const float *ps_weights(const ps_server *ps);
+const float *ps_velocity(const ps_server *ps);
+
+size_t ps_num_params(const ps_server *ps);
+uint64_t ps_timestamp(const ps_server *ps);
+int ps_pending(const ps_server *ps);
+
+/* Staleness of each gradient applied by the most recent apply call, in the
+ * order applied. Writes min(count, cap) values to out and returns count (or
+ * a negative status). */
+int ps_last_staleness(const ps_server *ps, int64_t *out, int cap);
+
+/* Block until all work enqueued by the server has completed. */
+int ps_sync(ps_server *ps);
+
+int ps_get_stats(const ps_server *ps, ps_stats *out);
+
+/* Message for the last failed call on this thread ("" if none). */
+const char *ps_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GADEI_PS_H */

@@ -1,0 +1,351 @@
+"""ctypes binding of libgadeips.so (the C ABI in include/ps.h).
+
+Module-level functions carry the C names and return the C status codes;
+they only marshal arguments. `ParameterServer` wraps a handle for torch
+device tensors and raises `PSError` on failure. Every computation runs in the
+library's HIP kernels; if the library is not built, loading raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+PS_OK = 0
+PS_EINVAL = -1
+PS_EFULL = -2
+PS_ENOMEM = -3
+PS_EHIP = -4
+PS_ESTATE = -5
+
+PS_F32 = 0
+PS_BF16 = 1
+
+PS_MAX_QUEUE_DEPTH = 64
+PS_MAX_REPLICAS = 64
+PS_MAX_LEARNERS = 65536
+PS_STALENESS_BINS = 64
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libgadeips.so")
+
+_u64 = ctypes.c_uint64
+
+
+class ps_stats(ctypes.Structure):
+    _fields_ = [
+        ("timestamp", _u64), ("pushes_accepted", _u64), ("pushes_rejected", _u64),
+        ("pushes_applied", _u64), ("applies", _u64), ("pulls", _u64), ("pulls_skipped", _u64),
+        ("staleness_max", _u64), ("staleness_sum", _u64),
+        ("staleness_hist", _u64 * PS_STALENESS_BINS),
+    ]
+
+
+# name -> (restype, argtypes); the same list the header declares
+_VP = ctypes.c_void_p
+_SIGS = {
+    "ps_create": (_VP, [ctypes.c_size_t, ctypes.c_float, ctypes.c_float]),
+    "ps_destroy": (None, [_VP]),
+    "ps_push": (ctypes.c_int, [_VP, ctypes.c_int, _VP]),
+    "ps_push_dtype": (ctypes.c_int, [_VP, ctypes.c_int, _VP, ctypes.c_int]),
+    "ps_apply_pending": (ctypes.c_int, [_VP]),
+    "ps_pull": (ctypes.c_int, [_VP, ctypes.c_int, _VP]),
+    "ps_pull_many": (ctypes.c_int, [_VP, ctypes.c_int, ctypes.POINTER(ctypes.c_int),
+                                    ctypes.POINTER(_VP), ctypes.c_int]),
+    "ps_apply_pull": (ctypes.c_int, [_VP, ctypes.c_int, ctypes.POINTER(ctypes.c_int),
+                                     ctypes.POINTER(_VP), ctypes.c_int]),
+    "ps_set_stream": (ctypes.c_int, [_VP, _VP]),
+    "ps_set_queue_depth": (ctypes.c_int, [_VP, ctypes.c_int]),
+    "ps_set_pull_skip": (ctypes.c_int, [_VP, ctypes.c_int]),
+    "ps_set_weights": (ctypes.c_int, [_VP, _VP]),
+    "ps_weights": (_VP, [_VP]),
+    "ps_velocity": (_VP, [_VP]),
+    "ps_num_params": (ctypes.c_size_t, [_VP]),
+    "ps_timestamp": (_u64, [_VP]),
+    "ps_pending": (ctypes.c_int, [_VP]),
+    "ps_last_staleness": (ctypes.c_int, [_VP, ctypes.POINTER(ctypes.c_int64), ctypes.c_int]),
+    "ps_sync": (ctypes.c_int, [_VP]),
+    "ps_get_stats": (ctypes.c_int, [_VP, ctypes.POINTER(ps_stats)]),
+    "ps_last_error": (ctypes.c_char_p, []),
+}
+
+_lib = None
+
+
+def load_library(path: Optional[str] = None):
+    """Load the built library (once). Raises if it is missing."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    p = path or LIB_PATH
+    if not os.path.exists(p):
+        raise RuntimeError(
+            f"{p} is not built: run `python -c 'import __graft_entry__ as g; g.build()'` "
+            "(the parameter server has no CPU fallback)")
+    L = ctypes.CDLL(p)
+    for name, (res, args) in _SIGS.items():
+        f = getattr(L, name)
+        f.restype = res
+        f.argtypes = args
+    if path is None:
+        _lib = L
+    return L
+
+
+class PSError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"[{code}] {msg}")
+        self.code = code
+
+
+def _ints(xs: Sequence[int]):
+    return (ctypes.c_int * max(1, len(xs)))(*xs)
+
+
+def _ptrs(xs: Sequence[int]):
+    return (_VP * max(1, len(xs)))(*xs)
+
+
+# ------------------------------------------------------------ C-named calls
+
+def ps_last_error() -> str:
+    return load_library().ps_last_error().decode()
+
+
+def ps_create(n_params: int, lr: float, momentum: float) -> int:
+    h = load_library().ps_create(n_params, lr, momentum)
+    if not h:
+        raise PSError(PS_EINVAL, ps_last_error())
+    return h
+
+
+def ps_destroy(h: int) -> None:
+    load_library().ps_destroy(h)
+
+
+def ps_push(h: int, learner_id: int, grad_ptr: int) -> int:
+    return load_library().ps_push(h, learner_id, grad_ptr)
+
+
+def ps_push_dtype(h: int, learner_id: int, grad_ptr: int, dtype: int) -> int:
+    return load_library().ps_push_dtype(h, learner_id, grad_ptr, dtype)
+
+
+def ps_apply_pending(h: int) -> int:
+    return load_library().ps_apply_pending(h)
+
+
+def ps_pull(h: int, learner_id: int, dst_ptr: int) -> int:
+    return load_library().ps_pull(h, learner_id, dst_ptr)
+
+
+def ps_pull_many(h: int, learner_ids: Sequence[int], dst_ptrs: Sequence[int], dst_dtype: int) -> int:
+    return load_library().ps_pull_many(h, len(learner_ids), _ints(learner_ids), _ptrs(dst_ptrs),
+                                       dst_dtype)
+
+
+def ps_apply_pull(h: int, learner_ids: Sequence[int], dst_ptrs: Sequence[int], dst_dtype: int) -> int:
+    return load_library().ps_apply_pull(h, len(learner_ids), _ints(learner_ids), _ptrs(dst_ptrs),
+                                        dst_dtype)
+
+
+def ps_set_stream(h: int, stream_ptr: int) -> int:
+    return load_library().ps_set_stream(h, stream_ptr)
+
+
+def ps_set_queue_depth(h: int, depth: int) -> int:
+    return load_library().ps_set_queue_depth(h, depth)
+
+
+def ps_set_pull_skip(h: int, enabled: bool) -> int:
+    return load_library().ps_set_pull_skip(h, 1 if enabled else 0)
+
+
+def ps_set_weights(h: int, src_ptr: int) -> int:
+    return load_library().ps_set_weights(h, src_ptr)
+
+
+def ps_weights(h: int) -> int:
+    return load_library().ps_weights(h) or 0
+
+
+def ps_velocity(h: int) -> int:
+    return load_library().ps_velocity(h) or 0
+
+
+def ps_num_params(h: int) -> int:
+    return load_library().ps_num_params(h)
+
+
+def ps_timestamp(h: int) -> int:
+    return load_library().ps_timestamp(h)
+
+
+def ps_pending(h: int) -> int:
+    return load_library().ps_pending(h)
+
+
+def ps_last_staleness(h: int, cap: int = PS_MAX_QUEUE_DEPTH):
+    out = (ctypes.c_int64 * cap)()
+    n = load_library().ps_last_staleness(h, out, cap)
+    if n < 0:
+        return n
+    return [int(out[i]) for i in range(min(n, cap))]
+
+
+def ps_sync(h: int) -> int:
+    return load_library().ps_sync(h)
+
+
+def ps_get_stats(h: int):
+    s = ps_stats()
+    rc = load_library().ps_get_stats(h, ctypes.byref(s))
+    return rc if rc < 0 else s
+
+
+# ------------------------------------------------------------ tensor wrapper
+
+def _dtype_code(t) -> int:
+    import torch
+    if t.dtype == torch.float32:
+        return PS_F32
+    if t.dtype == torch.bfloat16:
+        return PS_BF16
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+class ParameterServer:
+    """A server handle for torch device tensors.
+
+    Pushed gradients are borrowed: the tensor is kept referenced until the
+    apply that consumes it has been enqueued, and the caller must not write it
+    before that apply has run on the server's stream."""
+
+    def __init__(self, n_params: int, lr: float, momentum: float = 0.0,
+                 queue_depth: Optional[int] = None, stream=None):
+        self.h = ps_create(n_params, lr, momentum)
+        self.n = n_params
+        self._pending = []
+        if queue_depth is not None:
+            self._check(ps_set_queue_depth(self.h, queue_depth), "set_queue_depth")
+        if stream is not None:
+            self.set_stream(stream)
+
+    def _check(self, rc: int, what: str) -> int:
+        if rc < 0:
+            raise PSError(rc, f"{what}: {ps_last_error()}")
+        return rc
+
+    def _tensor(self, t, what: str):
+        if not t.is_cuda or not t.is_contiguous() or t.numel() != self.n:
+            raise ValueError(f"{what}: need a contiguous device tensor of {self.n} elements")
+        return t.data_ptr()
+
+    def close(self):
+        if self.h:
+            ps_destroy(self.h)
+            self.h = 0
+            self._pending = []
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def set_stream(self, stream) -> None:
+        ptr = stream if isinstance(stream, int) else stream.cuda_stream
+        self._check(ps_set_stream(self.h, ptr), "set_stream")
+
+    def set_weights(self, w0) -> None:
+        self._check(ps_set_weights(self.h, self._tensor(w0, "set_weights")), "set_weights")
+
+    def set_pull_skip(self, enabled: bool) -> None:
+        self._check(ps_set_pull_skip(self.h, enabled), "set_pull_skip")
+
+    def set_queue_depth(self, depth: int) -> None:
+        self._check(ps_set_queue_depth(self.h, depth), "set_queue_depth")
+
+    def push(self, learner: int, grad) -> bool:
+        """Enqueue; False when the queue is full (nothing enqueued)."""
+        rc = ps_push_dtype(self.h, learner, self._tensor(grad, "push"), _dtype_code(grad))
+        if rc == PS_EFULL:
+            return False
+        self._check(rc, "push")
+        self._pending.append(grad)
+        return True
+
+    def apply_pending(self) -> None:
+        self._check(ps_apply_pending(self.h), "apply_pending")
+        self._pending = []
+
+    def pull(self, learner: int, dst) -> None:
+        self.pull_many([learner], [dst])
+
+    def pull_many(self, learners: Sequence[int], dsts) -> None:
+        if len(dsts) != len(learners):
+            raise ValueError("one destination per learner")
+        dt = _dtype_code(dsts[0]) if len(dsts) else PS_F32
+        ptrs = [self._tensor(d, "pull") for d in dsts]
+        self._check(ps_pull_many(self.h, list(learners), ptrs, dt), "pull_many")
+
+    def apply_pull(self, learners: Sequence[int], dsts) -> None:
+        if len(dsts) != len(learners):
+            raise ValueError("one destination per learner")
+        dt = _dtype_code(dsts[0]) if len(dsts) else PS_F32
+        ptrs = [self._tensor(d, "apply_pull") for d in dsts]
+        self._check(ps_apply_pull(self.h, list(learners), ptrs, dt), "apply_pull")
+        self._pending = []
+
+    def sync(self) -> None:
+        self._check(ps_sync(self.h), "sync")
+
+    @property
+    def timestamp(self) -> int:
+        return ps_timestamp(self.h)
+
+    @property
+    def pending(self) -> int:
+        return ps_pending(self.h)
+
+    def last_staleness(self):
+        return ps_last_staleness(self.h)
+
+    def stats(self) -> ps_stats:
+        s = ps_get_stats(self.h)
+        if isinstance(s, int):
+            self._check(s, "get_stats")
+        return s
+
+    def weights_copy(self):
+        """A new device tensor holding w (waits for the server's stream)."""
+        return self._copy(ps_weights(self.h))
+
+    def velocity_copy(self):
+        p = ps_velocity(self.h)
+        return self._copy(p) if p else None
+
+    def _copy(self, ptr: int):
+        import torch
+        self.sync()
+        out = torch.empty(self.n, dtype=torch.float32, device="cuda")
+        stream = torch.cuda.current_stream().cuda_stream
+        rc = _hip().hipMemcpyAsync(ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ptr),
+                                   ctypes.c_size_t(4 * self.n), 3,   # device to device
+                                   ctypes.c_void_p(stream))
+        if rc != 0:
+            raise PSError(PS_EHIP, f"hipMemcpyAsync failed ({rc})")
+        return out
+
+
+_hip_rt = None
+
+
+def _hip():
+    """The HIP runtime the library links (for the plain copy above)."""
+    global _hip_rt
+    if _hip_rt is None:
+        _hip_rt = ctypes.CDLL("libamdhip64.so")
+        _hip_rt.hipMemcpyAsync.restype = ctypes.c_int
+        _hip_rt.hipMemcpyAsync.argtypes = [_VP, _VP, ctypes.c_size_t, ctypes.c_int, _VP]
+    return _hip_rt

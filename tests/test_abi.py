@@ -1,0 +1,70 @@
+"""The C ABI library loads on a machine without a GPU and exports every
+function include/ps.h declares; argument validation that needs no device
+answers with the documented status codes."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_1611_06213_amd import ps
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "ps.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ps_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(ps.LIB_PATH):
+        pytest.fail("libgadeips.so is not built (run __graft_entry__.build())")
+    return ps.load_library()
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = declared_functions()
+    assert "ps_create" in names and "ps_apply_pending" in names and len(names) >= 20
+    for n in names:
+        assert hasattr(lib, n), n
+    # and the binding covers the same list, under the same names
+    assert set(names) == set(ps._SIGS)
+    for n in names:
+        assert callable(getattr(ps, n)), n
+
+
+def test_header_constants_match_binding():
+    text = open(os.path.join(ROOT, "include", "ps.h")).read()
+    for name in ("PS_OK", "PS_EINVAL", "PS_EFULL", "PS_ENOMEM", "PS_EHIP", "PS_ESTATE",
+                 "PS_F32", "PS_BF16"):
+        m = re.search(rf"\b{name}\s*=\s*(-?\d+)", text)
+        assert m and int(m.group(1)) == getattr(ps, name), name
+    for name in ("PS_MAX_QUEUE_DEPTH", "PS_MAX_REPLICAS", "PS_MAX_LEARNERS", "PS_STALENESS_BINS"):
+        m = re.search(rf"#define {name} (\d+)", text)
+        assert m and int(m.group(1)) == getattr(ps, name), name
+    assert ctypes.sizeof(ps.ps_stats) == 8 * (9 + ps.PS_STALENESS_BINS)
+
+
+def test_validation_without_device(lib):
+    assert lib.ps_create(0, 0.1, 0.0) is None
+    assert "positive" in ps.ps_last_error()
+    assert lib.ps_create(10, float("nan"), 0.0) is None
+    assert lib.ps_create(10, 0.1, float("inf")) is None
+    assert lib.ps_push(None, 0, None) == ps.PS_EINVAL
+    assert lib.ps_apply_pending(None) == ps.PS_EINVAL
+    assert lib.ps_pull(None, 0, None) == ps.PS_EINVAL
+    assert ps.ps_pull_many(None, [0], [1], ps.PS_F32) == ps.PS_EINVAL
+    assert lib.ps_set_queue_depth(None, 4) == ps.PS_EINVAL
+    assert lib.ps_sync(None) == ps.PS_EINVAL
+    assert lib.ps_pending(None) == ps.PS_EINVAL
+    assert lib.ps_timestamp(None) == 0 and lib.ps_num_params(None) == 0
+    assert not lib.ps_weights(None)
+    lib.ps_destroy(None)   # no-op
+
+
+def test_binding_refuses_missing_library(tmp_path):
+    with pytest.raises(RuntimeError, match="not built"):
+        ps.load_library(str(tmp_path / "missing.so"))

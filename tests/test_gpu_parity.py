@@ -1,0 +1,372 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Bar: bitwise for fp32 weights, velocities and replicas and for bf16 replica
+bits (the library is built without contraction, like the oracle); exact
+integers for timestamps, staleness and counters. The bf16-gradient variant is
+also checked against the oracle fed the original fp32 gradients, within the
+1e-3 relative bound (R12 metric: max|a-b| / max(|b|, RMS(w0))).
+"""
+import dataclasses
+import os
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import server as orc
+from paper_1611_06213_amd import ps
+from paper_1611_06213_amd import workloads as wl
+from tests import golden_script, parity
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    ps.load_library()
+    return torch
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def free(torch):
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+# ---------------------------------------------------------------- workloads
+
+SMALL_N = 3 * 65536 + 7   # several 256-lane tiles and a ragged tail
+
+
+@pytest.mark.parametrize("fused", [False, True], ids=["separate", "fused"])
+@pytest.mark.parametrize("name", list(wl.CONFIGS))
+def test_workload_small_full_oracle(torch, name, fused):
+    """Each workload's whole schedule at a reduced parameter count; the
+    oracle covers every coordinate."""
+    cfg = wl.CONFIGS[name].scaled(SMALL_N, pool=min(wl.CONFIGS[name].pool, 64))
+    say(f"[small] {name} n={cfg.n} fused={fused}")
+    ev = wl.schedule(cfg)
+    pool = wl.make_pool(cfg, "cuda")
+    w0 = wl.make_w0(cfg, "cuda")
+    ranges = [(0, cfg.n)]
+    g = parity.gpu_replay(cfg, ev, pool, w0, ranges, fused=fused)
+    ps_, w0s = parity.host_inputs(cfg, pool, w0, ranges)
+    o = parity.oracle_replay(cfg, ev, ps_, w0s, ranges)
+    assert parity.compare(g, o, ranges) == []
+    del pool
+    free(torch)
+
+
+def test_mixed_variable_k_drain_each_burst(torch):
+    """Mixed workload, parity variant: apply at every burst end (K from 1
+    to 32 varies apply to apply)."""
+    cfg = dataclasses.replace(wl.CONFIGS["mixed"].scaled(SMALL_N), drain_each_burst=True)
+    ev = wl.schedule(cfg)
+    pool = wl.make_pool(cfg, "cuda")
+    w0 = wl.make_w0(cfg, "cuda")
+    ranges = [(0, cfg.n)]
+    for fused in (False, True):
+        g = parity.gpu_replay(cfg, ev, pool, w0, ranges, fused=fused)
+        ps_, w0s = parity.host_inputs(cfg, pool, w0, ranges)
+        o = parity.oracle_replay(cfg, ev, ps_, w0s, ranges)
+        assert parity.compare(g, o, ranges) == []
+    free(torch)
+
+
+def _full_ranges(cfg):
+    r = wl.sample_ranges(cfg.n, 4096, 6, seed=cfg.index)
+    for name, off, numel in wl.tensor_offsets(cfg)[-4:]:
+        lo = max(0, off - 2048)
+        r.append((lo, min(cfg.n, lo + 4096)))
+    return r
+
+
+@pytest.mark.parametrize("fused", [True, False], ids=["fused", "separate"])
+@pytest.mark.parametrize("name", list(wl.CONFIGS))
+def test_workload_full_size_sampled(torch, name, fused):
+    """Each workload at its full size, in the launch configuration the
+    benchmark uses; the oracle checks sampled coordinate ranges (head, tail
+    with the ragged end, seeded interior blocks, tensor boundaries) of the
+    weights, velocity and every replica after every pull event."""
+    cfg = wl.CONFIGS[name]
+    say(f"[full] {name} n={cfg.n} fused={fused}")
+    ev = wl.schedule(cfg)
+    pool = wl.make_pool(cfg, "cuda")
+    w0 = wl.make_w0(cfg, "cuda")
+    ranges = _full_ranges(cfg)
+    g = parity.gpu_replay(cfg, ev, pool, w0, ranges, fused=fused)
+    ps_, w0s = parity.host_inputs(cfg, pool, w0, ranges)
+    del pool
+    free(torch)
+    o = parity.oracle_replay(cfg, ev, ps_, w0s, ranges)
+    assert parity.compare(g, o, ranges) == []
+
+
+def test_mixed_bf16_within_1e3_of_fp32_gradients(torch):
+    """The bf16-gradient run stays within 1e-3 (relative to max(|w|, RMS(w0)))
+    of the oracle fed the original fp32 gradients; its bf16 replicas are
+    within one bf16 rounding of that oracle's weights."""
+    cfg = wl.CONFIGS["mixed"]
+    ev = wl.schedule(cfg)
+    pool = wl.make_pool(cfg, "cuda")
+    w0 = wl.make_w0(cfg, "cuda")
+    ranges = _full_ranges(cfg)
+    g = parity.gpu_replay(cfg, ev, pool, w0, ranges, fused=True)
+    del pool
+    f32_slices = [[None] * cfg.pool for _ in ranges]
+    for b in range(cfg.pool):
+        x = wl.make_grad_f32(cfg, b, "cuda")
+        for r, (lo, hi) in enumerate(ranges):
+            f32_slices[r][b] = parity.np_bits(x[lo:hi])
+        del x
+    w0s = [parity.np_bits(w0[lo:hi]) for lo, hi in ranges]
+    free(torch)
+    o = parity.oracle_replay(cfg, ev, f32_slices, w0s, ranges)
+    tau = float(np.sqrt(np.mean(np.concatenate(w0s).astype(np.float64) ** 2)))
+    worst = 0.0
+    for a, b in zip(g["w"], o["w"]):
+        err = np.abs(a.astype(np.float64) - b) / np.maximum(np.abs(b), tau)
+        worst = max(worst, float(err.max()))
+    say(f"[bf16 vs fp32 gradients] worst relative error {worst:.3e}")
+    assert worst <= 1e-3
+    # final replicas: bf16 of the GPU's w, within one bf16 ulp of the fp32-gradient w
+    last = g["snaps"][-1]
+    for l, slices in last.items():
+        for r, rep in enumerate(slices):
+            rep32 = orc.bf16_to_f32(rep).astype(np.float64)
+            ref = o["w"][r].astype(np.float64)
+            assert np.all(np.abs(rep32 - ref) <= np.abs(ref) * 2.0 ** -8 + tau * 1e-3)
+
+
+# ---------------------------------------------------------------- edges
+
+def _run_edge(torch, n, k, momentum, gdt, pdt, offset_g=0, offset_d=0, seed=0, lr=0.01):
+    """Push k gradients (optionally at element offsets that break vector
+    alignment), apply+pull into two replicas, pull into a third, compare."""
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(1000 + seed)
+    gtd = torch.bfloat16 if gdt == ps.PS_BF16 else torch.float32
+    ptd = torch.bfloat16 if pdt == ps.PS_BF16 else torch.float32
+    w0 = ((torch.rand(n, generator=gen, device="cuda") - 0.5) * 0.1).contiguous()
+    big = (torch.randn(k, n + 8, generator=gen, device="cuda") * 1e-2).to(gtd)
+    grads = [big[j, offset_g:offset_g + n] for j in range(k)]
+    dbig = torch.zeros(3, n + 8, dtype=ptd, device="cuda")
+    dsts = [dbig[r, offset_d:offset_d + n] for r in range(3)]
+    srv = ps.ParameterServer(n, lr, momentum, queue_depth=max(k, 1))
+    srv.set_weights(w0)
+    for j, gj in enumerate(grads):
+        assert srv.push(j % 5, gj)
+    srv.apply_pull([0, 1], dsts[:2])
+    srv.pull(2, dsts[2])
+    w = parity.np_bits(srv.weights_copy())
+    v = srv.velocity_copy()
+    reps = [parity.np_bits(d) for d in dsts]
+    st = srv.last_staleness()
+    srv.close()
+    o = orc.OracleServer(parity.np_bits(w0), lr, momentum, depth=max(k, 1))
+    for j, gj in enumerate(grads):
+        o.push(j % 5, parity.np_bits(gj))
+    o.apply_pending()
+    for l in range(3):
+        o.pull(l, l, pdt)
+    assert parity.bitwise(w, o.w), (n, k, momentum, gdt, pdt, offset_g, offset_d)
+    if momentum:
+        assert parity.bitwise(parity.np_bits(v), o.v)
+    for r in range(3):
+        assert parity.bitwise(reps[r], o.replicas[r]), r
+    assert st == o.staleness
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 4, 5, 7, 8, 9, 63, 64, 65, 255, 256, 257, 4095, 4097,
+                               4 * 256 * 7 + 3])
+def test_edge_sizes(torch, n):
+    for k in (1, 9):
+        for momentum in (0.0, 0.9):
+            for gdt, pdt in ((ps.PS_F32, ps.PS_F32), (ps.PS_BF16, ps.PS_BF16), (ps.PS_F32, ps.PS_BF16)):
+                _run_edge(torch, n, k, momentum, gdt, pdt, seed=n)
+
+
+@pytest.mark.parametrize("k", list(range(1, 18)) + [23, 31, 32, 33, 40, 47, 48, 63, 64])
+def test_edge_queue_depths(torch, k):
+    _run_edge(torch, 10007, k, 0.9, ps.PS_F32, ps.PS_F32, seed=k)
+    _run_edge(torch, 10007, k, 0.0, ps.PS_BF16, ps.PS_BF16, seed=k)
+
+
+@pytest.mark.parametrize("og,od", [(1, 0), (0, 1), (2, 3), (4, 4), (3, 0)])
+def test_misaligned_buffers_scalar_path(torch, og, od):
+    """Element offsets that break 16-byte (fp32) or 8-byte (bf16) alignment
+    take the scalar kernels and must give the same bits."""
+    for gdt, pdt in ((ps.PS_F32, ps.PS_F32), (ps.PS_BF16, ps.PS_BF16)):
+        for momentum in (0.0, 0.9):
+            _run_edge(torch, 20011, 5, momentum, gdt, pdt, offset_g=og, offset_d=od, seed=og * 7 + od)
+
+
+def test_lr_zero_and_zero_gradient(torch):
+    n = 5000
+    w0 = torch.linspace(-0.05, 0.05, n, device="cuda")
+    w0[:2] = torch.tensor([0.0, -0.0])
+    for lr, scale in ((0.0, 1.0), (0.01, 0.0)):
+        srv = ps.ParameterServer(n, lr, 0.9, queue_depth=4)
+        srv.set_weights(w0)
+        g = torch.randn(n, device="cuda") * scale
+        for _ in range(4):
+            srv.push(0, g)
+        srv.apply_pending()
+        w = srv.weights_copy()
+        o = orc.OracleServer(parity.np_bits(w0), lr, 0.9, depth=4)
+        for _ in range(4):
+            o.push(0, parity.np_bits(g))
+        o.apply_pending()
+        assert parity.bitwise(parity.np_bits(w), o.w)
+        if scale == 0.0:
+            assert parity.bitwise(parity.np_bits(w), parity.np_bits(w0))
+        srv.close()
+
+
+def test_mixed_dtype_queue(torch):
+    """fp32 and bf16 gradients in one queue: applied as runs, in push order."""
+    n = 30001
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(5)
+    w0 = (torch.rand(n, generator=gen, device="cuda") - 0.5) * 0.1
+    gs = [torch.randn(n, generator=gen, device="cuda") * 1e-2 for _ in range(7)]
+    gs = [g.to(torch.bfloat16) if j in (1, 2, 5) else g for j, g in enumerate(gs)]
+    for m in (0.0, 0.9):
+        srv = ps.ParameterServer(n, 0.01, m, queue_depth=8)
+        srv.set_weights(w0)
+        dst = torch.empty(n, device="cuda")
+        for j, g in enumerate(gs):
+            srv.push(j, g)
+        srv.apply_pull([0], [dst])
+        o = orc.OracleServer(parity.np_bits(w0), 0.01, m, depth=8)
+        for j, g in enumerate(gs):
+            o.push(j, parity.np_bits(g))
+        o.apply_pending()
+        assert parity.bitwise(parity.np_bits(srv.weights_copy()), o.w)
+        assert parity.bitwise(parity.np_bits(dst), o.w)
+        assert srv.timestamp == 7
+        srv.close()
+
+
+def test_golden_staleness_script_through_abi(torch):
+    """The hand-worked schedule of tests/golden/staleness_k2.txt, through the
+    C ABI (timestamps, staleness, queue bound, pull skip)."""
+    depth, ops, expect = golden_script.load("staleness_k2.txt")
+    n = 4
+    g = torch.full((n,), 0.5, device="cuda")
+    dsts = {l: torch.empty(n, device="cuda") for l in range(3)}
+    srv = ps.ParameterServer(n, 2.0 ** -4, 0.0, queue_depth=depth)
+    srv.set_weights(torch.zeros(n, device="cuda"))
+    stale = []
+    for op, l, outcome in ops:
+        if op == "push":
+            assert srv.push(l, g) == (outcome == "ok")
+        elif op == "apply":
+            srv.apply_pending()
+            stale += srv.last_staleness()
+        else:
+            before = srv.stats().pulls_skipped
+            srv.pull(l, dsts[l])
+            assert (srv.stats().pulls_skipped == before) == (outcome == "pulled")
+        assert 0 <= srv.pending <= depth
+    st = srv.stats()
+    assert stale == expect["staleness"]
+    assert srv.timestamp == expect["ts"][0]
+    assert (st.pulls, st.pulls_skipped, st.pushes_rejected) == (
+        expect["pulls"], expect["skipped"], expect["rejected"])
+    assert st.staleness_max == 4 and st.staleness_sum == sum(expect["staleness"])
+    assert torch.all(srv.weights_copy() == -7 / 32)
+    srv.close()
+
+
+def test_queue_full_and_errors(torch):
+    n = 1000
+    srv = ps.ParameterServer(n, 0.1, 0.0, queue_depth=3)
+    g = torch.ones(n, device="cuda")
+    assert all(srv.push(0, g) for _ in range(3))
+    assert not srv.push(1, g) and srv.pending == 3          # refused, unchanged
+    assert ps.ps_set_queue_depth(srv.h, 2) == ps.PS_ESTATE
+    assert ps.ps_set_queue_depth(srv.h, 65) == ps.PS_EINVAL
+    assert ps.ps_set_weights(srv.h, g.data_ptr()) == ps.PS_ESTATE
+    assert ps.ps_push(srv.h, -1, g.data_ptr()) == ps.PS_EINVAL
+    assert ps.ps_push(srv.h, ps.PS_MAX_LEARNERS, g.data_ptr()) == ps.PS_EINVAL
+    assert ps.ps_push_dtype(srv.h, 0, g.data_ptr(), 7) == ps.PS_EINVAL
+    d = torch.empty(n, device="cuda")
+    assert ps.ps_pull_many(srv.h, [0, 1], [d.data_ptr(), d.data_ptr()], ps.PS_F32) == ps.PS_EINVAL
+    assert ps.ps_pull_many(srv.h, [0] * 65, [d.data_ptr()] * 65, ps.PS_F32) == ps.PS_EINVAL
+    srv.apply_pending()
+    assert srv.timestamp == 3 and srv.pending == 0
+    srv.apply_pending()                                       # empty: no-op
+    assert srv.timestamp == 3
+    st = srv.stats()
+    assert (st.pushes_accepted, st.pushes_rejected, st.pushes_applied, st.applies) == (3, 1, 3, 1)
+    srv.close()
+
+
+def test_pull_skip_on_off_same_bits(torch):
+    cfg = wl.CONFIGS["alexnet"].scaled(20000, pushes=200, pool=16)
+    ev = wl.schedule(cfg)
+    pool = wl.make_pool(cfg, "cuda")
+    w0 = wl.make_w0(cfg, "cuda")
+    ranges = [(0, cfg.n)]
+    a = parity.gpu_replay(cfg, ev, pool, w0, ranges, pull_skip=True)
+    b = parity.gpu_replay(cfg, ev, pool, w0, ranges, pull_skip=False)
+    assert a["counts"][3] > 0 and b["counts"][3] == 0
+    for x, y in zip(a["snaps"], b["snaps"]):
+        for l in x:
+            assert parity.bitwise(x[l][0], y[l][0])
+    assert parity.bitwise(a["w"][0], b["w"][0])
+    ps_, w0s = parity.host_inputs(cfg, pool, w0, ranges)
+    o = parity.oracle_replay(cfg, ev, ps_, w0s, ranges, pull_skip=False)
+    assert parity.compare(b, o, ranges) == []
+
+
+def test_determinism_and_side_stream(torch):
+    """Two runs are bitwise identical, also on a non-default stream."""
+    cfg = wl.CONFIGS["vgg16"].scaled(100003, pushes=96, pool=40)
+    ev = wl.schedule(cfg)
+    pool = wl.make_pool(cfg, "cuda")
+    w0 = wl.make_w0(cfg, "cuda")
+    ranges = [(0, cfg.n)]
+    a = parity.gpu_replay(cfg, ev, pool, w0, ranges, fused=True)
+    s = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        b = parity.gpu_replay(cfg, ev, pool, w0, ranges, fused=True, stream=s)
+    assert parity.bitwise(a["w"][0], b["w"][0]) and parity.bitwise(a["v"][0], b["v"][0])
+
+
+def test_64bit_indexing_beyond_2_31_elements(torch):
+    """n = 2^31 + 5 fp32 weights: element offsets past 2^31 (byte offsets past
+    2^33) are indexed correctly; sampled against the oracle."""
+    n = 2 ** 31 + 5
+    k = 2
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(77)
+    w0 = torch.empty(n, device="cuda").uniform_(-0.05, 0.05, generator=gen)
+    grads = [torch.empty(n, device="cuda").normal_(0, 1e-2, generator=gen) for _ in range(k)]
+    dst = torch.empty(n, device="cuda")
+    srv = ps.ParameterServer(n, 0.01, 0.9, queue_depth=k)
+    srv.set_weights(w0)
+    for j, g in enumerate(grads):
+        srv.push(j, g)
+    srv.apply_pull([0], [dst])
+    srv.sync()
+    ranges = [(0, 1024), (2 ** 31 - 512, 2 ** 31 + 512), (n - 1029, n)]
+    w = srv.weights_copy()
+    for lo, hi in ranges:
+        o = orc.OracleServer(parity.np_bits(w0[lo:hi]), 0.01, 0.9, depth=k)
+        for j, g in enumerate(grads):
+            o.push(j, parity.np_bits(g[lo:hi]))
+        o.apply_pending()
+        assert parity.bitwise(parity.np_bits(w[lo:hi]), o.w)
+        assert parity.bitwise(parity.np_bits(dst[lo:hi]), o.w)
+    srv.close()
+    del w0, grads, dst, w
+    free(torch)
