@@ -1,0 +1,321 @@
+"""Benchmark: gradient pushes applied per second on one MI355X.
+
+Workload: the VGG-16-shaped parameter server (138,357,544 fp32 parameters,
+13 conv + 3 fc tensors flat; lr 0.001, heavy-ball momentum 0.9; 16 learners
+pushing Laplace(0, 1e-3) gradients in seeded random order; K = 32 gradients
+folded per apply; after each apply all 16 learners pull fp32 replicas).
+One step = 32 pushes + one apply + one 16-replica pull, i.e. one pass of the
+whole hot path over one batch. Inputs (64 distinct gradient buffers, 35 GB)
+are resident in HBM before timing starts, each buffer on its own 2 MiB-aligned
+row (as separately allocated learner buffers would be).
+
+Prints one JSON line (rank 0, N = 1). Extra keys: the dominant kernel's
+roofline (algorithmic bytes per launch / mean launch time from HIP events on
+the library's stream), HBM traffic from recorded rocprofv3 counters when the
+kernel source still matches them, a device-copy ceiling, and the oracle timed
+on the host's cores on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_GBPS = 8000.0          # MI355X HBM3E, published
+METRIC = "gradient pushes applied/sec + achieved HBM GB/s (% of peak), 1 MI355X"
+KERNEL_SRC = os.path.join(ROOT, "paper_1611_06213_amd", "csrc", "ps_kernels.hip")
+COUNTERS = os.path.join(ROOT, "profiles", "traffic_vgg16.txt")
+
+
+def algorithmic_bytes(cfg, mode: str, r: int):
+    """Bytes the method must move per step (one apply of K gradients + R
+    replica writes): K gradient reads, w read+write, v read+write (momentum),
+    R replica writes, plus one more read of w when the pull is its own
+    kernel. Returns (per step, per dominant-kernel launch)."""
+    n, k = cfg.n, cfg.depth
+    gb = 2 if cfg.grad_dtype == 1 else 4
+    rb = 2 if cfg.pull_dtype == 1 else 4
+    apply_b = k * n * gb + 8 * n + (8 * n if cfg.momentum else 0)
+    if mode == "fused":
+        step = apply_b + r * n * rb
+        return step, step
+    return apply_b + 4 * n + r * n * rb, apply_b
+
+
+def batches(cfg, wl):
+    """The schedule's full batches: (pushes [(learner, pool buffer)], learners
+    that pull after that apply, deduplicated). A pull issued between two
+    applies sees the weights of the earlier apply whatever its position, so
+    it is attached to that apply. The final partial batch is left out."""
+    out, pushes, last = [], [], None
+    for ev in wl.schedule(cfg):
+        if isinstance(ev, wl.Push):
+            pushes.append((ev.learner, ev.buf))
+        elif isinstance(ev, wl.Apply):
+            last = (pushes, [])
+            if len(pushes) == cfg.depth:
+                out.append(last)
+            pushes = []
+        elif last is not None:
+            for l in ev.learners:
+                if l not in last[1]:
+                    last[1].append(l)
+    return out
+
+
+def recorded_traffic(kernel_label: str):
+    """HBM bytes per launch from the committed counter summary, or None when
+    it is missing or was taken on a different kernel source."""
+    if not os.path.exists(COUNTERS):
+        return None
+    vals = {}
+    for line in open(COUNTERS):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            vals[k.strip()] = v.strip()
+    src = hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
+    if vals.get("kernel_source_sha256") != src or vals.get("mode") != kernel_label:
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(cfg, pool, w0, pulls_per_step: int, seconds: float, distinct: int = 16):
+    """The oracle, as it stands, on a bounded sample of the same workload:
+    whole steps (K pushes, one apply, the step's pulls) over the full vector,
+    single-threaded, repeated until `seconds` of CPU work have accumulated.
+    The pushes cycle over `distinct` pool buffers copied to host memory (the
+    values do not change the work)."""
+    from oracle import server as orc
+
+    import numpy as np
+    import torch
+
+    def host(t):
+        t = t.cpu()
+        if t.dtype == torch.bfloat16:
+            return t.view(torch.int16).numpy().view(np.uint16)
+        return t.numpy()
+
+    distinct = min(distinct, cfg.pool)
+    host_g = [host(pool[j]) for j in range(distinct)]
+    s = orc.OracleServer(w0.cpu().numpy(), cfg.lr, cfg.momentum, depth=cfg.depth)
+    j = steps = 0
+    t0 = time.perf_counter()
+    while True:
+        for _ in range(cfg.depth):
+            s.push(j % cfg.learners, host_g[j % distinct])
+            j += 1
+        s.apply_pending()
+        for r in range(pulls_per_step):
+            s.pull(r, r, cfg.pull_dtype)
+        steps += 1
+        t1 = time.perf_counter()
+        if t1 - t0 >= seconds:
+            break
+    del host_g
+    return {
+        "value": round(steps * cfg.depth / (t1 - t0), 4), "unit": "pushes/s", "cores": 1,
+        "kind": "oracle",
+        "sample": (f"{steps} whole steps ({cfg.depth} pushes + apply + {pulls_per_step} pulls) "
+                   f"over the full {cfg.n:,}-parameter vector, 1 thread, pushes cycling over "
+                   f"{distinct} host copies of pool buffers; {t1 - t0:.1f} s of CPU work"),
+    }
+
+
+def copy_ceiling(torch, ps, lib, n: int = 1 << 28, reps: int = 10):
+    """The library's pull kernel with a single fp32 replica is a plain
+    1-read/1-write device copy: its GB/s is the copy ceiling of this machine."""
+    h = ps.ps_create(n, 0.0, 0.0)
+    stream = torch.cuda.current_stream()
+    ps.ps_set_stream(h, stream.cuda_stream)
+    ps.ps_set_pull_skip(h, False)
+    dst = torch.empty(n, dtype=torch.float32, device="cuda")
+    ids, dp = ps._ints([0]), ps._ptrs([dst.data_ptr()])
+    lib.ps_pull_many(h, 1, ids, dp, 0)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        lib.ps_pull_many(h, 1, ids, dp, 0)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    ps.ps_destroy(h)
+    del dst
+    return 8 * n / (ms * 1e-3) / 1e9
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="vgg16")
+    ap.add_argument("--mode", choices=["fused", "separate"], default="separate",
+                    help="separate: ps_apply_pending + ps_pull_many (one kernel each, timed "
+                         "apart); fused: ps_apply_pull (the same kernels above one replica)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=8.0)
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="also run a plain 1 GiB copy (known bytes) for counter calibration")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the parameter server here runs on a single "
+              "MI355X; multi-GPU sharding is a design note, not built.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_1611_06213_amd import ps
+    from paper_1611_06213_amd import workloads as wl
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    lib = ps.load_library()
+    cfg = wl.CONFIGS[args.config]
+    n, K, R = cfg.n, cfg.depth, cfg.replicas
+    stream = torch.cuda.current_stream()
+
+    pool = wl.make_pool(cfg, "cuda")
+    w0 = wl.make_w0(cfg, "cuda")
+    rdt = torch.bfloat16 if cfg.pull_dtype == wl.BF16 else torch.float32
+    replicas = wl.Rows(R, n, rdt, "cuda")
+    plan = batches(cfg, wl)
+    torch.cuda.synchronize()
+
+    h = ps.ps_create(n, cfg.lr, cfg.momentum)
+    assert ps.ps_set_queue_depth(h, K) == 0
+    assert ps.ps_set_stream(h, stream.cuda_stream) == 0
+    assert ps.ps_set_weights(h, w0.data_ptr()) == 0
+
+    gptr = [pool[j].data_ptr() for j in range(cfg.pool)]
+    calls = []
+    for pushes_b, pulls_b in plan:
+        calls.append(([(l, gptr[b]) for l, b in pushes_b], len(pulls_b), ps._ints(pulls_b or [0]),
+                      ps._ptrs([replicas[l].data_ptr() for l in pulls_b] or [0])))
+    pdt = cfg.pull_dtype
+    gdt = cfg.grad_dtype
+    push = lib.ps_push_dtype
+    it = 0
+
+    def step(ev=None):
+        nonlocal it
+        pushes_b, r, ids, dptr = calls[it % len(calls)]
+        it += 1
+        for l, g in pushes_b:
+            if push(h, l, g, gdt) != 0:
+                raise RuntimeError(ps.ps_last_error())
+        if ev is not None:
+            ev[0].record(stream)
+        if args.mode == "fused":
+            rc = lib.ps_apply_pull(h, r, ids, dptr, pdt)
+            if ev is not None:
+                ev[1].record(stream)
+        else:
+            rc = lib.ps_apply_pending(h)
+            if ev is not None:
+                ev[1].record(stream)
+            rc = rc or lib.ps_pull_many(h, r, ids, dptr, pdt)
+            if ev is not None:
+                ev[2].record(stream)
+        if rc != 0:
+            raise RuntimeError(ps.ps_last_error())
+        return r
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    rs = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s_ in range(args.steps):
+        rs.append(step(evs[s_]))
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+
+    elapsed = t1 - t0
+    pushes = K * args.steps
+    step_bytes = sum(algorithmic_bytes(cfg, args.mode, r)[0] for r in rs)
+    launch_bytes = sum(algorithmic_bytes(cfg, args.mode, r)[1] for r in rs) / args.steps
+    k_ms = sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps
+    p_ms = (sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps) if args.mode == "separate" else 0.0
+    gbps = step_bytes / elapsed / 1e9
+    achieved = launch_bytes / (k_ms * 1e-3) / 1e9
+    label = f"{args.config}-{args.mode}"
+    traffic = recorded_traffic(label)
+
+    if args.calib_copy:
+        a = torch.empty(1 << 28, dtype=torch.float32, device="cuda").fill_(2.0)
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
+
+    ts = ps.ps_timestamp(h)
+    ps.ps_destroy(h)
+    ceiling = copy_ceiling(torch, ps, lib)
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        del replicas
+        torch.cuda.empty_cache()
+        cpu = cpu_baseline(cfg, pool, w0, round(sum(rs) / len(rs)), args.cpu_seconds)
+
+    kern = ("ps_apply_pull (apply + pull kernels)" if args.mode == "fused"
+            else "apply_vec (fused K-gradient apply)")
+    pull_bytes = sum(r * n * (2 if pdt == wl.BF16 else 4) + 4 * n for r in rs) / args.steps
+    out = {
+        "metric": METRIC,
+        "value": round(pushes / elapsed, 2),
+        "unit": "pushes/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(elapsed / args.steps * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if cfg.grad_dtype == wl.F32 else "bf16-grad/f32",
+        "data": "synthetic",
+        "config": {
+            "workload": (f"{cfg.name}: {n:,} fp32 params, K={K} pushes per apply, "
+                         f"R={max(rs)} {'fp32' if pdt == wl.F32 else 'bf16'} replicas per apply, "
+                         f"lr={cfg.lr}, momentum={cfg.momentum}, {cfg.learners} learners, "
+                         f"{args.mode} apply+pull"),
+            "params": n, "queue_depth": K, "replicas_per_apply": round(sum(rs) / len(rs), 2),
+            "mode": args.mode,
+        },
+        "gbps": round(gbps, 1),
+        "pct_peak": round(100 * gbps / PEAK_GBPS, 2),
+        "bytes_per_step": round(step_bytes / args.steps),
+        "pushes_per_s_device": round(pushes / ((k_ms + p_ms) * args.steps * 1e-3), 2),
+        "kernel_ms": {"apply": round(k_ms, 4), **({"pull": round(p_ms, 4)} if p_ms else {})},
+        **({"pull_kernel_gbps": round(pull_bytes / (p_ms * 1e-3) / 1e9, 1)} if p_ms else {}),
+        "roofline": {
+            "bound": "hbm", "kernel": kern,
+            "achieved": round(achieved, 1), "peak": PEAK_GBPS, "unit": "GB/s",
+            "frac": round(achieved / PEAK_GBPS, 4),
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": round(launch_bytes),
+        },
+        "copy_gbps": round(ceiling, 1),
+        "cpu_baseline": cpu,
+        "timestamp_after": ts,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

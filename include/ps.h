@@ -42,8 +42,10 @@
  *
  * Pointers named "device" must point to device memory (hipMalloc or torch
  * CUDA tensors) on the device that was current at ps_create. Any alignment is
- * accepted; 16-byte-aligned fp32 buffers and 8-byte-aligned bf16 buffers take
- * the vector path, others a scalar path with identical results.
+ * accepted and gives identical results: 16-byte-aligned buffers take the
+ * widest vector path, 8-byte-aligned bf16 buffers a narrower one, others a
+ * scalar path. Buffers that start on 256-byte (better: 2 MiB) boundaries
+ * stream fastest.
  *
  * Status codes: every int-returning call returns PS_OK (0) or a negative
  * PS_E* code; ps_last_error() then describes the failure (per thread).
@@ -128,15 +130,22 @@ int ps_apply_pending(ps_server *ps);
 int ps_pull(ps_server *ps, int learner_id, void *dst);
 
 /* Pull for n learners at once: learner_ids[i] into dsts[i], all in dst_dtype
- * (PS_F32, or PS_BF16 = round to nearest even). One fan-out kernel reads w
- * once and writes every replica that is not skipped. 0 <= n <=
- * PS_MAX_REPLICAS; the buffers that are written must be distinct. */
+ * (PS_F32, or PS_BF16 = round to nearest even). One fan-out kernel writes
+ * every replica that is not skipped, reading w from HBM once (it walks w in
+ * tiles that stay cached while the replicas of a tile are written).
+ * 0 <= n <= PS_MAX_REPLICAS; the buffers that are written must be distinct. */
 int ps_pull_many(ps_server *ps, int n, const int *learner_ids, void *const *dsts, int dst_dtype);
 
-/* ps_apply_pending followed by ps_pull_many, fused: the replicas are written
- * from the same pass that updates w, so w is not read again. The result is
- * identical to the two calls in sequence. */
+/* ps_apply_pending followed by ps_pull_many, in one call; the result is
+ * identical to the two calls in sequence. Up to the fusion limit (see
+ * ps_set_pull_fusion) the replicas are written from the same pass that
+ * updates w, so w is not read again; above it the apply kernel is followed
+ * by the tiled fan-out, which serves many replicas faster than one pass. */
 int ps_apply_pull(ps_server *ps, int n, const int *learner_ids, void *const *dsts, int dst_dtype);
+
+/* Largest replica count ps_apply_pull writes from the apply pass itself
+ * (0..PS_MAX_REPLICAS; default 1). */
+int ps_set_pull_fusion(ps_server *ps, int max_replicas);
 
 /* Use hip_stream (a hipStream_t; NULL = the null stream) for all later device
  * work. The caller orders it against work already on the previous stream. */

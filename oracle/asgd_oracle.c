@@ -13,6 +13,13 @@
  * Precision: the paper stores weights and gradients as 32-bit floats (Sec. 4.4,
  * "Half-precision floating point operations"), so each step computes in
  * binary32; lr and momentum arrive as C floats.
+ *
+ * Pins (tests/test_oracle_pins.py): closed forms of the constant-gradient
+ * run, zero gradients, an exact-rational evaluation with round-to-nearest-even
+ * after every operation over every arrival order of small cases, and torch's
+ * bfloat16 conversions. The momentum step is pinned to its own closed form
+ * only: the paper has no momentum, so against the paper it is parity
+ * unpinned.
  */
 #include <stddef.h>
 #include <stdint.h>

@@ -33,15 +33,25 @@ struct PullArgs {
 
 // Launch geometry: blocks are 256 threads; max_blocks caps the grid (the
 // kernels then stride over the remaining chunks). 0 = one chunk per lane.
+// Applies of at least occupancy_cap_min_k gradients reserve
+// occupancy_cap_lds bytes of LDS per block (0 = none), chosen at server
+// creation so that one block fits per compute unit.
 struct Geometry {
     int max_blocks = 0;
+    unsigned occupancy_cap_lds = 0;
+    int occupancy_cap_min_k = 16;
 };
 
+// LDS bytes that leave room for exactly one block per compute unit on the
+// current device, or 0 if the device does not allow such a reservation.
+unsigned one_block_per_cu_lds();
+
 // grad_dtype: PS_F32 | PS_BF16. pull_dtype: -1 (no replicas), PS_F32, PS_BF16.
-// vec: every pointer meets the vector alignment (16 B fp32, 8 B bf16).
-hipError_t launch_apply(const ApplyArgs &a, int grad_dtype, int pull_dtype, bool vec,
+// level: 2 = every buffer 16-byte aligned; 1 = fp32 buffers 16-byte and bf16
+// buffers 8-byte aligned; 0 = anything else (scalar kernels).
+hipError_t launch_apply(const ApplyArgs &a, int grad_dtype, int pull_dtype, int level,
                         const Geometry &geo, hipStream_t s);
-hipError_t launch_pull(const PullArgs &a, int pull_dtype, bool vec, const Geometry &geo,
+hipError_t launch_pull(const PullArgs &a, int pull_dtype, int level, const Geometry &geo,
                        hipStream_t s);
 hipError_t launch_zero(float *p, uint64_t n, hipStream_t s);
 

@@ -14,8 +14,10 @@
 //         registers, and the result stored once: K sequential steps cost one
 //         pass over w instead of K. Optionally the same pass writes R replica
 //         copies of the new w (a fused pull).
-// pull:   load w once, write it to R replica buffers (fp32, or bf16 rounded
-//         to nearest even).
+// pull:   write w to R replica buffers (fp32, or bf16 rounded to nearest
+//         even). One replica: a streaming copy. Several: a tiled fan-out that
+//         keeps each tile of w in the memory-side cache while the replicas
+//         are written one after another (see pull_tiled).
 //
 // Every product and sum is rounded on its own (no fused multiply-add), so
 // the result is bit-identical to sequential binary32 steps.
@@ -28,32 +30,59 @@
 namespace gadei {
 namespace {
 
-constexpr int kBlock = 256;   // 4 waves of 64 lanes
-constexpr int kGroup = 8;     // gradients whose loads are issued together
+#ifndef PS_BLOCK
+#define PS_BLOCK 256
+#endif
+#ifndef PS_GROUP
+#define PS_GROUP 16
+#endif
+#ifndef PS_NT_WV
+#define PS_NT_WV 1
+#endif
+
+constexpr int kBlock = PS_BLOCK;      // threads per block (waves of 64 lanes)
+constexpr int kGroup = PS_GROUP;      // gradients whose loads are issued together
+// w and v are read once and written once per launch and are not touched
+// again until the next apply, after tens of GB of other traffic: stream them
+// with the non-temporal hint too.
+constexpr bool kNtWV = PS_NT_WV != 0;
+
+// A launch's work-items (blocks * threads) must stay below 2^32.
+constexpr uint64_t kMaxBlocks = 0xffffffffull / kBlock;
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // ---------------------------------------------------------------- loads
 
-// E consecutive fp32 values starting at p (E = 4: one 16-byte load).
-template <int E>
+// E consecutive fp32 values starting at p (E = 4: one 16-byte load; E = 8:
+// two adjacent ones).
+template <int E, bool NT>
 __device__ __forceinline__ void ld_f32(float (&x)[E], const float *p) {
-    if constexpr (E == 4) {
-        f32x4 t = *reinterpret_cast<const f32x4 *>(p);
-        x[0] = t.x; x[1] = t.y; x[2] = t.z; x[3] = t.w;
+    if constexpr (E == 1) {
+        x[0] = NT ? __builtin_nontemporal_load(p) : *p;
     } else {
-        x[0] = *p;
+#pragma unroll
+        for (int h = 0; h < E / 4; ++h) {
+            const f32x4 *q = reinterpret_cast<const f32x4 *>(p) + h;
+            f32x4 t = NT ? __builtin_nontemporal_load(q) : *q;
+            x[4 * h] = t.x; x[4 * h + 1] = t.y; x[4 * h + 2] = t.z; x[4 * h + 3] = t.w;
+        }
     }
 }
 
-template <int E>
+template <int E, bool NT>
 __device__ __forceinline__ void st_f32(float *p, const float (&x)[E]) {
-    if constexpr (E == 4) {
-        f32x4 t = {x[0], x[1], x[2], x[3]};
-        *reinterpret_cast<f32x4 *>(p) = t;
+    if constexpr (E == 1) {
+        if constexpr (NT) __builtin_nontemporal_store(x[0], p); else *p = x[0];
     } else {
-        *p = x[0];
+#pragma unroll
+        for (int h = 0; h < E / 4; ++h) {
+            f32x4 t = {x[4 * h], x[4 * h + 1], x[4 * h + 2], x[4 * h + 3]};
+            f32x4 *q = reinterpret_cast<f32x4 *>(p) + h;
+            if constexpr (NT) __builtin_nontemporal_store(t, q); else *q = t;
+        }
     }
 }
 
@@ -61,19 +90,26 @@ __device__ __forceinline__ void st_f32(float *p, const float (&x)[E]) {
 __device__ __forceinline__ float lo_bf16(uint32_t u) { return __uint_as_float(u << 16); }
 __device__ __forceinline__ float hi_bf16(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
 
-// Gradient values for coordinates i .. i+E-1. Gradients are read exactly once
-// per launch, so the loads carry the non-temporal hint.
+// Gradient values for coordinates i .. i+E-1 (i is a multiple of E).
+// Gradients are read exactly once per launch, so the loads carry the
+// non-temporal hint. fp32 chunks are 4 values (16 bytes); bf16 chunks are 8
+// values (16 bytes) or 4 (8 bytes) when a buffer is only 8-byte aligned.
 template <int GDT, int E>
 __device__ __forceinline__ void ld_grad(float (&x)[E], const void *g, uint64_t i) {
     if constexpr (GDT == PS_F32) {
-        if constexpr (E == 4) {
-            f32x4 t = __builtin_nontemporal_load(reinterpret_cast<const f32x4 *>(g) + (i >> 2));
-            x[0] = t.x; x[1] = t.y; x[2] = t.z; x[3] = t.w;
-        } else {
+        if constexpr (E == 1) {
             x[0] = static_cast<const float *>(g)[i];
+        } else {
+            ld_f32<E, true>(x, static_cast<const float *>(g) + i);
         }
     } else {
-        if constexpr (E == 4) {
+        if constexpr (E == 8) {
+            u32x4 u = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(g) + (i >> 3));
+            x[0] = lo_bf16(u.x); x[1] = hi_bf16(u.x);
+            x[2] = lo_bf16(u.y); x[3] = hi_bf16(u.y);
+            x[4] = lo_bf16(u.z); x[5] = hi_bf16(u.z);
+            x[6] = lo_bf16(u.w); x[7] = hi_bf16(u.w);
+        } else if constexpr (E == 4) {
             u32x2 u = __builtin_nontemporal_load(reinterpret_cast<const u32x2 *>(g) + (i >> 2));
             x[0] = lo_bf16(u.x); x[1] = hi_bf16(u.x);
             x[2] = lo_bf16(u.y); x[3] = hi_bf16(u.y);
@@ -93,19 +129,26 @@ __device__ __forceinline__ uint32_t bf16_rne(float f) {
     return ((u & 0x7fffffffu) > 0x7f800000u) ? ((u >> 16) | 0x40u) : r;
 }
 
-// One replica's values for coordinates i .. i+E-1. Replicas are not read
-// back by the server, so the stores carry the non-temporal hint.
+// One replica's values for coordinates i .. i+E-1 (i a multiple of E).
+// Replicas are not read back by the server, so the stores carry the
+// non-temporal hint.
 template <int PDT, int E>
 __device__ __forceinline__ void st_dst(void *d, uint64_t i, const float (&x)[E]) {
     if constexpr (PDT == PS_F32) {
-        if constexpr (E == 4) {
-            f32x4 t = {x[0], x[1], x[2], x[3]};
-            __builtin_nontemporal_store(t, reinterpret_cast<f32x4 *>(d) + (i >> 2));
-        } else {
+        if constexpr (E == 1) {
             static_cast<float *>(d)[i] = x[0];
+        } else {
+            st_f32<E, true>(static_cast<float *>(d) + i, x);
         }
     } else {
-        if constexpr (E == 4) {
+        if constexpr (E == 8) {
+            u32x4 t;
+            t.x = bf16_rne(x[0]) | (bf16_rne(x[1]) << 16);
+            t.y = bf16_rne(x[2]) | (bf16_rne(x[3]) << 16);
+            t.z = bf16_rne(x[4]) | (bf16_rne(x[5]) << 16);
+            t.w = bf16_rne(x[6]) | (bf16_rne(x[7]) << 16);
+            __builtin_nontemporal_store(t, reinterpret_cast<u32x4 *>(d) + (i >> 3));
+        } else if constexpr (E == 4) {
             u32x2 t;
             t.x = bf16_rne(x[0]) | (bf16_rne(x[1]) << 16);
             t.y = bf16_rne(x[2]) | (bf16_rne(x[3]) << 16);
@@ -137,51 +180,62 @@ __device__ __forceinline__ void step(float (&w)[E], float (&v)[E], const float (
 }
 
 // Coordinates i .. i+E-1 through all K pending gradients, oldest first.
-// Gradients go in groups of kGroup whose loads are all issued before the
-// group's updates, so each lane keeps kGroup independent loads in flight;
-// full groups carry no predicates (their pointer loads batch and the waits
-// count down one load at a time), the last partial group is predicated.
+// Gradients go in groups whose loads are all issued before the group's
+// updates, so each lane keeps many independent loads in flight: full groups
+// of kGroup, then one of 8 if that many remain (neither carries predicates,
+// so their pointer loads batch and the waits count down one load at a
+// time), then a predicated group for the last 0..7.
+template <bool MOM, int GDT, int E, int G>
+__device__ __forceinline__ void apply_group(const ApplyArgs &a, int k0, uint64_t i, float (&w)[E],
+                                            float (&v)[E], float lr, float m) {
+    float g[G][E];
+#pragma unroll
+    for (int j = 0; j < G; ++j) ld_grad<GDT, E>(g[j], a.g[k0 + j], i);
+#pragma unroll
+    for (int j = 0; j < G; ++j) step<MOM, E>(w, v, g[j], lr, m);
+}
+
 template <bool MOM, int GDT, int PDT, int E>
 __device__ __forceinline__ void apply_chunk(const ApplyArgs &a, uint64_t i) {
     float w[E], v[E];
-    ld_f32<E>(w, a.w + i);
-    if constexpr (MOM) ld_f32<E>(v, a.v + i);
+    ld_f32<E, kNtWV>(w, a.w + i);
+    if constexpr (MOM) ld_f32<E, kNtWV>(v, a.v + i);
     const float lr = a.lr;
     const float m = a.m;
     const int k = a.k;
     int k0 = 0;
-    for (; k0 + kGroup <= k; k0 += kGroup) {
-        float g[kGroup][E];
-#pragma unroll
-        for (int j = 0; j < kGroup; ++j) ld_grad<GDT, E>(g[j], a.g[k0 + j], i);
-#pragma unroll
-        for (int j = 0; j < kGroup; ++j) step<MOM, E>(w, v, g[j], lr, m);
+    for (; k0 + kGroup <= k; k0 += kGroup) apply_group<MOM, GDT, E, kGroup>(a, k0, i, w, v, lr, m);
+    if constexpr (kGroup > 8) {
+        if (k0 + 8 <= k) {
+            apply_group<MOM, GDT, E, 8>(a, k0, i, w, v, lr, m);
+            k0 += 8;
+        }
     }
     if (k0 < k) {
-        float g[kGroup][E];
+        float g[8][E];
 #pragma unroll
-        for (int j = 0; j < kGroup; ++j)
+        for (int j = 0; j < 8; ++j)
             if (k0 + j < k) ld_grad<GDT, E>(g[j], a.g[k0 + j], i);
 #pragma unroll
-        for (int j = 0; j < kGroup; ++j)
+        for (int j = 0; j < 8; ++j)
             if (k0 + j < k) step<MOM, E>(w, v, g[j], lr, m);
     }
-    st_f32<E>(a.w + i, w);
-    if constexpr (MOM) st_f32<E>(a.v + i, v);
+    st_f32<E, kNtWV>(a.w + i, w);
+    if constexpr (MOM) st_f32<E, kNtWV>(a.v + i, v);
     if constexpr (PDT >= 0) {
         for (int r = 0; r < a.r; ++r) st_dst<PDT, E>(a.dst[r], i, w);
     }
 }
 
-// Vector path: lane t of the grid owns 4-coordinate chunks t, t + stride, ...
-// The n mod 4 trailing coordinates go to the first lanes of the grid.
-template <bool MOM, int GDT, int PDT>
+// Vector path: lane t of the grid owns E-coordinate chunks t, t + stride, ...
+// The n mod E trailing coordinates go to the first lanes of the grid.
+template <bool MOM, int GDT, int PDT, int E>
 __global__ void __launch_bounds__(kBlock) apply_vec(const ApplyArgs a) {
-    const uint64_t chunks = a.n >> 2;
+    const uint64_t chunks = a.n / E;
     const uint64_t tid = static_cast<uint64_t>(blockIdx.x) * kBlock + threadIdx.x;
     const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kBlock;
-    for (uint64_t c = tid; c < chunks; c += stride) apply_chunk<MOM, GDT, PDT, 4>(a, c << 2);
-    if (tid < a.n - (chunks << 2)) apply_chunk<MOM, GDT, PDT, 1>(a, (chunks << 2) + tid);
+    for (uint64_t c = tid; c < chunks; c += stride) apply_chunk<MOM, GDT, PDT, E>(a, c * E);
+    if (tid < a.n - chunks * E) apply_chunk<MOM, GDT, PDT, 1>(a, chunks * E + tid);
 }
 
 // Scalar path for buffers without vector alignment: one coordinate per lane.
@@ -194,27 +248,66 @@ __global__ void __launch_bounds__(kBlock) apply_scalar(const ApplyArgs a) {
 
 // ---------------------------------------------------------------- pull
 
-template <int PDT, int E>
+template <int PDT, int E, bool NT>
 __device__ __forceinline__ void pull_chunk(const PullArgs &a, uint64_t i) {
     float w[E];
-    ld_f32<E>(w, a.w + i);
+    ld_f32<E, NT>(w, a.w + i);
     for (int r = 0; r < a.r; ++r) st_dst<PDT, E>(a.dst[r], i, w);
 }
 
+// One pass: each lane reads its chunk of w once and writes it to every
+// replica. Used for a single replica (a plain streaming copy).
 template <int PDT>
 __global__ void __launch_bounds__(kBlock) pull_vec(const PullArgs a) {
     const uint64_t chunks = a.n >> 2;
     const uint64_t tid = static_cast<uint64_t>(blockIdx.x) * kBlock + threadIdx.x;
     const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kBlock;
-    for (uint64_t c = tid; c < chunks; c += stride) pull_chunk<PDT, 4>(a, c << 2);
-    if (tid < a.n - (chunks << 2)) pull_chunk<PDT, 1>(a, (chunks << 2) + tid);
+    for (uint64_t c = tid; c < chunks; c += stride) pull_chunk<PDT, 4, true>(a, c << 2);
+    if (tid < a.n - (chunks << 2)) pull_chunk<PDT, 1, true>(a, (chunks << 2) + tid);
 }
 
+// Tiled fan-out for R >= 2 replicas. w is cut into tiles of kTileBytes; the
+// block index enumerates (tile, replica, block within the tile) with the last
+// fastest, so in-order dispatch walks replica 0 of tile 0, replica 1 of tile
+// 0, ... The R re-reads of a tile then hit the memory-side cache (the tile
+// is loaded with ordinary, allocating loads) and HBM sees one replica's
+// write stream at a time instead of R interleaved ones, which the memory
+// system serves markedly faster. HBM traffic stays one read of w plus the R
+// replica writes.
+constexpr uint64_t kTileBytes = 8u << 20;   // of w
+constexpr unsigned kTileBlocks = 1024;      // blocks per (tile, replica)
+
+template <int PDT, int E>
+__global__ void __launch_bounds__(kBlock) pull_tiled(const PullArgs a, unsigned bpt) {
+    constexpr uint64_t kTileChunksE = kTileBytes / (4 * E);
+    const uint64_t chunks = a.n / E;
+    const unsigned b = blockIdx.x % bpt;
+    const unsigned tr = blockIdx.x / bpt;
+    const int r = static_cast<int>(tr % static_cast<unsigned>(a.r));
+    const uint64_t t = tr / static_cast<unsigned>(a.r);
+    const uint64_t c0 = t * kTileChunksE;
+    const uint64_t c1 = c0 + kTileChunksE < chunks ? c0 + kTileChunksE : chunks;
+    void *d = a.dst[r];
+    for (uint64_t c = c0 + static_cast<uint64_t>(b) * kBlock + threadIdx.x; c < c1;
+         c += static_cast<uint64_t>(bpt) * kBlock) {
+        float w[E];
+        ld_f32<E, false>(w, a.w + c * E);
+        st_dst<PDT, E>(d, c * E, w);
+    }
+    if (t == 0 && b == 0 && threadIdx.x < a.n - chunks * E) {
+        const uint64_t i = chunks * E + threadIdx.x;
+        float w[1];
+        ld_f32<1, false>(w, a.w + i);
+        st_dst<PDT, 1>(d, i, w);
+    }
+}
+
+// Scalar path for replicas without vector alignment.
 template <int PDT>
 __global__ void __launch_bounds__(kBlock) pull_scalar(const PullArgs a) {
     const uint64_t tid = static_cast<uint64_t>(blockIdx.x) * kBlock + threadIdx.x;
     const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kBlock;
-    for (uint64_t i = tid; i < a.n; i += stride) pull_chunk<PDT, 1>(a, i);
+    for (uint64_t i = tid; i < a.n; i += stride) pull_chunk<PDT, 1, false>(a, i);
 }
 
 __global__ void __launch_bounds__(kBlock) zero_f32(float *p, uint64_t n) {
@@ -228,57 +321,115 @@ __global__ void __launch_bounds__(kBlock) zero_f32(float *p, uint64_t n) {
 unsigned grid_for(uint64_t items, const Geometry &geo) {
     uint64_t blocks = (items + kBlock - 1) / kBlock;
     if (blocks == 0) blocks = 1;
-    const uint64_t cap = geo.max_blocks > 0 ? static_cast<uint64_t>(geo.max_blocks) : 0x7fffffffull;
+    uint64_t cap = geo.max_blocks > 0 ? static_cast<uint64_t>(geo.max_blocks) : kMaxBlocks;
+    if (cap > kMaxBlocks) cap = kMaxBlocks;
     return static_cast<unsigned>(blocks < cap ? blocks : cap);
 }
 
 template <bool MOM, int GDT, int PDT>
-hipError_t go_apply(const ApplyArgs &a, bool vec, const Geometry &geo, hipStream_t s) {
-    if (vec) {
-        hipLaunchKernelGGL((apply_vec<MOM, GDT, PDT>), dim3(grid_for(a.n >> 2, geo)), dim3(kBlock),
-                           0, s, a);
-    } else {
+hipError_t go_apply(const ApplyArgs &a, int level, const Geometry &geo, hipStream_t s) {
+    if (level == 0) {
         hipLaunchKernelGGL((apply_scalar<MOM, GDT, PDT>), dim3(grid_for(a.n, geo)), dim3(kBlock),
                            0, s, a);
+        return hipGetLastError();
     }
+    // bf16 gradients move 16 bytes per lane as 8 values when every buffer is
+    // 16-byte aligned; otherwise (and for fp32) a lane's chunk is 4 values.
+    const bool e8 = GDT == PS_BF16 && level == 2;
+    // fp32 gradients: with many gradients per apply each lane keeps >= 16
+    // loads of 16 bytes in flight; one block per CU then saturates HBM, and
+    // fewer resident waves keep fewer DRAM pages and translations live at
+    // once across the K+2 streams, which measured faster and steadier. The
+    // kernel uses no LDS: the reservation only limits residency. bf16
+    // gradients (half the bytes per value) measured best at full residency.
+    const unsigned lds =
+        (GDT == PS_F32 && a.k >= geo.occupancy_cap_min_k) ? geo.occupancy_cap_lds : 0;
+    if constexpr (GDT == PS_BF16) {
+        if (e8) {
+            hipLaunchKernelGGL((apply_vec<MOM, GDT, PDT, 8>), dim3(grid_for(a.n / 8, geo)),
+                               dim3(kBlock), lds, s, a);
+            return hipGetLastError();
+        }
+    }
+    hipLaunchKernelGGL((apply_vec<MOM, GDT, PDT, 4>), dim3(grid_for(a.n / 4, geo)), dim3(kBlock),
+                       lds, s, a);
     return hipGetLastError();
 }
 
 template <bool MOM, int GDT>
-hipError_t go_apply_p(const ApplyArgs &a, int pdt, bool vec, const Geometry &geo, hipStream_t s) {
-    if (pdt == PS_F32) return go_apply<MOM, GDT, PS_F32>(a, vec, geo, s);
-    if (pdt == PS_BF16) return go_apply<MOM, GDT, PS_BF16>(a, vec, geo, s);
-    return go_apply<MOM, GDT, -1>(a, vec, geo, s);
+hipError_t go_apply_p(const ApplyArgs &a, int pdt, int level, const Geometry &geo, hipStream_t s) {
+    if (pdt == PS_F32) return go_apply<MOM, GDT, PS_F32>(a, level, geo, s);
+    if (pdt == PS_BF16) return go_apply<MOM, GDT, PS_BF16>(a, level, geo, s);
+    return go_apply<MOM, GDT, -1>(a, level, geo, s);
 }
 
 template <bool MOM>
-hipError_t go_apply_g(const ApplyArgs &a, int gdt, int pdt, bool vec, const Geometry &geo,
+hipError_t go_apply_g(const ApplyArgs &a, int gdt, int pdt, int level, const Geometry &geo,
                       hipStream_t s) {
-    if (gdt == PS_BF16) return go_apply_p<MOM, PS_BF16>(a, pdt, vec, geo, s);
-    return go_apply_p<MOM, PS_F32>(a, pdt, vec, geo, s);
+    if (gdt == PS_BF16) return go_apply_p<MOM, PS_BF16>(a, pdt, level, geo, s);
+    return go_apply_p<MOM, PS_F32>(a, pdt, level, geo, s);
 }
 
 }  // namespace
 
-hipError_t launch_apply(const ApplyArgs &a, int grad_dtype, int pull_dtype, bool vec,
+hipError_t launch_apply(const ApplyArgs &a, int grad_dtype, int pull_dtype, int level,
                         const Geometry &geo, hipStream_t s) {
     if (a.r == 0) pull_dtype = -1;
-    if (a.v != nullptr) return go_apply_g<true>(a, grad_dtype, pull_dtype, vec, geo, s);
-    return go_apply_g<false>(a, grad_dtype, pull_dtype, vec, geo, s);
+    if (a.v != nullptr) return go_apply_g<true>(a, grad_dtype, pull_dtype, level, geo, s);
+    return go_apply_g<false>(a, grad_dtype, pull_dtype, level, geo, s);
 }
 
-hipError_t launch_pull(const PullArgs &a, int pull_dtype, bool vec, const Geometry &geo,
-                       hipStream_t s) {
-    const uint64_t items = vec ? (a.n >> 2) : a.n;
-    const dim3 grid(grid_for(items, geo)), block(kBlock);
-    if (pull_dtype == PS_BF16) {
-        if (vec) hipLaunchKernelGGL(pull_vec<PS_BF16>, grid, block, 0, s, a);
-        else hipLaunchKernelGGL(pull_scalar<PS_BF16>, grid, block, 0, s, a);
-    } else {
-        if (vec) hipLaunchKernelGGL(pull_vec<PS_F32>, grid, block, 0, s, a);
-        else hipLaunchKernelGGL(pull_scalar<PS_F32>, grid, block, 0, s, a);
+template <int PDT, int E>
+void go_pull_tiled(const PullArgs &a, const Geometry &geo, hipStream_t s) {
+    // tiles * R * bpt blocks; a tile smaller than a full one needs fewer blocks
+    constexpr uint64_t kTileChunksE = kTileBytes / (4 * E);
+    const uint64_t chunks = a.n / E;
+    const uint64_t tiles = chunks == 0 ? 1 : (chunks + kTileChunksE - 1) / kTileChunksE;
+    const uint64_t per_tile = chunks < kTileChunksE ? chunks : kTileChunksE;
+    uint64_t bpt = (per_tile + 2 * kBlock - 1) / (2 * kBlock);
+    if (bpt < 1) bpt = 1;
+    if (bpt > kTileBlocks) bpt = kTileBlocks;
+    const uint64_t groups = tiles * static_cast<uint64_t>(a.r);
+    if (groups * bpt > kMaxBlocks) bpt = kMaxBlocks / groups;   // lanes stride further
+    if (bpt < 1) {
+        // more (tile, replica) pairs than a grid can hold: one pass per lane
+        hipLaunchKernelGGL(pull_vec<PDT>, dim3(grid_for(a.n >> 2, geo)), dim3(kBlock), 0, s, a);
+        return;
     }
+    hipLaunchKernelGGL((pull_tiled<PDT, E>), dim3(static_cast<unsigned>(groups * bpt)),
+                       dim3(kBlock), 0, s, a, static_cast<unsigned>(bpt));
+}
+
+template <int PDT>
+void go_pull(const PullArgs &a, int level, const Geometry &geo, hipStream_t s) {
+    if (level == 0) {
+        hipLaunchKernelGGL(pull_scalar<PDT>, dim3(grid_for(a.n, geo)), dim3(kBlock), 0, s, a);
+    } else if (a.r == 1) {
+        hipLaunchKernelGGL(pull_vec<PDT>, dim3(grid_for(a.n >> 2, geo)), dim3(kBlock), 0, s, a);
+    } else if (PDT == PS_BF16 && level == 2) {
+        go_pull_tiled<PDT, 8>(a, geo, s);
+    } else {
+        go_pull_tiled<PDT, 4>(a, geo, s);
+    }
+}
+
+hipError_t launch_pull(const PullArgs &a, int pull_dtype, int level, const Geometry &geo,
+                       hipStream_t s) {
+    if (pull_dtype == PS_BF16) go_pull<PS_BF16>(a, level, geo, s);
+    else go_pull<PS_F32>(a, level, geo, s);
     return hipGetLastError();
+}
+
+unsigned one_block_per_cu_lds() {
+    int dev = 0, per_cu = 0, per_block = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 0;
+    if (hipDeviceGetAttribute(&per_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) !=
+            hipSuccess ||
+        hipDeviceGetAttribute(&per_block, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) !=
+            hipSuccess)
+        return 0;
+    const unsigned want = static_cast<unsigned>(per_cu) / 2 + 1024;   // two blocks cannot fit
+    return want <= static_cast<unsigned>(per_block) ? want : 0;
 }
 
 hipError_t launch_zero(float *p, uint64_t n, hipStream_t s) {

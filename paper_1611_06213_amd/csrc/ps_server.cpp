@@ -53,8 +53,14 @@ struct PullKey {
 };
 
 bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
-size_t dsize(int dtype) { return dtype == PS_BF16 ? 2 : 4; }
-size_t valign(int dtype) { return dtype == PS_BF16 ? 8 : 16; }
+
+// Vector level a buffer allows (see launch_apply): 2 if 16-byte aligned, 1 if
+// a bf16 buffer is 8-byte aligned, else 0.
+int level_of(const void *p, int dtype) {
+    if (aligned(p, 16)) return 2;
+    if (dtype == PS_BF16 && aligned(p, 8)) return 1;
+    return 0;
+}
 
 }  // namespace
 
@@ -68,6 +74,7 @@ struct ps_server {
     hipStream_t stream = nullptr;
     int depth = PS_MAX_QUEUE_DEPTH / 2;
     bool pull_skip = true;
+    int fuse_max_r = 1;   // ps_apply_pull writes up to this many replicas in the apply pass
     gadei::Geometry geo;
 
     std::vector<PushDesc> queue;
@@ -197,10 +204,10 @@ int launch_queue(ps_server *ps, int pull_dtype, void *const *dsts, const std::ve
     while (start < q) {
         const int gdt = ps->queue[start].dtype;
         size_t end = start;
-        bool vec = true;
+        int level = 2;
         while (end < q && ps->queue[end].dtype == gdt) {
             a.g[end - start] = ps->queue[end].grad;
-            vec = vec && aligned(ps->queue[end].grad, valign(gdt));
+            level = std::min(level, level_of(ps->queue[end].grad, gdt));
             ++end;
         }
         a.k = static_cast<int>(end - start);
@@ -211,10 +218,10 @@ int launch_queue(ps_server *ps, int pull_dtype, void *const *dsts, const std::ve
             a.r = static_cast<int>(write.size());
             for (size_t j = 0; j < write.size(); ++j) {
                 a.dst[j] = dsts[write[j]];
-                vec = vec && aligned(a.dst[j], valign(pull_dtype));
+                level = std::min(level, level_of(a.dst[j], pull_dtype));
             }
         }
-        hipError_t e = gadei::launch_apply(a, gdt, pdt, vec, ps->geo, ps->stream);
+        hipError_t e = gadei::launch_apply(a, gdt, pdt, level, ps->geo, ps->stream);
         if (e != hipSuccess) return fail_hip(e, "apply kernel launch");
         start = end;
     }
@@ -228,12 +235,12 @@ int launch_pulls(ps_server *ps, void *const *dsts, int dtype, const std::vector<
     a.w = ps->w;
     a.n = ps->n;
     a.r = static_cast<int>(write.size());
-    bool vec = true;
+    int level = 2;
     for (size_t j = 0; j < write.size(); ++j) {
         a.dst[j] = dsts[write[j]];
-        vec = vec && aligned(a.dst[j], valign(dtype));
+        level = std::min(level, level_of(a.dst[j], dtype));
     }
-    hipError_t e = gadei::launch_pull(a, dtype, vec, ps->geo, ps->stream);
+    hipError_t e = gadei::launch_pull(a, dtype, level, ps->geo, ps->stream);
     if (e != hipSuccess) return fail_hip(e, "pull kernel launch");
     return PS_OK;
 }
@@ -275,6 +282,7 @@ ps_server *ps_create(size_t n_params, float lr, float momentum) {
         return nullptr;
     }
     ps->queue.reserve(PS_MAX_QUEUE_DEPTH);
+    ps->geo.occupancy_cap_lds = gadei::one_block_per_cu_lds();
     return ps;
 }
 
@@ -341,7 +349,13 @@ int ps_apply_pull(ps_server *ps, int n, const int *learner_ids, void *const *dst
     const uint64_t ts_after = ps->ts + ps->queue.size();
     if (int rc = plan_pulls(ps, n, learner_ids, dsts, dst_dtype, ts_after, write)) return rc;
     if (int rc = use_device(ps)) return rc;
-    if (int rc = launch_queue(ps, dst_dtype, dsts, write)) return rc;
+    if (static_cast<int>(write.size()) <= ps->fuse_max_r) {
+        if (int rc = launch_queue(ps, dst_dtype, dsts, write)) return rc;
+    } else {
+        static const std::vector<int> none;
+        if (int rc = launch_queue(ps, -1, nullptr, none)) return rc;
+        if (int rc = launch_pulls(ps, dsts, dst_dtype, write)) return rc;
+    }
     commit_apply(ps);
     commit_pulls(ps, n, learner_ids, dsts, dst_dtype, write);
     return PS_OK;
@@ -360,6 +374,14 @@ int ps_set_queue_depth(ps_server *ps, int depth) {
     if (static_cast<size_t>(depth) < ps->queue.size())
         return fail(PS_ESTATE, "%zu gradients pending, more than depth %d", ps->queue.size(), depth);
     ps->depth = depth;
+    return PS_OK;
+}
+
+int ps_set_pull_fusion(ps_server *ps, int max_replicas) {
+    if (int rc = check(ps)) return rc;
+    if (max_replicas < 0 || max_replicas > PS_MAX_REPLICAS)
+        return fail(PS_EINVAL, "fusion limit %d outside [0, %d]", max_replicas, PS_MAX_REPLICAS);
+    ps->fuse_max_r = max_replicas;
     return PS_OK;
 }
 

@@ -57,6 +57,7 @@ _SIGS = {
     "ps_set_stream": (ctypes.c_int, [_VP, _VP]),
     "ps_set_queue_depth": (ctypes.c_int, [_VP, ctypes.c_int]),
     "ps_set_pull_skip": (ctypes.c_int, [_VP, ctypes.c_int]),
+    "ps_set_pull_fusion": (ctypes.c_int, [_VP, ctypes.c_int]),
     "ps_set_weights": (ctypes.c_int, [_VP, _VP]),
     "ps_weights": (_VP, [_VP]),
     "ps_velocity": (_VP, [_VP]),
@@ -161,6 +162,10 @@ def ps_set_pull_skip(h: int, enabled: bool) -> int:
     return load_library().ps_set_pull_skip(h, 1 if enabled else 0)
 
 
+def ps_set_pull_fusion(h: int, max_replicas: int) -> int:
+    return load_library().ps_set_pull_fusion(h, max_replicas)
+
+
 def ps_set_weights(h: int, src_ptr: int) -> int:
     return load_library().ps_set_weights(h, src_ptr)
 
@@ -262,6 +267,9 @@ class ParameterServer:
 
     def set_pull_skip(self, enabled: bool) -> None:
         self._check(ps_set_pull_skip(self.h, enabled), "set_pull_skip")
+
+    def set_pull_fusion(self, max_replicas: int) -> None:
+        self._check(ps_set_pull_fusion(self.h, max_replicas), "set_pull_fusion")
 
     def set_queue_depth(self, depth: int) -> None:
         self._check(ps_set_queue_depth(self.h, depth), "set_queue_depth")

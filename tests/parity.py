@@ -42,14 +42,19 @@ def pull_rounds(learners: Sequence[int]) -> List[List[int]]:
 
 
 def gpu_replay(cfg: wl.Config, events, pool, w0, ranges: Sequence[Tuple[int, int]],
-               fused: bool = False, pull_skip: bool = True, stream=None):
+               fused: bool = False, pull_skip: bool = True, stream=None, fusion=None):
+    """fused: drive apply+pull through ps_apply_pull; fusion: the replica
+    count up to which that call writes replicas from the apply pass."""
     import torch
     srv = ps.ParameterServer(cfg.n, cfg.lr, cfg.momentum, queue_depth=cfg.depth)
     srv.set_pull_skip(pull_skip)
+    if fusion is not None:
+        srv.set_pull_fusion(fusion)
     srv.set_stream(stream or torch.cuda.current_stream())
     srv.set_weights(w0)
     rdt = torch.bfloat16 if cfg.pull_dtype == wl.BF16 else torch.float32
-    replicas = torch.zeros((cfg.replicas, cfg.n), dtype=rdt, device="cuda")
+    replicas = wl.Rows(cfg.replicas, cfg.n, rdt, "cuda")
+    replicas.buf.zero_()
     snaps, stale = [], []
 
     widths = [hi - lo for lo, hi in ranges]
@@ -57,8 +62,8 @@ def gpu_replay(cfg: wl.Config, events, pool, w0, ranges: Sequence[Tuple[int, int
     def snap(learners):
         # one gather and one device-to-host copy per pull event
         ls = list(dict.fromkeys(learners))
-        idx = torch.tensor(ls, device="cuda")
-        rows = np_bits(torch.cat([replicas[idx, lo:hi] for lo, hi in ranges], dim=1))
+        rows = np_bits(torch.stack([torch.cat([replicas[l][lo:hi] for lo, hi in ranges])
+                                    for l in ls]))
         d = {}
         for j, l in enumerate(ls):
             parts, off = [], 0
@@ -146,7 +151,7 @@ def oracle_replay(cfg: wl.Config, events, pool_slices, w0_slices, ranges, pull_s
 
 def host_inputs(cfg: wl.Config, pool, w0, ranges):
     """Slices of the device inputs for the oracle (same bits)."""
-    pool_slices = [[np_bits(pool[b, lo:hi]) for b in range(cfg.pool)] for lo, hi in ranges]
+    pool_slices = [[np_bits(pool[b][lo:hi]) for b in range(cfg.pool)] for lo, hi in ranges]
     w0_slices = [np_bits(w0[lo:hi]) for lo, hi in ranges]
     return pool_slices, w0_slices
 

@@ -45,18 +45,21 @@ def free(torch):
 SMALL_N = 3 * 65536 + 7   # several 256-lane tiles and a ragged tail
 
 
-@pytest.mark.parametrize("fused", [False, True], ids=["separate", "fused"])
+@pytest.mark.parametrize("fused,fusion", [(False, None), (True, None), (True, 64)],
+                         ids=["separate", "fused", "fused-one-pass"])
 @pytest.mark.parametrize("name", list(wl.CONFIGS))
-def test_workload_small_full_oracle(torch, name, fused):
+def test_workload_small_full_oracle(torch, name, fused, fusion):
     """Each workload's whole schedule at a reduced parameter count; the
-    oracle covers every coordinate."""
+    oracle covers every coordinate. "fused-one-pass" writes every replica
+    from the apply pass; "fused" uses the default (tiled fan-out after the
+    apply for more than one replica)."""
     cfg = wl.CONFIGS[name].scaled(SMALL_N, pool=min(wl.CONFIGS[name].pool, 64))
-    say(f"[small] {name} n={cfg.n} fused={fused}")
+    say(f"[small] {name} n={cfg.n} fused={fused} fusion={fusion}")
     ev = wl.schedule(cfg)
     pool = wl.make_pool(cfg, "cuda")
     w0 = wl.make_w0(cfg, "cuda")
     ranges = [(0, cfg.n)]
-    g = parity.gpu_replay(cfg, ev, pool, w0, ranges, fused=fused)
+    g = parity.gpu_replay(cfg, ev, pool, w0, ranges, fused=fused, fusion=fusion)
     ps_, w0s = parity.host_inputs(cfg, pool, w0, ranges)
     o = parity.oracle_replay(cfg, ev, ps_, w0s, ranges)
     assert parity.compare(g, o, ranges) == []
@@ -88,20 +91,21 @@ def _full_ranges(cfg):
     return r
 
 
-@pytest.mark.parametrize("fused", [True, False], ids=["fused", "separate"])
+@pytest.mark.parametrize("fused,fusion", [(True, None), (False, None), (True, 64)],
+                         ids=["fused", "separate", "fused-one-pass"])
 @pytest.mark.parametrize("name", list(wl.CONFIGS))
-def test_workload_full_size_sampled(torch, name, fused):
+def test_workload_full_size_sampled(torch, name, fused, fusion):
     """Each workload at its full size, in the launch configuration the
     benchmark uses; the oracle checks sampled coordinate ranges (head, tail
     with the ragged end, seeded interior blocks, tensor boundaries) of the
     weights, velocity and every replica after every pull event."""
     cfg = wl.CONFIGS[name]
-    say(f"[full] {name} n={cfg.n} fused={fused}")
+    say(f"[full] {name} n={cfg.n} fused={fused} fusion={fusion}")
     ev = wl.schedule(cfg)
     pool = wl.make_pool(cfg, "cuda")
     w0 = wl.make_w0(cfg, "cuda")
     ranges = _full_ranges(cfg)
-    g = parity.gpu_replay(cfg, ev, pool, w0, ranges, fused=fused)
+    g = parity.gpu_replay(cfg, ev, pool, w0, ranges, fused=fused, fusion=fusion)
     ps_, w0s = parity.host_inputs(cfg, pool, w0, ranges)
     del pool
     free(torch)
@@ -123,7 +127,7 @@ def test_mixed_bf16_quantisation_bound_vs_fp32_gradients(torch):
     w0 = wl.make_w0(cfg, "cuda")
     ranges = _full_ranges(cfg)
     g = parity.gpu_replay(cfg, ev, pool, w0, ranges, fused=True)
-    bf_slices = [[parity.np_bits(pool[b, lo:hi]) for b in range(cfg.pool)] for lo, hi in ranges]
+    bf_slices = [[parity.np_bits(pool[b][lo:hi]) for b in range(cfg.pool)] for lo, hi in ranges]
     del pool
     f32_slices = [[None] * cfg.pool for _ in ranges]
     for b in range(cfg.pool):
@@ -157,7 +161,7 @@ def test_mixed_bf16_quantisation_bound_vs_fp32_gradients(torch):
 
 # ---------------------------------------------------------------- edges
 
-def _run_edge(torch, n, k, momentum, gdt, pdt, offset_g=0, offset_d=0, seed=0, lr=0.01):
+def _run_edge(torch, n, k, momentum, gdt, pdt, offset_g=0, offset_d=0, seed=0, lr=0.01, fusion=None):
     """Push k gradients (optionally at element offsets that break vector
     alignment), apply+pull into two replicas, pull into a third, compare."""
     gen = torch.Generator(device="cuda")
@@ -170,6 +174,8 @@ def _run_edge(torch, n, k, momentum, gdt, pdt, offset_g=0, offset_d=0, seed=0, l
     dbig = torch.zeros(3, n + 8, dtype=ptd, device="cuda")
     dsts = [dbig[r, offset_d:offset_d + n] for r in range(3)]
     srv = ps.ParameterServer(n, lr, momentum, queue_depth=max(k, 1))
+    if fusion is not None:
+        srv.set_pull_fusion(fusion)
     srv.set_weights(w0)
     for j, gj in enumerate(grads):
         assert srv.push(j % 5, gj)
@@ -200,13 +206,14 @@ def test_edge_sizes(torch, n):
     for k in (1, 9):
         for momentum in (0.0, 0.9):
             for gdt, pdt in ((ps.PS_F32, ps.PS_F32), (ps.PS_BF16, ps.PS_BF16), (ps.PS_F32, ps.PS_BF16)):
-                _run_edge(torch, n, k, momentum, gdt, pdt, seed=n)
+                for fusion in (None, 2):
+                    _run_edge(torch, n, k, momentum, gdt, pdt, seed=n, fusion=fusion)
 
 
 @pytest.mark.parametrize("k", list(range(1, 18)) + [23, 31, 32, 33, 40, 47, 48, 63, 64])
 def test_edge_queue_depths(torch, k):
     _run_edge(torch, 10007, k, 0.9, ps.PS_F32, ps.PS_F32, seed=k)
-    _run_edge(torch, 10007, k, 0.0, ps.PS_BF16, ps.PS_BF16, seed=k)
+    _run_edge(torch, 10007, k, 0.0, ps.PS_BF16, ps.PS_BF16, seed=k, fusion=2)
 
 
 @pytest.mark.parametrize("og,od", [(1, 0), (0, 1), (2, 3), (4, 4), (3, 0)])
@@ -215,7 +222,32 @@ def test_misaligned_buffers_scalar_path(torch, og, od):
     take the scalar kernels and must give the same bits."""
     for gdt, pdt in ((ps.PS_F32, ps.PS_F32), (ps.PS_BF16, ps.PS_BF16)):
         for momentum in (0.0, 0.9):
-            _run_edge(torch, 20011, 5, momentum, gdt, pdt, offset_g=og, offset_d=od, seed=og * 7 + od)
+            for fusion in (None, 2):
+                _run_edge(torch, 20011, 5, momentum, gdt, pdt, offset_g=og, offset_d=od,
+                          seed=og * 7 + od, fusion=fusion)
+
+
+@pytest.mark.parametrize("r", [2, 3, 16, 64])
+def test_tiled_pull_many_tiles_ragged(torch, r):
+    """The tiled fan-out over several full tiles (8 MiB of w each), a partial
+    tile and a ragged tail: every replica equals w (fp32) or RNE(w) (bf16)."""
+    n = 2 * (8 << 20) // 4 + 1234567 + 3
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(r)
+    w0 = (torch.rand(n, generator=gen, device="cuda") - 0.5) * 0.1
+    srv = ps.ParameterServer(n, 0.01, 0.0, queue_depth=1)
+    srv.set_weights(w0)
+    w_host = parity.np_bits(w0)
+    for dt, tdt in ((ps.PS_F32, torch.float32), (ps.PS_BF16, torch.bfloat16)):
+        reps = wl.Rows(r, n, tdt, "cuda")
+        reps.buf.fill_(7.0)
+        srv.pull_many(list(range(r)), reps.rows)
+        srv.sync()
+        want = w_host if dt == ps.PS_F32 else orc.f32_to_bf16(w_host)
+        for j in range(r):
+            assert parity.bitwise(parity.np_bits(reps[j]), want), (dt, j)
+        del reps
+    srv.close()
 
 
 def test_lr_zero_and_zero_gradient(torch):
