@@ -125,3 +125,33 @@ void orc_pull_bf16(uint16_t *dst, const float *w, size_t n)
     for (size_t i = 0; i < n; ++i)
         dst[i] = orc_f32_to_bf16(w[i]);
 }
+
+/* Synchronous SGD step (Eq. "ssgd", Sec. 2.1): the server averages the
+ * lambda gradients it collected, one per learner, and takes one step of
+ * Eq. "gd" with the average. The sum runs in learner order 1..lambda from
+ * +0, then is divided by lambda (correctly rounded division), then the step.
+ * grads points at lambda gradient pointers of n values; is_bf16 says they hold
+ * bf16 bit patterns. With v non-NULL the heavy-ball form is used with the
+ * average as the gradient. */
+void orc_ssgd_step(float *w, float *v, const void *const *grads, int lambda, int is_bf16,
+                   size_t n, float lr, float m)
+{
+    for (size_t i = 0; i < n; ++i) {
+        float s = 0.0f;
+        for (int l = 0; l < lambda; ++l) {
+            float x = is_bf16 ? orc_bf16_to_f32(((const uint16_t *)grads[l])[i])
+                              : ((const float *)grads[l])[i];
+            s = s + x;
+        }
+        float avg = s / (float)lambda;
+        if (v != NULL) {
+            float t = m * v[i];
+            v[i] = t + avg;
+            float p = lr * v[i];
+            w[i] = w[i] - p;
+        } else {
+            float p = lr * avg;
+            w[i] = w[i] - p;
+        }
+    }
+}

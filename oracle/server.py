@@ -17,6 +17,10 @@ What it follows (GaDei, arXiv 1611.06213):
   * Sec. 4.1: a pull is skipped when the learner's copy already carries the
     server's timestamp.
 
+Synchronous SGD (Eq. "ssgd") is also provided: apply_sync() averages the
+pending gradients (one per learner), summed in queue order, and applies one
+update.
+
 Readings where the paper is silent (each also listed in the design notes):
   * one global FIFO in push-call order stands in for the per-learner queues;
   * a batch of K pending gradients is applied as K sequential steps, each over
@@ -81,8 +85,10 @@ def lib():
     L.orc_bf16_to_f32.restype = ctypes.c_float
     L.orc_f32_to_bf16.argtypes = [ctypes.c_float]
     L.orc_f32_to_bf16.restype = ctypes.c_uint16
+    L.orc_ssgd_step.argtypes = [fp, fp, ctypes.POINTER(ctypes.c_void_p), ctypes.c_int,
+                                ctypes.c_int, sz, fl, fl]
     for f in ("orc_step_f32", "orc_step_mom_f32", "orc_step_bf16", "orc_step_mom_bf16",
-              "orc_pull_f32", "orc_pull_bf16"):
+              "orc_pull_f32", "orc_pull_bf16", "orc_ssgd_step"):
         getattr(L, f).restype = None
     _lib = L
     return L
@@ -117,6 +123,20 @@ def step(w: np.ndarray, g: np.ndarray, lr: float, v: Optional[np.ndarray] = None
             L.orc_step_mom_bf16(_fp(w), _fp(v), _up(g), n, lr, momentum)
         else:
             L.orc_step_mom_f32(_fp(w), _fp(v), _fp(g), n, lr, momentum)
+
+
+def ssgd_step(w: np.ndarray, grads, lr: float, v: Optional[np.ndarray] = None,
+              momentum: float = 0.0) -> None:
+    """One synchronous step (Eq. "ssgd") in place: average of `grads` (all
+    float32, or all uint16 bf16 bit patterns) in list order, then one step."""
+    L = lib()
+    n = w.size
+    is_bf16 = grads[0].dtype == np.uint16
+    for g in grads:
+        assert g.size == n and (g.dtype == np.uint16) == is_bf16 and g.flags.c_contiguous
+    ptrs = (ctypes.c_void_p * len(grads))(*[g.ctypes.data for g in grads])
+    vp = _fp(v) if v is not None else None
+    L.orc_ssgd_step(_fp(w), vp, ptrs, len(grads), int(is_bf16), n, lr, momentum)
 
 
 def pull_copy(w: np.ndarray, dtype: int) -> np.ndarray:
@@ -184,6 +204,22 @@ class OracleServer:
             self.applied_order.append(learner)
             step(self.w, g, self.lr, self.v, self.momentum)
             self.ts += 1
+        self.queue = []
+        return OK
+
+    def apply_sync(self) -> int:
+        """Synchronous step over the pending gradients (Eq. "ssgd"): their
+        average, summed in queue order, applied as one update; the timestamp
+        grows by one. All pending gradients must share a dtype."""
+        if not self.queue:
+            return OK
+        if len({g.dtype for _, g, _ in self.queue}) != 1:
+            return EINVAL
+        for learner, _, lts in self.queue:
+            self.staleness.append(self.ts - lts)
+            self.applied_order.append(learner)
+        ssgd_step(self.w, [g for _, g, _ in self.queue], self.lr, self.v, self.momentum)
+        self.ts += 1
         self.queue = []
         return OK
 

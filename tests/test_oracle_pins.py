@@ -399,3 +399,120 @@ def test_set_depth_rules():
         s.push(0, np.zeros(2, np.float32))
     assert s.set_depth(2) == orc.ESTATE
     assert s.set_depth(3) == orc.OK
+
+
+# ------------------------------------------------ synchronous SGD (Eq. "ssgd")
+
+def exact_ssgd(w0, grads, lr, m=None, steps=1):
+    """Exact-rational reference of `steps` synchronous steps, each over the
+    same list of learner gradients: s = RNE(s + g_l) in order, avg = RNE(s/lambda),
+    then the (momentum) step with RNE after each operation."""
+    lr = F(float(np.float32(lr)))
+    w = [F(float(x)) for x in w0]
+    v = [F(0)] * len(w) if m is not None else None
+    mm = F(float(np.float32(m))) if m is not None else None
+    lam = len(grads)
+    for _ in range(steps):
+        for i in range(len(w)):
+            s = F(0)
+            for g in grads:
+                s = rne32(s + F(float(g[i])))
+            avg = rne32(s / lam)
+            if v is None:
+                p = rne32(lr * avg)
+            else:
+                t = rne32(mm * v[i])
+                v[i] = rne32(t + avg)
+                p = rne32(lr * v[i])
+            w[i] = rne32(w[i] - p)
+    return np.array([float(x) for x in w], np.float32), (
+        None if v is None else np.array([float(x) for x in v], np.float32))
+
+
+def run_sync(w0, grads, lr, m=0.0, steps=1):
+    s = orc.OracleServer(w0, lr, m, depth=64)
+    for _ in range(steps):
+        for l, g in enumerate(grads):
+            assert s.push(l, g) == orc.OK
+        assert s.apply_sync() == orc.OK
+    return s
+
+
+def test_ssgd_one_learner_is_an_asgd_step():
+    """lambda = 1: the average is the gradient itself (0 + g = g, g / 1 = g), so
+    Eq. "ssgd" reduces to one step of Eq. "asgd"."""
+    rng = np.random.default_rng(20)
+    w0 = rng.uniform(-0.05, 0.05, 5000).astype(np.float32)
+    g = rand_f32(rng, 5000, 0.01)
+    for m in (0.0, 0.9):
+        a = run_sync(w0, [g], 0.01, m, steps=3)
+        b = run_oracle(w0, [g, g, g], 0.01, m=m, depth=1)
+        assert np.array_equal(bits(a.w), bits(b.w))
+        assert a.ts == 3
+
+
+def test_ssgd_equal_gradients_power_of_two():
+    """lambda = 4 learners sending the same dyadic gradient: the sum is exact,
+    dividing by 4 is exact, so the sync step equals one step with g."""
+    w0 = np.array([1.0, -0.5, 0.75], np.float32)
+    g = np.array([2 ** -10, 3 * 2 ** -12, -2 ** -9], np.float32)
+    a = run_sync(w0, [g] * 4, 2 ** -7, steps=5)
+    expect = np.array([float(F(float(x)) - 5 * F(1, 2 ** 7) * F(float(y))) for x, y in zip(w0, g)])
+    assert np.array_equal(a.w.astype(np.float64), expect)
+
+
+def test_ssgd_closed_form_mean_of_learners():
+    """T sync steps with fixed per-learner gradients: w_T = w0 - T*lr*mean(g_l);
+    dyadic values with a representable mean make it bitwise."""
+    w0 = np.array([0.5, 0.25], np.float32)
+    gs = [np.array([2 ** -8, -2 ** -9], np.float32), np.array([3 * 2 ** -8, 2 ** -9], np.float32),
+          np.array([0.0, 2 ** -7], np.float32), np.array([2 ** -8, 0.0], np.float32)]
+    T, lr = 7, 2 ** -6
+    a = run_sync(w0, gs, lr, steps=T)
+    mean = [sum(F(float(g[i])) for g in gs) / 4 for i in range(2)]
+    expect = [float(F(float(w0[i])) - T * F(lr) * mean[i]) for i in range(2)]
+    assert list(a.w.astype(np.float64)) == expect
+
+
+@pytest.mark.parametrize("m", [None, 0.9])
+def test_ssgd_brute_force_every_learner_order(m):
+    """Every order of 5 learners' gradients on 8 coordinates, two steps: the
+    oracle equals the exact-rational evaluation with RNE after the sum of each
+    learner, the division and each step operation."""
+    rng = np.random.default_rng(21)
+    w0 = rng.uniform(-0.05, 0.05, 8).astype(np.float32)
+    grads = [rand_f32(rng, 8, 0.01) for _ in range(5)]
+    for perm in itertools.permutations(range(5)):
+        seq = [grads[p] for p in perm]
+        s = run_sync(w0, seq, 0.0123, m or 0.0, steps=2)
+        ew, ev = exact_ssgd(w0, seq, 0.0123, m, steps=2)
+        assert same_bits(s.w, ew), perm
+        if m is not None:
+            assert same_bits(s.v, ev), perm
+
+
+def test_ssgd_division_not_reciprocal():
+    """The average divides by lambda (one rounding); multiplying by a rounded
+    1/lambda differs on some inputs, so the brute-force test above would catch
+    that substitution."""
+    rng = np.random.default_rng(22)
+    xs = rand_f32(rng, 2000, 1.0)
+    div = [rne32(F(float(x)) / 3) for x in xs]
+    rec = [rne32(F(float(x)) * rne32(F(1, 3))) for x in xs]
+    assert any(a != b for a, b in zip(div, rec))
+
+
+def test_ssgd_bf16_and_mixed_dtypes():
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(23)
+    w0 = rng.uniform(-0.05, 0.05, 3000).astype(np.float32)
+    xs = [torch.from_numpy(rand_f32(rng, 3000, 1e-3)).to(torch.bfloat16) for _ in range(6)]
+    bbits = [x.view(torch.int16).numpy().view(np.uint16).copy() for x in xs]
+    wide = [x.float().numpy().copy() for x in xs]
+    a = run_sync(w0, bbits, 0.001, 0.9, steps=2)
+    b = run_sync(w0, wide, 0.001, 0.9, steps=2)
+    assert np.array_equal(bits(a.w), bits(b.w))
+    s = orc.OracleServer(w0, 0.001, depth=4)
+    s.push(0, bbits[0])
+    s.push(1, wide[1])
+    assert s.apply_sync() == orc.EINVAL
