@@ -162,12 +162,17 @@ def main():
     ap.add_argument("--mode", choices=["fused", "separate"], default="separate",
                     help="separate: ps_apply_pending + ps_pull_many (one kernel each, timed "
                          "apart); fused: ps_apply_pull (the same kernels above one replica)")
+    ap.add_argument("--apply", choices=["asgd", "sync"], default="asgd",
+                    help="asgd: the workload's K-gradient asynchronous applies; sync: one "
+                         "synchronous step (Eq. ssgd) per step over one gradient per learner")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=8.0)
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run a plain 1 GiB copy (known bytes) for counter calibration")
     args = ap.parse_args()
 
+    if args.apply == "sync" and args.mode == "fused":
+        ap.error("--apply sync runs apply and pull as separate calls (--mode separate)")
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the parameter server here runs on a single "
               "MI355X; multi-GPU sharding is a design note, not built.", file=sys.stderr)
@@ -182,6 +187,9 @@ def main():
         sys.exit(1)
     lib = ps.load_library()
     cfg = wl.CONFIGS[args.config]
+    if args.apply == "sync":
+        # one gradient per learner per step; every learner pulls after it
+        cfg = wl.dataclasses.replace(cfg, depth=cfg.learners)
     n, K, R = cfg.n, cfg.depth, cfg.replicas
     stream = torch.cuda.current_stream()
 
@@ -189,7 +197,11 @@ def main():
     w0 = wl.make_w0(cfg, "cuda")
     rdt = torch.bfloat16 if cfg.pull_dtype == wl.BF16 else torch.float32
     replicas = wl.Rows(R, n, rdt, "cuda")
-    plan = batches(cfg, wl)
+    if args.apply == "sync":
+        plan = [([(l, (s * cfg.learners + l) % cfg.pool) for l in range(cfg.learners)],
+                 list(range(cfg.replicas))) for s in range(cfg.pool)]
+    else:
+        plan = batches(cfg, wl)
     torch.cuda.synchronize()
 
     h = ps.ps_create(n, cfg.lr, cfg.momentum)
@@ -221,7 +233,7 @@ def main():
             if ev is not None:
                 ev[1].record(stream)
         else:
-            rc = lib.ps_apply_pending(h)
+            rc = lib.ps_apply_sync(h) if args.apply == "sync" else lib.ps_apply_pending(h)
             if ev is not None:
                 ev[1].record(stream)
             rc = rc or lib.ps_pull_many(h, r, ids, dptr, pdt)
@@ -252,7 +264,7 @@ def main():
     p_ms = (sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps) if args.mode == "separate" else 0.0
     gbps = step_bytes / elapsed / 1e9
     achieved = launch_bytes / (k_ms * 1e-3) / 1e9
-    label = f"{args.config}-{args.mode}"
+    label = f"{args.config}-{args.mode}" + ("-sync" if args.apply == "sync" else "")
     traffic = recorded_traffic(label)
 
     if args.calib_copy:
@@ -274,6 +286,7 @@ def main():
         cpu = cpu_baseline(cfg, pool, w0, round(sum(rs) / len(rs)), args.cpu_seconds)
 
     kern = ("ps_apply_pull (apply + pull kernels)" if args.mode == "fused"
+            else "sync_vec (synchronous step)" if args.apply == "sync"
             else "apply_vec (fused K-gradient apply)")
     pull_bytes = sum(r * n * (2 if pdt == wl.BF16 else 4) + 4 * n for r in rs) / args.steps
     out = {
@@ -295,7 +308,7 @@ def main():
                          f"lr={cfg.lr}, momentum={cfg.momentum}, {cfg.learners} learners, "
                          f"{args.mode} apply+pull"),
             "params": n, "queue_depth": K, "replicas_per_apply": round(sum(rs) / len(rs), 2),
-            "mode": args.mode,
+            "mode": args.mode, "apply": args.apply,
         },
         "gbps": round(gbps, 1),
         "pct_peak": round(100 * gbps / PEAK_GBPS, 2),

@@ -122,6 +122,16 @@ int ps_push_dtype(ps_server *ps, int learner_id, const void *grad, int dtype);
  * recorded (ps_last_staleness, ps_get_stats). An empty queue is a no-op. */
 int ps_apply_pending(ps_server *ps);
 
+/* Synchronous SGD step (Eq. "ssgd", Sec. 2.1): average the pending
+ * gradients -- the caller pushes one per learner, lambda in all -- summed per
+ * coordinate in push order from +0 and divided by their count (correctly
+ * rounded division), and apply the average as one step of Eq. "gd" (the
+ * heavy-ball form when momentum != 0). The timestamp grows by one; each
+ * gradient's staleness is recorded as for ps_apply_pending. All pending
+ * gradients must share one dtype (PS_EINVAL otherwise, nothing applied). An
+ * empty queue is a no-op. Asynchronous on the server's stream. */
+int ps_apply_sync(ps_server *ps);
+
 /* Pull: write the current weights into the learner's replica buffer
  * dst[n_params] (device, fp32). Asynchronous on the server's stream; the copy
  * sees every apply issued before it. Skipped (no device work) when the same

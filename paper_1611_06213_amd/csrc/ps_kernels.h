@@ -53,6 +53,9 @@ hipError_t launch_apply(const ApplyArgs &a, int grad_dtype, int pull_dtype, int 
                         const Geometry &geo, hipStream_t s);
 hipError_t launch_pull(const PullArgs &a, int pull_dtype, int level, const Geometry &geo,
                        hipStream_t s);
+// Synchronous step over a.k gradients of one dtype (no replicas).
+hipError_t launch_sync(const ApplyArgs &a, int grad_dtype, int level, const Geometry &geo,
+                       hipStream_t s);
 hipError_t launch_zero(float *p, uint64_t n, hipStream_t s);
 
 }  // namespace gadei

@@ -227,6 +227,66 @@ __device__ __forceinline__ void apply_chunk(const ApplyArgs &a, uint64_t i) {
     }
 }
 
+// Synchronous SGD (Eq. "ssgd"): the K pending gradients (one per learner)
+// are summed per coordinate in push order from +0, divided by K (correctly
+// rounded division), and the average is applied as one step. Same streams
+// and grouping as the apply; only the reduction differs.
+template <int GDT, int E, int G>
+__device__ __forceinline__ void sum_group(const ApplyArgs &a, int k0, uint64_t i, float (&s)[E]) {
+    float g[G][E];
+#pragma unroll
+    for (int j = 0; j < G; ++j) ld_grad<GDT, E>(g[j], a.g[k0 + j], i);
+#pragma unroll
+    for (int j = 0; j < G; ++j)
+#pragma unroll
+        for (int e = 0; e < E; ++e) s[e] = s[e] + g[j][e];
+}
+
+template <bool MOM, int GDT, int E>
+__device__ __forceinline__ void sync_chunk(const ApplyArgs &a, uint64_t i) {
+    float w[E], v[E], s[E];
+    ld_f32<E, kNtWV>(w, a.w + i);
+    if constexpr (MOM) ld_f32<E, kNtWV>(v, a.v + i);
+#pragma unroll
+    for (int e = 0; e < E; ++e) s[e] = 0.0f;
+    const int k = a.k;
+    int k0 = 0;
+    for (; k0 + kGroup <= k; k0 += kGroup) sum_group<GDT, E, kGroup>(a, k0, i, s);
+    if constexpr (kGroup > 8) {
+        if (k0 + 8 <= k) {
+            sum_group<GDT, E, 8>(a, k0, i, s);
+            k0 += 8;
+        }
+    }
+    if (k0 < k) {
+        float g[8][E];
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            if (k0 + j < k) ld_grad<GDT, E>(g[j], a.g[k0 + j], i);
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            if (k0 + j < k)
+#pragma unroll
+                for (int e = 0; e < E; ++e) s[e] = s[e] + g[j][e];
+    }
+    const float kf = static_cast<float>(k);
+    float avg[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) avg[e] = s[e] / kf;
+    step<MOM, E>(w, v, avg, a.lr, a.m);
+    st_f32<E, kNtWV>(a.w + i, w);
+    if constexpr (MOM) st_f32<E, kNtWV>(a.v + i, v);
+}
+
+template <bool MOM, int GDT, int E>
+__global__ void __launch_bounds__(kBlock) sync_vec(const ApplyArgs a) {
+    const uint64_t chunks = a.n / E;
+    const uint64_t tid = static_cast<uint64_t>(blockIdx.x) * kBlock + threadIdx.x;
+    const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kBlock;
+    for (uint64_t c = tid; c < chunks; c += stride) sync_chunk<MOM, GDT, E>(a, c * E);
+    if (tid < a.n - chunks * E) sync_chunk<MOM, GDT, 1>(a, chunks * E + tid);
+}
+
 // Vector path: lane t of the grid owns E-coordinate chunks t, t + stride, ...
 // The n mod E trailing coordinates go to the first lanes of the grid.
 template <bool MOM, int GDT, int PDT, int E>
@@ -357,6 +417,27 @@ hipError_t go_apply(const ApplyArgs &a, int level, const Geometry &geo, hipStrea
 }
 
 template <bool MOM, int GDT>
+hipError_t go_sync(const ApplyArgs &a, int level, const Geometry &geo, hipStream_t s) {
+    if (level == 0) {
+        hipLaunchKernelGGL((sync_vec<MOM, GDT, 1>), dim3(grid_for(a.n, geo)), dim3(kBlock), 0, s,
+                           a);
+        return hipGetLastError();
+    }
+    const unsigned lds =
+        (GDT == PS_F32 && a.k >= geo.occupancy_cap_min_k) ? geo.occupancy_cap_lds : 0;
+    if constexpr (GDT == PS_BF16) {
+        if (level == 2) {
+            hipLaunchKernelGGL((sync_vec<MOM, GDT, 8>), dim3(grid_for(a.n / 8, geo)),
+                               dim3(kBlock), lds, s, a);
+            return hipGetLastError();
+        }
+    }
+    hipLaunchKernelGGL((sync_vec<MOM, GDT, 4>), dim3(grid_for(a.n / 4, geo)), dim3(kBlock), lds,
+                       s, a);
+    return hipGetLastError();
+}
+
+template <bool MOM, int GDT>
 hipError_t go_apply_p(const ApplyArgs &a, int pdt, int level, const Geometry &geo, hipStream_t s) {
     if (pdt == PS_F32) return go_apply<MOM, GDT, PS_F32>(a, level, geo, s);
     if (pdt == PS_BF16) return go_apply<MOM, GDT, PS_BF16>(a, level, geo, s);
@@ -411,6 +492,16 @@ void go_pull(const PullArgs &a, int level, const Geometry &geo, hipStream_t s) {
     } else {
         go_pull_tiled<PDT, 4>(a, geo, s);
     }
+}
+
+hipError_t launch_sync(const ApplyArgs &a, int grad_dtype, int level, const Geometry &geo,
+                       hipStream_t s) {
+    if (a.v != nullptr) {
+        return grad_dtype == PS_BF16 ? go_sync<true, PS_BF16>(a, level, geo, s)
+                                     : go_sync<true, PS_F32>(a, level, geo, s);
+    }
+    return grad_dtype == PS_BF16 ? go_sync<false, PS_BF16>(a, level, geo, s)
+                                 : go_sync<false, PS_F32>(a, level, geo, s);
 }
 
 hipError_t launch_pull(const PullArgs &a, int pull_dtype, int level, const Geometry &geo,

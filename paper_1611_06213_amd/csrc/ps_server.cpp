@@ -326,6 +326,45 @@ int ps_apply_pending(ps_server *ps) {
     return PS_OK;
 }
 
+int ps_apply_sync(ps_server *ps) {
+    if (int rc = check(ps)) return rc;
+    if (ps->queue.empty()) return PS_OK;
+    const int gdt = ps->queue.front().dtype;
+    for (const PushDesc &d : ps->queue)
+        if (d.dtype != gdt) return fail(PS_EINVAL, "synchronous step needs one gradient dtype");
+    if (int rc = use_device(ps)) return rc;
+    gadei::ApplyArgs a;
+    std::memset(&a, 0, sizeof a);
+    a.w = ps->w;
+    a.v = ps->v;
+    a.n = ps->n;
+    a.lr = ps->lr;
+    a.m = ps->m;
+    a.k = static_cast<int>(ps->queue.size());
+    int level = 2;
+    for (size_t j = 0; j < ps->queue.size(); ++j) {
+        a.g[j] = ps->queue[j].grad;
+        level = std::min(level, level_of(a.g[j], gdt));
+    }
+    hipError_t e = gadei::launch_sync(a, gdt, level, ps->geo, ps->stream);
+    if (e != hipSuccess) return fail_hip(e, "synchronous step launch");
+    // one update: every gradient is applied at the same timestamp
+    ps->last_staleness.clear();
+    for (const PushDesc &d : ps->queue) {
+        const uint64_t u = ps->ts - d.learner_ts;
+        ps->last_staleness.push_back(static_cast<int64_t>(u));
+        ps->stats.staleness_sum += u;
+        ps->stats.staleness_max = std::max(ps->stats.staleness_max, u);
+        ps->stats.staleness_hist[std::min<uint64_t>(u, PS_STALENESS_BINS - 1)] += 1;
+    }
+    ps->ts += 1;
+    ps->stats.pushes_applied += ps->queue.size();
+    ps->stats.applies += 1;
+    ps->stats.timestamp = ps->ts;
+    ps->queue.clear();
+    return PS_OK;
+}
+
 int ps_pull_many(ps_server *ps, int n, const int *learner_ids, void *const *dsts, int dst_dtype) {
     if (int rc = check(ps)) return rc;
     std::vector<int> write;

@@ -49,6 +49,7 @@ _SIGS = {
     "ps_push": (ctypes.c_int, [_VP, ctypes.c_int, _VP]),
     "ps_push_dtype": (ctypes.c_int, [_VP, ctypes.c_int, _VP, ctypes.c_int]),
     "ps_apply_pending": (ctypes.c_int, [_VP]),
+    "ps_apply_sync": (ctypes.c_int, [_VP]),
     "ps_pull": (ctypes.c_int, [_VP, ctypes.c_int, _VP]),
     "ps_pull_many": (ctypes.c_int, [_VP, ctypes.c_int, ctypes.POINTER(ctypes.c_int),
                                     ctypes.POINTER(_VP), ctypes.c_int]),
@@ -134,6 +135,10 @@ def ps_push_dtype(h: int, learner_id: int, grad_ptr: int, dtype: int) -> int:
 
 def ps_apply_pending(h: int) -> int:
     return load_library().ps_apply_pending(h)
+
+
+def ps_apply_sync(h: int) -> int:
+    return load_library().ps_apply_sync(h)
 
 
 def ps_pull(h: int, learner_id: int, dst_ptr: int) -> int:
@@ -285,6 +290,10 @@ class ParameterServer:
 
     def apply_pending(self) -> None:
         self._check(ps_apply_pending(self.h), "apply_pending")
+        self._pending = []
+
+    def apply_sync(self) -> None:
+        self._check(ps_apply_sync(self.h), "apply_sync")
         self._pending = []
 
     def pull(self, learner: int, dst) -> None:

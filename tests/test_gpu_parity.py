@@ -413,3 +413,97 @@ def test_64bit_indexing_beyond_2_31_elements(torch):
     srv.close()
     del w0, grads, dst, w
     free(torch)
+
+
+# ---------------------------------------------------------------- SSGD
+
+def _run_sync(torch, n, lam, steps, momentum, gdt, offset=0, seed=0, lr=0.01):
+    """`steps` synchronous steps of `lam` learners (one gradient each), with a
+    pull of every learner after each step, against the oracle."""
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(3000 + seed)
+    gtd = torch.bfloat16 if gdt == ps.PS_BF16 else torch.float32
+    w0 = (torch.rand(n, generator=gen, device="cuda") - 0.5) * 0.1
+    big = (torch.randn(lam * steps, n + 8, generator=gen, device="cuda") * 1e-2).to(gtd)
+    grads = [big[j, offset:offset + n] for j in range(lam * steps)]
+    dst = torch.empty(n, device="cuda")
+    srv = ps.ParameterServer(n, lr, momentum, queue_depth=lam)
+    srv.set_weights(w0)
+    o = orc.OracleServer(parity.np_bits(w0), lr, momentum, depth=lam)
+    stale = []
+    for s in range(steps):
+        for l in range(lam):
+            g = grads[s * lam + l]
+            assert srv.push(l, g)
+            assert o.push(l, parity.np_bits(g)) == orc.OK
+        srv.apply_sync()
+        stale += srv.last_staleness()
+        assert o.apply_sync() == orc.OK
+        for l in range(lam):
+            srv.pull(l, dst)
+            o.pull(l, "d", orc.F32)
+    w = parity.np_bits(srv.weights_copy())
+    assert parity.bitwise(w, o.w), (n, lam, momentum, gdt, offset)
+    if momentum:
+        assert parity.bitwise(parity.np_bits(srv.velocity_copy()), o.v)
+    assert parity.bitwise(parity.np_bits(dst), o.w)
+    assert srv.timestamp == o.ts == steps and stale == o.staleness
+    srv.close()
+
+
+@pytest.mark.parametrize("lam", [1, 2, 3, 7, 8, 9, 15, 16, 17, 24, 31, 32, 33, 64])
+def test_sync_parity(torch, lam):
+    for momentum in (0.0, 0.9):
+        for gdt in (ps.PS_F32, ps.PS_BF16):
+            _run_sync(torch, 30011, lam, 3, momentum, gdt, seed=lam)
+
+
+@pytest.mark.parametrize("n", [1, 5, 8, 9, 4097, 2 * 1024 * 1024 + 3])
+def test_sync_sizes_and_alignment(torch, n):
+    for offset in (0, 1, 4):
+        for gdt in (ps.PS_F32, ps.PS_BF16):
+            _run_sync(torch, n, 16, 2, 0.9, gdt, offset=offset, seed=n + offset)
+
+
+def test_sync_rejects_mixed_dtypes(torch):
+    n = 1000
+    srv = ps.ParameterServer(n, 0.1, 0.0, queue_depth=4)
+    srv.push(0, torch.ones(n, device="cuda"))
+    srv.push(1, torch.ones(n, dtype=torch.bfloat16, device="cuda"))
+    assert ps.ps_apply_sync(srv.h) == ps.PS_EINVAL
+    assert srv.pending == 2 and srv.timestamp == 0
+    srv.apply_pending()
+    assert srv.timestamp == 2
+    srv.close()
+
+
+def test_sync_vgg16_shaped_full_size_sampled(torch):
+    """VGG-16 shape (138,357,544 parameters), 16 learners pushing one gradient
+    each per synchronous step, 6 steps, all pulling after each step; sampled
+    against the oracle."""
+    cfg = wl.CONFIGS["vgg16"]
+    pool = wl.make_pool(dataclasses.replace(cfg, pool=32), "cuda")
+    w0 = wl.make_w0(cfg, "cuda")
+    ranges = _full_ranges(cfg)
+    srv = ps.ParameterServer(cfg.n, cfg.lr, cfg.momentum, queue_depth=16)
+    srv.set_weights(w0)
+    reps = wl.Rows(16, cfg.n, torch.float32, "cuda")
+    steps = 6
+    for s in range(steps):
+        for l in range(16):
+            srv.push(l, pool[(s * 16 + l) % 32])
+        srv.apply_sync()
+        srv.pull_many(list(range(16)), reps.rows)
+    w = srv.weights_copy()
+    got = [parity.np_bits(w[lo:hi]) for lo, hi in ranges]
+    rep = [parity.np_bits(reps[7][lo:hi]) for lo, hi in ranges]
+    srv.close()
+    for r, (lo, hi) in enumerate(ranges):
+        o = orc.OracleServer(parity.np_bits(w0[lo:hi]), cfg.lr, cfg.momentum, depth=16)
+        for s in range(steps):
+            for l in range(16):
+                o.push(l, parity.np_bits(pool[(s * 16 + l) % 32][lo:hi]))
+            o.apply_sync()
+        assert parity.bitwise(got[r], o.w) and parity.bitwise(rep[r], o.w), (lo, hi)
+    del pool, reps
+    free(torch)
