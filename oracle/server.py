@@ -21,6 +21,16 @@ Synchronous SGD (Eq. "ssgd") is also provided: apply_sync() averages the
 pending gradients (one per learner), summed in queue order, and applies one
 update.
 
+Round-robin mode (set_queue_mode(ROUND_ROBIN, slots)) follows Sec. 4.1 more
+literally: every learner has its own FIFO with a fixed number of slots (the
+lambda single-producer single-consumer queues) and a push on a full one is
+refused (Lemma 1 per learner). The server visits the learners in increasing
+id order, cyclically, starting after the learner it served last, and takes
+one gradient per visit of a non-empty queue; an apply takes up to `depth`
+gradients this way. A synchronous step takes one gradient from every
+non-empty queue, summed in increasing learner order (Eq. "ssgd" sums over
+l = 1..lambda).
+
 Readings where the paper is silent (each also listed in the design notes):
   * one global FIFO in push-call order stands in for the per-learner queues;
   * a batch of K pending gradients is applied as K sequential steps, each over
@@ -43,6 +53,9 @@ import os
 from typing import Dict, List, Optional, Tuple
 
 import numpy as np
+
+FIFO = 0
+ROUND_ROBIN = 1
 
 OK = 0
 EINVAL = -1
@@ -186,41 +199,89 @@ class OracleServer:
         self.applied_order: List[int] = []    # learner of each applied push
         self.pulls = 0
         self.pulls_skipped = 0
+        self.mode = FIFO
+        self.slots = 0
+        self.per_learner: Dict[int, List[Tuple[int, np.ndarray, int]]] = {}
+        self.last_served = -1
+
+    def set_queue_mode(self, mode: int, slots: int = 1) -> int:
+        if mode not in (FIFO, ROUND_ROBIN) or not 1 <= slots <= MAX_DEPTH:
+            return EINVAL
+        if self.pending():
+            return ESTATE
+        self.mode, self.slots = mode, slots
+        return OK
 
     def pending(self) -> int:
+        if self.mode == ROUND_ROBIN:
+            return sum(len(q) for q in self.per_learner.values())
         return len(self.queue)
 
     def push(self, learner: int, grad: np.ndarray) -> int:
         if learner < 0:
             return EINVAL
+        entry = (learner, grad, self.learner_ts.get(learner, 0))
+        if self.mode == ROUND_ROBIN:
+            q = self.per_learner.setdefault(learner, [])
+            if len(q) == self.slots:
+                return EFULL
+            q.append(entry)
+            return OK
         if len(self.queue) == self.depth:
             return EFULL
-        self.queue.append((learner, grad, self.learner_ts.get(learner, 0)))
+        self.queue.append(entry)
         return OK
 
+    def _round_robin_batch(self) -> List[Tuple[int, np.ndarray, int]]:
+        """Visit learners in increasing id order, cyclically, starting after
+        the last one served; one gradient per visit; at most `depth`."""
+        batch = []
+        while len(batch) < self.depth:
+            waiting = sorted(l for l, q in self.per_learner.items() if q)
+            if not waiting:
+                break
+            after = [l for l in waiting if l > self.last_served]
+            nxt = after[0] if after else waiting[0]
+            batch.append(self.per_learner[nxt].pop(0))
+            self.last_served = nxt
+        return batch
+
     def apply_pending(self) -> int:
-        for learner, g, lts in self.queue:
+        if self.mode == ROUND_ROBIN:
+            batch = self._round_robin_batch()
+        else:
+            batch, self.queue = self.queue, []
+        for learner, g, lts in batch:
             self.staleness.append(self.ts - lts)
             self.applied_order.append(learner)
             step(self.w, g, self.lr, self.v, self.momentum)
             self.ts += 1
-        self.queue = []
         return OK
 
     def apply_sync(self) -> int:
-        """Synchronous step over the pending gradients (Eq. "ssgd"): their
-        average, summed in queue order, applied as one update; the timestamp
-        grows by one. All pending gradients must share a dtype."""
-        if not self.queue:
+        """Synchronous step (Eq. "ssgd"): the average of the pending gradients
+        (FIFO mode: all of them, in queue order; round-robin mode: the oldest
+        of every non-empty learner queue, in increasing learner order),
+        applied as one update; the timestamp grows by one. The gradients of
+        a step must share a dtype."""
+        if self.mode == ROUND_ROBIN:
+            batch = [self.per_learner[l][0] for l in sorted(self.per_learner) if self.per_learner[l]]
+        else:
+            batch = list(self.queue)
+        if not batch:
             return OK
-        if len({g.dtype for _, g, _ in self.queue}) != 1:
+        if len({g.dtype for _, g, _ in batch}) != 1:
             return EINVAL
-        for learner, _, lts in self.queue:
+        if self.mode == ROUND_ROBIN:
+            for l, _, _ in batch:
+                self.per_learner[l].pop(0)
+        else:
+            self.queue = []
+        for learner, _, lts in batch:
             self.staleness.append(self.ts - lts)
             self.applied_order.append(learner)
-        ssgd_step(self.w, [g for _, g, _ in self.queue], self.lr, self.v, self.momentum)
+        ssgd_step(self.w, [g for _, g, _ in batch], self.lr, self.v, self.momentum)
         self.ts += 1
-        self.queue = []
         return OK
 
     def pull(self, learner: int, dst_key, dtype: int = F32) -> bool:
@@ -238,7 +299,7 @@ class OracleServer:
     def set_depth(self, depth: int) -> int:
         if not 1 <= depth <= MAX_DEPTH:
             return EINVAL
-        if depth < len(self.queue):
+        if self.mode == FIFO and depth < len(self.queue):
             return ESTATE
         self.depth = depth
         return OK

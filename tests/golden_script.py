@@ -4,9 +4,10 @@ import os
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
 
 
-def load(name):
-    """Return (depth, ops, expect). ops: list of (op, learner|None, outcome)."""
-    depth, ops, expect = None, [], {}
+def load(name, with_mode=False):
+    """Return (depth, ops, expect) -- and the queue mode (None | ("rr", slots))
+    when with_mode. ops: list of (op, learner|None, outcome)."""
+    depth, ops, expect, mode = None, [], {}, None
     with open(os.path.join(GOLDEN, name)) as f:
         for raw in f:
             line = raw.split("#", 1)[0].strip()
@@ -15,6 +16,8 @@ def load(name):
             tok = line.split()
             if tok[0] == "depth":
                 depth = int(tok[1])
+            elif tok[0] == "mode":
+                mode = (tok[1], int(tok[2]))
             elif tok[0] == "expect":
                 key = tok[1]
                 if key == "pulls":
@@ -28,4 +31,6 @@ def load(name):
                 op = tok[0]
                 learner = int(tok[1]) if arrow > 1 else None
                 ops.append((op, learner, tok[arrow + 1]))
+    if with_mode:
+        return depth, ops, expect, mode
     return depth, ops, expect

@@ -516,3 +516,82 @@ def test_ssgd_bf16_and_mixed_dtypes():
     s.push(0, bbits[0])
     s.push(1, wide[1])
     assert s.apply_sync() == orc.EINVAL
+
+
+# ------------------------------------------------ round-robin per-learner queues
+
+def test_golden_round_robin_script():
+    """tests/golden/round_robin_k4.txt, worked by hand from Sec. 4.1 and
+    Lemma 1 / Theorem 2."""
+    depth, ops, expect, mode = golden_script.load("round_robin_k4.txt", with_mode=True)
+    s = orc.OracleServer(np.zeros(2, np.float32), 2.0 ** -4, 0.0, depth=depth)
+    assert s.set_queue_mode(orc.ROUND_ROBIN, mode[1]) == orc.OK
+    g = np.full(2, 0.5, np.float32)
+    rejected = 0
+    for op, l, outcome in ops:
+        if op == "push":
+            rc = s.push(l, g)
+            assert rc == {"ok": orc.OK, "full": orc.EFULL}[outcome]
+            rejected += rc == orc.EFULL
+        elif op == "apply":
+            s.apply_pending()
+        else:
+            assert s.pull(l, ("dst", l), orc.F32) == (outcome == "pulled")
+    assert s.applied_order == expect["order"]
+    assert s.staleness == expect["staleness"]
+    assert s.ts == expect["ts"][0]
+    assert (s.pulls, s.pulls_skipped, rejected) == (expect["pulls"], expect["skipped"], expect["rejected"])
+
+
+def test_round_robin_lemma1_theorem2_fairness():
+    """Random interleavings: each learner's queue stays within 0..slots and a
+    push on a full one is refused without effect (Lemma 1); every accepted
+    gradient is applied exactly once and a learner's gradients in push order
+    (Theorem 2); consecutive services cycle through the waiting learners
+    (no learner is served twice while another waits)."""
+    rng = np.random.default_rng(30)
+    for slots, depth in ((1, 1), (2, 4), (3, 8), (5, 64)):
+        s = orc.OracleServer(np.zeros(1, np.float32), 1.0, depth=depth)
+        s.set_queue_mode(orc.ROUND_ROBIN, slots)
+        pushed = {l: [] for l in range(6)}
+        tag = 0
+        for _ in range(800):
+            if rng.random() < 0.75:
+                l = int(rng.integers(0, 6))
+                before = s.pending()
+                rc = s.push(l, np.array([float(tag)], np.float32))
+                if rc == orc.OK:
+                    pushed[l].append(tag)
+                else:
+                    assert rc == orc.EFULL and s.pending() == before
+                    assert len(s.per_learner[l]) == slots
+                tag += 1
+            else:
+                waiting = sorted(l for l, q in s.per_learner.items() if q)
+                start = len(s.applied_order)
+                s.apply_pending()
+                served = s.applied_order[start:]
+                # the first len(waiting) services visit distinct learners
+                head = served[:len(waiting)]
+                assert len(set(head)) == len(head)
+            assert all(0 <= len(q) <= slots for q in s.per_learner.values())
+        while s.pending():
+            s.apply_pending()
+        # w = -sum of applied tags (lr 1, small integers: exact): each once
+        assert s.w[0] == -float(sum(sum(v) for v in pushed.values()))
+        assert s.ts == sum(len(v) for v in pushed.values())
+
+
+def test_round_robin_sync_one_per_learner_in_id_order():
+    """Round-robin mode, synchronous step: the oldest gradient of each learner,
+    summed in increasing learner id (Eq. "ssgd" sums l = 1..lambda)."""
+    s = orc.OracleServer(np.zeros(1, np.float32), 1.0, depth=8)
+    s.set_queue_mode(orc.ROUND_ROBIN, 2)
+    for l, x in ((2, 4.0), (0, 1.0), (2, 8.0), (1, 2.0)):
+        s.push(l, np.array([x], np.float32))
+    s.apply_sync()
+    assert s.applied_order == [0, 1, 2] and s.w[0] == -(1.0 + 2.0 + 4.0) / 3
+    assert s.pending() == 1 and s.ts == 1
+    s.apply_sync()
+    assert s.w[0] == np.float32(-(7.0 / 3)) - 8.0
+    assert s.set_queue_mode(orc.FIFO) == orc.OK
