@@ -73,6 +73,12 @@ enum {
 
 enum { PS_F32 = 0, PS_BF16 = 1 };
 
+/* Queue modes (ps_set_queue_mode). */
+enum {
+    PS_QUEUE_FIFO = 0,        /* one queue of `depth` slots, push-call order   */
+    PS_QUEUE_ROUND_ROBIN = 1  /* a queue per learner, served round-robin      */
+};
+
 #define PS_MAX_QUEUE_DEPTH 64   /* K: gradients folded by one apply         */
 #define PS_MAX_REPLICAS 64      /* replica buffers written by one pull call */
 #define PS_MAX_LEARNERS 65536   /* learner ids are 0 .. PS_MAX_LEARNERS-1   */
@@ -115,11 +121,13 @@ int ps_push(ps_server *ps, int learner_id, const void *grad);
  * gradient holds n_params 16-bit values). */
 int ps_push_dtype(ps_server *ps, int learner_id, const void *grad, int dtype);
 
-/* Apply every pending gradient, oldest first, each as one step of Eq.
- * "asgd", then empty the queue. Enqueues one kernel per run of equal-dtype
+/* Apply the pending gradients -- FIFO mode: all of them, oldest first;
+ * round-robin mode: up to `depth` in service order (ps_set_queue_mode) --
+ * each as one step of Eq. "asgd", and remove them from their queues. Enqueues one kernel per run of equal-dtype
  * gradients (one in the usual case) on the server's stream; returns without
  * waiting. The timestamp grows by the number applied; staleness of each is
- * recorded (ps_last_staleness, ps_get_stats). An empty queue is a no-op. */
+ * recorded (ps_last_staleness, ps_last_applied, ps_get_stats). With nothing
+ * pending no device work is done and the last-apply queries report 0. */
 int ps_apply_pending(ps_server *ps);
 
 /* Synchronous SGD step (Eq. "ssgd", Sec. 2.1): average the pending
@@ -161,9 +169,24 @@ int ps_set_pull_fusion(ps_server *ps, int max_replicas);
  * work. The caller orders it against work already on the previous stream. */
 int ps_set_stream(ps_server *ps, void *hip_stream);
 
-/* Queue depth K, 1..PS_MAX_QUEUE_DEPTH. PS_ESTATE if more gradients are
- * pending than the new depth. */
+/* Queue depth K, 1..PS_MAX_QUEUE_DEPTH: the FIFO's slots, and the most
+ * gradients one asynchronous apply takes. PS_ESTATE if (FIFO mode) more
+ * gradients are pending than the new depth. */
 int ps_set_queue_depth(ps_server *ps, int depth);
+
+/* Queue topology. PS_QUEUE_FIFO (default): one queue of `depth` slots in
+ * push-call order. PS_QUEUE_ROUND_ROBIN: each learner has its own queue of
+ * slots_per_learner slots (1..PS_MAX_QUEUE_DEPTH) -- the paper's lambda
+ * single-producer single-consumer queues with a fixed number of slots per
+ * learner (Sec. 4.1) -- and a push on a full one returns PS_EFULL (Lemma 1).
+ * The server visits learners in increasing id order, cyclically, starting
+ * after the learner it served last, and takes one gradient per visit of a
+ * non-empty queue (Sec. 4.1); an asynchronous apply takes up to `depth`
+ * gradients this way and leaves the rest queued. A synchronous step takes
+ * the oldest gradient of every waiting learner, in increasing id, and
+ * returns PS_ESTATE if more than PS_MAX_QUEUE_DEPTH learners wait. PS_ESTATE
+ * if any gradient is pending; slots_per_learner is ignored for FIFO. */
+int ps_set_queue_mode(ps_server *ps, int mode, int slots_per_learner);
 
 /* Enable (1) or disable (0) skipping of pulls that are already current. */
 int ps_set_pull_skip(ps_server *ps, int enabled);
@@ -183,10 +206,15 @@ size_t ps_num_params(const ps_server *ps);
 uint64_t ps_timestamp(const ps_server *ps);
 int ps_pending(const ps_server *ps);
 
-/* Staleness of each gradient applied by the most recent apply call, in the
- * order applied. Writes min(count, cap) values to out and returns count (or
+/* Staleness of each gradient applied by the most recent apply call
+ * (ps_apply_pending, ps_apply_pull, ps_apply_sync), in the order applied. Writes min(count, cap) values to out and returns count (or
  * a negative status). */
 int ps_last_staleness(const ps_server *ps, int64_t *out, int cap);
+
+/* Learner ids of the gradients applied by the most recent apply call, in
+ * the order applied. Writes min(count, cap) ids and returns count (or a
+ * negative status). */
+int ps_last_applied(const ps_server *ps, int *learner_ids, int cap);
 
 /* Block until all work enqueued by the server has completed. */
 int ps_sync(ps_server *ps);

@@ -1,11 +1,18 @@
 // Host side of the parameter server: the C ABI declared in include/ps.h.
 //
 // The host keeps the protocol state of the paper's server (Sec. 2.1, 4.1):
-// the FIFO of pushed gradients with its fixed number of slots, the scalar
+// the queued gradients with their fixed number of slots, the scalar
 // timestamp, each learner's timestamp and last pull, and the staleness
 // statistics. Device work is only ever enqueued on the server's stream:
-// ps_push moves no data, ps_apply_pending launches one fused kernel per run
-// of equal-dtype gradients, the pulls launch one fan-out.
+// ps_push moves no data, an apply launches one kernel per run of equal-dtype
+// gradients, a pull launches one fan-out.
+//
+// Queue modes. FIFO: one queue of `depth` slots in push-call order. Round
+// robin: every learner has its own queue of `slots` slots (the paper's lambda
+// single-producer single-consumer queues) and the server visits learners in
+// increasing id order, cyclically, starting after the learner it served
+// last, taking one gradient per visit (Sec. 4.1). Either way an apply takes a
+// "batch" of at most `depth` gradients, which the kernels fold in order.
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
@@ -13,7 +20,9 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <deque>
 #include <new>
+#include <set>
 #include <string>
 #include <vector>
 
@@ -77,11 +86,19 @@ struct ps_server {
     int fuse_max_r = 1;   // ps_apply_pull writes up to this many replicas in the apply pass
     gadei::Geometry geo;
 
-    std::vector<PushDesc> queue;
+    int mode = PS_QUEUE_FIFO;
+    std::vector<PushDesc> fifo;            // FIFO mode
+    int slots = 1;                         // round-robin mode: slots per learner
+    std::vector<std::deque<PushDesc>> rr;  // ... queue of each learner id
+    std::set<int> waiting;                 // ... ids whose queue is not empty
+    size_t rr_count = 0;
+    int last_served = -1;
+
     uint64_t ts = 0;
     std::vector<uint64_t> learner_ts;   // indexed by learner id, grown on demand
     std::vector<PullKey> last_pull;
     std::vector<int64_t> last_staleness;
+    std::vector<int> last_applied;
     ps_stats stats{};
 };
 
@@ -105,6 +122,10 @@ void grow(ps_server *ps, int id) {
     }
 }
 
+size_t pending(const ps_server *ps) {
+    return ps->mode == PS_QUEUE_FIFO ? ps->fifo.size() : ps->rr_count;
+}
+
 int use_device(const ps_server *ps) {
     int cur = -1;
     hipError_t e = hipGetDevice(&cur);
@@ -116,7 +137,84 @@ int use_device(const ps_server *ps) {
     return PS_OK;
 }
 
-// Which of the n requested pulls must write, after the queue (if fused) has
+// The gradients an apply takes, in the order it applies them, and how many
+// each learner queue gives (round-robin mode). Nothing is removed while
+// planning: consume() does that once the launch has succeeded.
+struct Batch {
+    std::vector<PushDesc> items;
+    std::vector<std::pair<int, int>> taken;   // (learner, count), round robin
+    int last_served = -1;
+};
+
+void plan_async(const ps_server *ps, Batch &b) {
+    b.items.clear();
+    b.taken.clear();
+    b.last_served = ps->last_served;
+    if (ps->mode == PS_QUEUE_FIFO) {
+        b.items = ps->fifo;
+        return;
+    }
+    std::vector<std::pair<int, size_t>> avail;   // (learner, queued), increasing id
+    for (int l : ps->waiting) avail.emplace_back(l, ps->rr[l].size());
+    std::vector<size_t> used(avail.size(), 0);
+    size_t left = ps->rr_count;
+    int cur = ps->last_served;
+    while (static_cast<int>(b.items.size()) < ps->depth && left > 0) {
+        // the next learner after `cur`, cyclically, whose queue still has one
+        size_t pick = avail.size();
+        for (size_t j = 0; j < avail.size(); ++j)
+            if (avail[j].first > cur && used[j] < avail[j].second) {
+                pick = j;
+                break;
+            }
+        if (pick == avail.size())
+            for (size_t j = 0; j < avail.size(); ++j)
+                if (used[j] < avail[j].second) {
+                    pick = j;
+                    break;
+                }
+        const int l = avail[pick].first;
+        b.items.push_back(ps->rr[l][used[pick]]);
+        ++used[pick];
+        --left;
+        cur = l;
+    }
+    for (size_t j = 0; j < avail.size(); ++j)
+        if (used[j]) b.taken.emplace_back(avail[j].first, static_cast<int>(used[j]));
+    b.last_served = cur;
+}
+
+// Synchronous step: FIFO takes every pending gradient in push order; round
+// robin the oldest gradient of every waiting learner, in increasing id.
+void plan_sync(const ps_server *ps, Batch &b) {
+    b.items.clear();
+    b.taken.clear();
+    b.last_served = ps->last_served;
+    if (ps->mode == PS_QUEUE_FIFO) {
+        b.items = ps->fifo;
+        return;
+    }
+    for (int l : ps->waiting) {
+        b.items.push_back(ps->rr[l].front());
+        b.taken.emplace_back(l, 1);
+    }
+}
+
+void consume(ps_server *ps, const Batch &b) {
+    if (ps->mode == PS_QUEUE_FIFO) {
+        ps->fifo.erase(ps->fifo.begin(), ps->fifo.begin() + b.items.size());
+        return;
+    }
+    for (const auto &t : b.taken) {
+        auto &q = ps->rr[t.first];
+        for (int i = 0; i < t.second; ++i) q.pop_front();
+        if (q.empty()) ps->waiting.erase(t.first);
+    }
+    ps->rr_count -= b.items.size();
+    ps->last_served = b.last_served;
+}
+
+// Which of the n requested pulls must write, after the batch (if fused) has
 // been applied and the timestamp is `ts_after`. A pull is skipped when the
 // same learner last pulled into the same buffer, same dtype, at ts_after
 // (Sec. 4.1); duplicates inside one call see the earlier entry's effect.
@@ -170,28 +268,34 @@ void commit_pulls(ps_server *ps, int n, const int *ids, void *const *dsts, int d
     }
 }
 
-// Staleness of each queued gradient when applied (Sec. 2.1), then advance
-// the timestamp and empty the queue.
-void commit_apply(ps_server *ps) {
-    ps->last_staleness.clear();
-    for (const PushDesc &d : ps->queue) {
-        const int64_t s = static_cast<int64_t>(ps->ts - d.learner_ts);
-        ps->last_staleness.push_back(s);
-        const uint64_t u = static_cast<uint64_t>(s);
-        ps->stats.staleness_sum += u;
-        ps->stats.staleness_max = std::max(ps->stats.staleness_max, u);
-        ps->stats.staleness_hist[std::min<uint64_t>(u, PS_STALENESS_BINS - 1)] += 1;
-        ps->ts += 1;
-    }
-    ps->stats.pushes_applied += ps->queue.size();
-    ps->stats.applies += 1;
-    ps->stats.timestamp = ps->ts;
-    ps->queue.clear();
+void record_staleness(ps_server *ps, const PushDesc &d, uint64_t at) {
+    const uint64_t u = at - d.learner_ts;
+    ps->last_staleness.push_back(static_cast<int64_t>(u));
+    ps->last_applied.push_back(d.learner);
+    ps->stats.staleness_sum += u;
+    ps->stats.staleness_max = std::max(ps->stats.staleness_max, u);
+    ps->stats.staleness_hist[std::min<uint64_t>(u, PS_STALENESS_BINS - 1)] += 1;
 }
 
-// Launch the queue as runs of equal gradient dtype, oldest first. The last
-// run also writes the replicas listed in `write` when pull_dtype >= 0.
-int launch_queue(ps_server *ps, int pull_dtype, void *const *dsts, const std::vector<int> &write) {
+// Asynchronous apply done: staleness of each gradient when applied (Sec.
+// 2.1), one timestamp step per gradient, and the batch leaves its queues.
+void commit_async(ps_server *ps, const Batch &b) {
+    ps->last_staleness.clear();
+    ps->last_applied.clear();
+    for (const PushDesc &d : b.items) {
+        record_staleness(ps, d, ps->ts);
+        ps->ts += 1;
+    }
+    ps->stats.pushes_applied += b.items.size();
+    ps->stats.applies += 1;
+    ps->stats.timestamp = ps->ts;
+    consume(ps, b);
+}
+
+// Launch a batch as runs of equal gradient dtype, in order. The last run
+// also writes the replicas listed in `write` when pull_dtype >= 0.
+int launch_batch(ps_server *ps, const std::vector<PushDesc> &items, int pull_dtype,
+                 void *const *dsts, const std::vector<int> &write) {
     gadei::ApplyArgs a;
     std::memset(&a, 0, sizeof a);
     a.w = ps->w;
@@ -199,15 +303,15 @@ int launch_queue(ps_server *ps, int pull_dtype, void *const *dsts, const std::ve
     a.n = ps->n;
     a.lr = ps->lr;
     a.m = ps->m;
-    const size_t q = ps->queue.size();
+    const size_t q = items.size();
     size_t start = 0;
     while (start < q) {
-        const int gdt = ps->queue[start].dtype;
+        const int gdt = items[start].dtype;
         size_t end = start;
         int level = 2;
-        while (end < q && ps->queue[end].dtype == gdt) {
-            a.g[end - start] = ps->queue[end].grad;
-            level = std::min(level, level_of(ps->queue[end].grad, gdt));
+        while (end < q && items[end].dtype == gdt) {
+            a.g[end - start] = items[end].grad;
+            level = std::min(level, level_of(items[end].grad, gdt));
             ++end;
         }
         a.k = static_cast<int>(end - start);
@@ -243,6 +347,13 @@ int launch_pulls(ps_server *ps, void *const *dsts, int dtype, const std::vector<
     hipError_t e = gadei::launch_pull(a, dtype, level, ps->geo, ps->stream);
     if (e != hipSuccess) return fail_hip(e, "pull kernel launch");
     return PS_OK;
+}
+
+// An apply with nothing to apply launches nothing; the last-apply queries
+// then report an empty apply.
+void clear_last(ps_server *ps) {
+    ps->last_staleness.clear();
+    ps->last_applied.clear();
 }
 
 }  // namespace
@@ -281,7 +392,7 @@ ps_server *ps_create(size_t n_params, float lr, float momentum) {
         delete ps;
         return nullptr;
     }
-    ps->queue.reserve(PS_MAX_QUEUE_DEPTH);
+    ps->fifo.reserve(PS_MAX_QUEUE_DEPTH);
     ps->geo.occupancy_cap_lds = gadei::one_block_per_cu_lds();
     return ps;
 }
@@ -301,13 +412,26 @@ int ps_push_dtype(ps_server *ps, int learner_id, const void *grad, int dtype) {
     if (int rc = check_learner(learner_id)) return rc;
     if (grad == nullptr) return fail(PS_EINVAL, "null gradient");
     if (dtype != PS_F32 && dtype != PS_BF16) return fail(PS_EINVAL, "bad gradient dtype %d", dtype);
-    if (static_cast<int>(ps->queue.size()) >= ps->depth) {
-        ps->stats.pushes_rejected += 1;
-        return fail(PS_EFULL, "queue full (%d pending)", ps->depth);
-    }
     const uint64_t lts =
         static_cast<size_t>(learner_id) < ps->learner_ts.size() ? ps->learner_ts[learner_id] : 0;
-    ps->queue.push_back(PushDesc{learner_id, dtype, grad, lts});
+    const PushDesc d{learner_id, dtype, grad, lts};
+    if (ps->mode == PS_QUEUE_FIFO) {
+        if (static_cast<int>(ps->fifo.size()) >= ps->depth) {
+            ps->stats.pushes_rejected += 1;
+            return fail(PS_EFULL, "queue full (%d pending)", ps->depth);
+        }
+        ps->fifo.push_back(d);
+    } else {
+        if (static_cast<size_t>(learner_id) >= ps->rr.size()) ps->rr.resize(learner_id + 1);
+        auto &q = ps->rr[learner_id];
+        if (static_cast<int>(q.size()) >= ps->slots) {
+            ps->stats.pushes_rejected += 1;
+            return fail(PS_EFULL, "learner %d queue full (%d slots)", learner_id, ps->slots);
+        }
+        q.push_back(d);
+        ps->waiting.insert(learner_id);
+        ps->rr_count += 1;
+    }
     ps->stats.pushes_accepted += 1;
     return PS_OK;
 }
@@ -318,19 +442,32 @@ int ps_push(ps_server *ps, int learner_id, const void *grad) {
 
 int ps_apply_pending(ps_server *ps) {
     if (int rc = check(ps)) return rc;
-    if (ps->queue.empty()) return PS_OK;
+    if (pending(ps) == 0) {
+        clear_last(ps);
+        return PS_OK;
+    }
     if (int rc = use_device(ps)) return rc;
+    Batch b;
+    plan_async(ps, b);
     static const std::vector<int> none;
-    if (int rc = launch_queue(ps, -1, nullptr, none)) return rc;
-    commit_apply(ps);
+    if (int rc = launch_batch(ps, b.items, -1, nullptr, none)) return rc;
+    commit_async(ps, b);
     return PS_OK;
 }
 
 int ps_apply_sync(ps_server *ps) {
     if (int rc = check(ps)) return rc;
-    if (ps->queue.empty()) return PS_OK;
-    const int gdt = ps->queue.front().dtype;
-    for (const PushDesc &d : ps->queue)
+    if (pending(ps) == 0) {
+        clear_last(ps);
+        return PS_OK;
+    }
+    Batch b;
+    plan_sync(ps, b);
+    if (b.items.size() > PS_MAX_QUEUE_DEPTH)
+        return fail(PS_ESTATE, "%zu learners waiting, more than one step can average (%d)",
+                    b.items.size(), PS_MAX_QUEUE_DEPTH);
+    const int gdt = b.items.front().dtype;
+    for (const PushDesc &d : b.items)
         if (d.dtype != gdt) return fail(PS_EINVAL, "synchronous step needs one gradient dtype");
     if (int rc = use_device(ps)) return rc;
     gadei::ApplyArgs a;
@@ -340,28 +477,23 @@ int ps_apply_sync(ps_server *ps) {
     a.n = ps->n;
     a.lr = ps->lr;
     a.m = ps->m;
-    a.k = static_cast<int>(ps->queue.size());
+    a.k = static_cast<int>(b.items.size());
     int level = 2;
-    for (size_t j = 0; j < ps->queue.size(); ++j) {
-        a.g[j] = ps->queue[j].grad;
+    for (size_t j = 0; j < b.items.size(); ++j) {
+        a.g[j] = b.items[j].grad;
         level = std::min(level, level_of(a.g[j], gdt));
     }
     hipError_t e = gadei::launch_sync(a, gdt, level, ps->geo, ps->stream);
     if (e != hipSuccess) return fail_hip(e, "synchronous step launch");
     // one update: every gradient is applied at the same timestamp
     ps->last_staleness.clear();
-    for (const PushDesc &d : ps->queue) {
-        const uint64_t u = ps->ts - d.learner_ts;
-        ps->last_staleness.push_back(static_cast<int64_t>(u));
-        ps->stats.staleness_sum += u;
-        ps->stats.staleness_max = std::max(ps->stats.staleness_max, u);
-        ps->stats.staleness_hist[std::min<uint64_t>(u, PS_STALENESS_BINS - 1)] += 1;
-    }
+    ps->last_applied.clear();
+    for (const PushDesc &d : b.items) record_staleness(ps, d, ps->ts);
     ps->ts += 1;
-    ps->stats.pushes_applied += ps->queue.size();
+    ps->stats.pushes_applied += b.items.size();
     ps->stats.applies += 1;
     ps->stats.timestamp = ps->ts;
-    ps->queue.clear();
+    consume(ps, b);
     return PS_OK;
 }
 
@@ -383,19 +515,25 @@ int ps_pull(ps_server *ps, int learner_id, void *dst) {
 
 int ps_apply_pull(ps_server *ps, int n, const int *learner_ids, void *const *dsts, int dst_dtype) {
     if (int rc = check(ps)) return rc;
-    if (ps->queue.empty()) return ps_pull_many(ps, n, learner_ids, dsts, dst_dtype);
+    if (pending(ps) == 0) {
+        const int rc = ps_pull_many(ps, n, learner_ids, dsts, dst_dtype);
+        if (rc == PS_OK) clear_last(ps);
+        return rc;
+    }
+    Batch b;
+    plan_async(ps, b);
     std::vector<int> write;
-    const uint64_t ts_after = ps->ts + ps->queue.size();
+    const uint64_t ts_after = ps->ts + b.items.size();
     if (int rc = plan_pulls(ps, n, learner_ids, dsts, dst_dtype, ts_after, write)) return rc;
     if (int rc = use_device(ps)) return rc;
     if (static_cast<int>(write.size()) <= ps->fuse_max_r) {
-        if (int rc = launch_queue(ps, dst_dtype, dsts, write)) return rc;
+        if (int rc = launch_batch(ps, b.items, dst_dtype, dsts, write)) return rc;
     } else {
         static const std::vector<int> none;
-        if (int rc = launch_queue(ps, -1, nullptr, none)) return rc;
+        if (int rc = launch_batch(ps, b.items, -1, nullptr, none)) return rc;
         if (int rc = launch_pulls(ps, dsts, dst_dtype, write)) return rc;
     }
-    commit_apply(ps);
+    commit_async(ps, b);
     commit_pulls(ps, n, learner_ids, dsts, dst_dtype, write);
     return PS_OK;
 }
@@ -410,9 +548,23 @@ int ps_set_queue_depth(ps_server *ps, int depth) {
     if (int rc = check(ps)) return rc;
     if (depth < 1 || depth > PS_MAX_QUEUE_DEPTH)
         return fail(PS_EINVAL, "queue depth %d outside [1, %d]", depth, PS_MAX_QUEUE_DEPTH);
-    if (static_cast<size_t>(depth) < ps->queue.size())
-        return fail(PS_ESTATE, "%zu gradients pending, more than depth %d", ps->queue.size(), depth);
+    if (ps->mode == PS_QUEUE_FIFO && static_cast<size_t>(depth) < ps->fifo.size())
+        return fail(PS_ESTATE, "%zu gradients pending, more than depth %d", ps->fifo.size(), depth);
     ps->depth = depth;
+    return PS_OK;
+}
+
+int ps_set_queue_mode(ps_server *ps, int mode, int slots_per_learner) {
+    if (int rc = check(ps)) return rc;
+    if (mode != PS_QUEUE_FIFO && mode != PS_QUEUE_ROUND_ROBIN)
+        return fail(PS_EINVAL, "bad queue mode %d", mode);
+    if (mode == PS_QUEUE_ROUND_ROBIN &&
+        (slots_per_learner < 1 || slots_per_learner > PS_MAX_QUEUE_DEPTH))
+        return fail(PS_EINVAL, "slots per learner %d outside [1, %d]", slots_per_learner,
+                    PS_MAX_QUEUE_DEPTH);
+    if (pending(ps) != 0) return fail(PS_ESTATE, "gradients pending");
+    ps->mode = mode;
+    if (mode == PS_QUEUE_ROUND_ROBIN) ps->slots = slots_per_learner;
     return PS_OK;
 }
 
@@ -433,7 +585,7 @@ int ps_set_pull_skip(ps_server *ps, int enabled) {
 int ps_set_weights(ps_server *ps, const float *src) {
     if (int rc = check(ps)) return rc;
     if (src == nullptr) return fail(PS_EINVAL, "null source");
-    if (!ps->queue.empty()) return fail(PS_ESTATE, "gradients pending");
+    if (pending(ps) != 0) return fail(PS_ESTATE, "gradients pending");
     if (int rc = use_device(ps)) return rc;
     hipError_t e = hipMemcpyAsync(ps->w, src, ps->n * sizeof(float), hipMemcpyDeviceToDevice,
                                   ps->stream);
@@ -446,6 +598,8 @@ int ps_set_weights(ps_server *ps, const float *src) {
     ps->learner_ts.clear();
     ps->last_pull.clear();
     ps->last_staleness.clear();
+    ps->last_applied.clear();
+    ps->last_served = -1;
     ps->stats = ps_stats{};
     return PS_OK;
 }
@@ -457,7 +611,7 @@ uint64_t ps_timestamp(const ps_server *ps) { return ps ? ps->ts : 0; }
 
 int ps_pending(const ps_server *ps) {
     if (int rc = check(ps)) return rc;
-    return static_cast<int>(ps->queue.size());
+    return static_cast<int>(pending(ps));
 }
 
 int ps_last_staleness(const ps_server *ps, int64_t *out, int cap) {
@@ -465,6 +619,14 @@ int ps_last_staleness(const ps_server *ps, int64_t *out, int cap) {
     if (cap < 0 || (cap > 0 && out == nullptr)) return fail(PS_EINVAL, "bad output buffer");
     const int count = static_cast<int>(ps->last_staleness.size());
     for (int i = 0; i < count && i < cap; ++i) out[i] = ps->last_staleness[i];
+    return count;
+}
+
+int ps_last_applied(const ps_server *ps, int *learner_ids, int cap) {
+    if (int rc = check(ps)) return rc;
+    if (cap < 0 || (cap > 0 && learner_ids == nullptr)) return fail(PS_EINVAL, "bad output buffer");
+    const int count = static_cast<int>(ps->last_applied.size());
+    for (int i = 0; i < count && i < cap; ++i) learner_ids[i] = ps->last_applied[i];
     return count;
 }
 

@@ -21,6 +21,9 @@ PS_ESTATE = -5
 PS_F32 = 0
 PS_BF16 = 1
 
+PS_QUEUE_FIFO = 0
+PS_QUEUE_ROUND_ROBIN = 1
+
 PS_MAX_QUEUE_DEPTH = 64
 PS_MAX_REPLICAS = 64
 PS_MAX_LEARNERS = 65536
@@ -58,6 +61,8 @@ _SIGS = {
     "ps_set_stream": (ctypes.c_int, [_VP, _VP]),
     "ps_set_queue_depth": (ctypes.c_int, [_VP, ctypes.c_int]),
     "ps_set_pull_skip": (ctypes.c_int, [_VP, ctypes.c_int]),
+    "ps_set_queue_mode": (ctypes.c_int, [_VP, ctypes.c_int, ctypes.c_int]),
+    "ps_last_applied": (ctypes.c_int, [_VP, ctypes.POINTER(ctypes.c_int), ctypes.c_int]),
     "ps_set_pull_fusion": (ctypes.c_int, [_VP, ctypes.c_int]),
     "ps_set_weights": (ctypes.c_int, [_VP, _VP]),
     "ps_weights": (_VP, [_VP]),
@@ -167,6 +172,18 @@ def ps_set_pull_skip(h: int, enabled: bool) -> int:
     return load_library().ps_set_pull_skip(h, 1 if enabled else 0)
 
 
+def ps_set_queue_mode(h: int, mode: int, slots_per_learner: int = 1) -> int:
+    return load_library().ps_set_queue_mode(h, mode, slots_per_learner)
+
+
+def ps_last_applied(h: int, cap: int = PS_MAX_QUEUE_DEPTH):
+    out = (ctypes.c_int * cap)()
+    n = load_library().ps_last_applied(h, out, cap)
+    if n < 0:
+        return n
+    return [int(out[i]) for i in range(min(n, cap))]
+
+
 def ps_set_pull_fusion(h: int, max_replicas: int) -> int:
     return load_library().ps_set_pull_fusion(h, max_replicas)
 
@@ -272,6 +289,12 @@ class ParameterServer:
 
     def set_pull_skip(self, enabled: bool) -> None:
         self._check(ps_set_pull_skip(self.h, enabled), "set_pull_skip")
+
+    def set_queue_mode(self, mode: int, slots_per_learner: int = 1) -> None:
+        self._check(ps_set_queue_mode(self.h, mode, slots_per_learner), "set_queue_mode")
+
+    def last_applied(self):
+        return ps_last_applied(self.h)
 
     def set_pull_fusion(self, max_replicas: int) -> None:
         self._check(ps_set_pull_fusion(self.h, max_replicas), "set_pull_fusion")

@@ -39,7 +39,7 @@ def test_every_declared_symbol_is_exported(lib):
 def test_header_constants_match_binding():
     text = open(os.path.join(ROOT, "include", "ps.h")).read()
     for name in ("PS_OK", "PS_EINVAL", "PS_EFULL", "PS_ENOMEM", "PS_EHIP", "PS_ESTATE",
-                 "PS_F32", "PS_BF16"):
+                 "PS_F32", "PS_BF16", "PS_QUEUE_FIFO", "PS_QUEUE_ROUND_ROBIN"):
         m = re.search(rf"\b{name}\s*=\s*(-?\d+)", text)
         assert m and int(m.group(1)) == getattr(ps, name), name
     for name in ("PS_MAX_QUEUE_DEPTH", "PS_MAX_REPLICAS", "PS_MAX_LEARNERS", "PS_STALENESS_BINS"):

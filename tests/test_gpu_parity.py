@@ -507,3 +507,102 @@ def test_sync_vgg16_shaped_full_size_sampled(torch):
         assert parity.bitwise(got[r], o.w) and parity.bitwise(rep[r], o.w), (lo, hi)
     del pool, reps
     free(torch)
+
+
+# ---------------------------------------------------------------- round robin
+
+def test_golden_round_robin_through_abi(torch):
+    """tests/golden/round_robin_k4.txt through the C ABI: service order, per-
+    learner slot limit, staleness, counters."""
+    depth, ops, expect, mode = golden_script.load("round_robin_k4.txt", with_mode=True)
+    n = 4
+    g = torch.full((n,), 0.5, device="cuda")
+    dsts = {l: torch.empty(n, device="cuda") for l in range(3)}
+    srv = ps.ParameterServer(n, 2.0 ** -4, 0.0, queue_depth=depth)
+    srv.set_queue_mode(ps.PS_QUEUE_ROUND_ROBIN, mode[1])
+    srv.set_weights(torch.zeros(n, device="cuda"))
+    order, stale = [], []
+    for op, l, outcome in ops:
+        if op == "push":
+            assert srv.push(l, g) == (outcome == "ok")
+        elif op == "apply":
+            srv.apply_pending()
+            order += srv.last_applied()
+            stale += srv.last_staleness()
+        else:
+            srv.pull(l, dsts[l])
+    st = srv.stats()
+    assert order == expect["order"] and stale == expect["staleness"]
+    assert srv.timestamp == expect["ts"][0]
+    assert (st.pulls, st.pulls_skipped, st.pushes_rejected) == (
+        expect["pulls"], expect["skipped"], expect["rejected"])
+    srv.close()
+
+
+@pytest.mark.parametrize("slots,depth", [(1, 1), (2, 4), (3, 5), (4, 16), (8, 64)])
+def test_round_robin_random_vs_oracle(torch, slots, depth):
+    """Random pushes (some refused), asynchronous applies, synchronous steps
+    and pulls in round-robin mode with momentum: weights, velocity, service
+    order, staleness and refusals equal the oracle's, bit for bit."""
+    n = 50001
+    lam = 6
+    rng = np.random.default_rng(slots * 100 + depth)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(slots * 100 + depth)
+    w0 = (torch.rand(n, generator=gen, device="cuda") - 0.5) * 0.1
+    pool = [torch.randn(n, generator=gen, device="cuda") * 1e-2 for _ in range(24)]
+    host = [parity.np_bits(p) for p in pool]
+    dst = torch.empty(n, device="cuda")
+    srv = ps.ParameterServer(n, 0.01, 0.9, queue_depth=depth)
+    srv.set_queue_mode(ps.PS_QUEUE_ROUND_ROBIN, slots)
+    srv.set_weights(w0)
+    o = orc.OracleServer(parity.np_bits(w0), 0.01, 0.9, depth=depth)
+    assert o.set_queue_mode(orc.ROUND_ROBIN, slots) == orc.OK
+    order, stale = [], []
+    for step in range(400):
+        r = rng.random()
+        if r < 0.6:
+            l, b = int(rng.integers(0, lam)), int(rng.integers(0, len(pool)))
+            ok = srv.push(l, pool[b])
+            assert ok == (o.push(l, host[b]) == orc.OK)
+        elif r < 0.85:
+            srv.apply_pending()
+            o.apply_pending()
+            order += srv.last_applied()
+            stale += srv.last_staleness()
+        elif r < 0.9:
+            srv.apply_sync()
+            assert o.apply_sync() == orc.OK
+            order += srv.last_applied()
+            stale += srv.last_staleness()
+        else:
+            l = int(rng.integers(0, lam))
+            srv.pull(l, dst)
+            o.pull(l, "d", orc.F32)
+        assert srv.pending == o.pending()
+    assert order == o.applied_order and stale == o.staleness
+    assert parity.bitwise(parity.np_bits(srv.weights_copy()), o.w)
+    assert parity.bitwise(parity.np_bits(srv.velocity_copy()), o.v)
+    assert srv.stats().pushes_rejected > 0 or slots >= 4
+    srv.close()
+
+
+def test_queue_mode_rules(torch):
+    n = 100
+    srv = ps.ParameterServer(n, 0.1, 0.0, queue_depth=4)
+    g = torch.ones(n, device="cuda")
+    assert ps.ps_set_queue_mode(srv.h, 7, 1) == ps.PS_EINVAL
+    assert ps.ps_set_queue_mode(srv.h, ps.PS_QUEUE_ROUND_ROBIN, 0) == ps.PS_EINVAL
+    assert ps.ps_set_queue_mode(srv.h, ps.PS_QUEUE_ROUND_ROBIN, 65) == ps.PS_EINVAL
+    srv.push(0, g)
+    assert ps.ps_set_queue_mode(srv.h, ps.PS_QUEUE_ROUND_ROBIN, 2) == ps.PS_ESTATE
+    srv.apply_pending()
+    srv.set_queue_mode(ps.PS_QUEUE_ROUND_ROBIN, 1)
+    # 65 learners waiting is more than one synchronous step can average
+    for l in range(65):
+        srv.push(l, g)
+    assert ps.ps_apply_sync(srv.h) == ps.PS_ESTATE
+    while srv.pending:
+        srv.apply_pending()
+    assert srv.timestamp == 66
+    srv.close()
