@@ -296,6 +296,19 @@ class OracleServer:
         self.learner_ts[learner] = self.ts
         return True
 
+    def drop_learner(self, learner: int) -> int:
+        """A learner died (Sec. 4.3): its queued gradients are discarded, the
+        others keep their order. Returns how many were dropped."""
+        if self.mode == ROUND_ROBIN:
+            q = self.per_learner.get(learner, [])
+            dropped = len(q)
+            self.per_learner[learner] = []
+            return dropped
+        keep = [e for e in self.queue if e[0] != learner]
+        dropped = len(self.queue) - len(keep)
+        self.queue = keep
+        return dropped
+
     def set_depth(self, depth: int) -> int:
         if not 1 <= depth <= MAX_DEPTH:
             return EINVAL

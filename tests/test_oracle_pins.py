@@ -595,3 +595,29 @@ def test_round_robin_sync_one_per_learner_in_id_order():
     s.apply_sync()
     assert s.w[0] == np.float32(-(7.0 / 3)) - 8.0
     assert s.set_queue_mode(orc.FIFO) == orc.OK
+
+
+# ------------------------------------------------ dead learners (Sec. 4.3)
+
+def test_drop_learner_isolates_failure():
+    """Dropping a dead learner's queued gradients leaves the others' in order
+    and the result equals a run in which it never pushed them (the server
+    keeps no per-learner state beyond timestamps, Sec. 4.3)."""
+    rng = np.random.default_rng(40)
+    w0 = rng.uniform(-0.05, 0.05, 64).astype(np.float32)
+    gs = [rand_f32(rng, 64, 0.01) for _ in range(9)]
+    learners = [0, 1, 2, 1, 0, 2, 2, 1, 0]
+    for mode in (orc.FIFO, orc.ROUND_ROBIN):
+        a = orc.OracleServer(w0, 0.01, 0.9, depth=9)
+        b = orc.OracleServer(w0, 0.01, 0.9, depth=9)
+        a.set_queue_mode(mode, 4)
+        b.set_queue_mode(mode, 4)
+        for l, g in zip(learners, gs):
+            a.push(l, g)
+            if l != 2:
+                b.push(l, g)
+        assert a.drop_learner(2) == 3 and a.drop_learner(2) == 0
+        a.apply_pending()
+        b.apply_pending()
+        assert np.array_equal(bits(a.w), bits(b.w)) and a.applied_order == b.applied_order
+        assert 2 not in a.applied_order
