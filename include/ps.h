@@ -68,7 +68,8 @@ enum {
     PS_EFULL = -2,   /* push on a full queue; nothing was enqueued          */
     PS_ENOMEM = -3,  /* device or host allocation failed                    */
     PS_EHIP = -4,    /* a HIP runtime call or kernel launch failed          */
-    PS_ESTATE = -5   /* call not allowed in the current state               */
+    PS_ESTATE = -5,  /* call not allowed in the current state               */
+    PS_EIO = -6      /* checkpoint file could not be written, read or trusted */
 };
 
 enum { PS_F32 = 0, PS_BF16 = 1 };
@@ -89,6 +90,7 @@ typedef struct ps_stats {
     uint64_t pushes_accepted;
     uint64_t pushes_rejected;  /* PS_EFULL returns                          */
     uint64_t pushes_applied;
+    uint64_t pushes_dropped;   /* discarded by ps_drop_learner              */
     uint64_t applies;          /* apply calls that launched device work     */
     uint64_t pulls;            /* replica refreshes requested               */
     uint64_t pulls_skipped;    /* ... of which skipped as already current   */
@@ -215,6 +217,27 @@ int ps_last_staleness(const ps_server *ps, int64_t *out, int cap);
  * the order applied. Writes min(count, cap) ids and returns count (or a
  * negative status). */
 int ps_last_applied(const ps_server *ps, int *learner_ids, int cap);
+
+/* A learner died (Sec. 4.3): discard its queued gradients -- its borrowed
+ * buffers may be gone with it -- and keep every other gradient in order. The
+ * server holds no other per-learner state that the others depend on, so
+ * training continues with the live learners. Returns the number dropped
+ * (>= 0) or a negative status. */
+int ps_drop_learner(ps_server *ps, int learner_id);
+
+/* Checkpoint (Sec. 4.3: the server checkpoints its parameters so that a
+ * restart resumes from the last checkpoint). ps_save writes w, v, the
+ * timestamp, the round-robin position and every learner's timestamp to
+ * `path` (waits for the server's stream first); ps_load restores them into
+ * a server created with the same n_params, lr and momentum, after checking
+ * the whole file (format, sizes, checksum) -- on any failure the server is
+ * unchanged. Pull history and statistics start afresh after a load (learners
+ * pull again after a restart). Both need an empty queue (PS_ESTATE
+ * otherwise); file errors give PS_EIO, mismatched servers PS_EINVAL.
+ * Continuing from a loaded checkpoint gives the bits of the uninterrupted
+ * run. */
+int ps_save(ps_server *ps, const char *path);
+int ps_load(ps_server *ps, const char *path);
 
 /* Block until all work enqueued by the server has completed. */
 int ps_sync(ps_server *ps);

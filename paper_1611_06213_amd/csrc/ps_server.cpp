@@ -16,6 +16,7 @@
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
+#include <cstdio>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -356,6 +357,56 @@ void clear_last(ps_server *ps) {
     ps->last_applied.clear();
 }
 
+// ---------------------------------------------------------------- checkpoint
+//
+// File layout (little-endian, as the host writes it):
+//   CkptHeader, then learner_ts[n_learner_ts] (uint64), then w[n] (fp32),
+//   then v[n] (fp32) when the server has momentum.
+// `checksum` is FNV-1a (64-bit) over every byte after the header.
+
+struct CkptHeader {
+    char magic[8];
+    uint32_t version;
+    uint32_t has_v;
+    uint64_t n;
+    float lr;
+    float m;
+    uint64_t ts;
+    int64_t last_served;
+    uint64_t n_learner_ts;
+    uint64_t checksum;
+};
+
+constexpr char kMagic[8] = {'G', 'A', 'D', 'E', 'I', 'P', 'S', '1'};
+constexpr size_t kChunk = size_t(16) << 20;   // floats per device<->host copy
+
+struct Fnv {
+    uint64_t h = 1469598103934665603ull;
+    void add(const void *p, size_t bytes) {
+        const unsigned char *c = static_cast<const unsigned char *>(p);
+        for (size_t i = 0; i < bytes; ++i) {
+            h ^= c[i];
+            h *= 1099511628211ull;
+        }
+    }
+};
+
+int write_all(FILE *f, const void *p, size_t bytes, Fnv *fnv) {
+    if (fnv) fnv->add(p, bytes);
+    return std::fwrite(p, 1, bytes, f) == bytes ? PS_OK : fail(PS_EIO, "checkpoint write failed");
+}
+
+// Device array -> file, in chunks through a host buffer.
+int save_array(FILE *f, const float *dev, size_t n, std::vector<float> &buf, Fnv &fnv) {
+    for (size_t off = 0; off < n; off += kChunk) {
+        const size_t cnt = std::min(kChunk, n - off);
+        hipError_t e = hipMemcpy(buf.data(), dev + off, cnt * sizeof(float), hipMemcpyDeviceToHost);
+        if (e != hipSuccess) return fail_hip(e, "checkpoint read-back");
+        if (int rc = write_all(f, buf.data(), cnt * sizeof(float), &fnv)) return rc;
+    }
+    return PS_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -535,6 +586,121 @@ int ps_apply_pull(ps_server *ps, int n, const int *learner_ids, void *const *dst
     }
     commit_async(ps, b);
     commit_pulls(ps, n, learner_ids, dsts, dst_dtype, write);
+    return PS_OK;
+}
+
+int ps_drop_learner(ps_server *ps, int learner_id) {
+    if (int rc = check(ps)) return rc;
+    if (int rc = check_learner(learner_id)) return rc;
+    int dropped = 0;
+    if (ps->mode == PS_QUEUE_FIFO) {
+        auto keep = std::remove_if(ps->fifo.begin(), ps->fifo.end(),
+                                   [&](const PushDesc &d) { return d.learner == learner_id; });
+        dropped = static_cast<int>(ps->fifo.end() - keep);
+        ps->fifo.erase(keep, ps->fifo.end());
+    } else if (static_cast<size_t>(learner_id) < ps->rr.size()) {
+        dropped = static_cast<int>(ps->rr[learner_id].size());
+        ps->rr[learner_id].clear();
+        ps->waiting.erase(learner_id);
+        ps->rr_count -= dropped;
+    }
+    ps->stats.pushes_dropped += dropped;
+    return dropped;
+}
+
+int ps_save(ps_server *ps, const char *path) {
+    if (int rc = check(ps)) return rc;
+    if (path == nullptr) return fail(PS_EINVAL, "null path");
+    if (pending(ps) != 0) return fail(PS_ESTATE, "gradients pending");
+    if (int rc = use_device(ps)) return rc;
+    hipError_t e = hipStreamSynchronize(ps->stream);
+    if (e != hipSuccess) return fail_hip(e, "hipStreamSynchronize");
+    FILE *f = std::fopen(path, "wb");
+    if (f == nullptr) return fail(PS_EIO, "cannot open %s for writing", path);
+    CkptHeader h;
+    std::memset(&h, 0, sizeof h);
+    std::memcpy(h.magic, kMagic, sizeof kMagic);
+    h.version = 1;
+    h.has_v = ps->v != nullptr;
+    h.n = ps->n;
+    h.lr = ps->lr;
+    h.m = ps->m;
+    h.ts = ps->ts;
+    h.last_served = ps->last_served;
+    h.n_learner_ts = ps->learner_ts.size();
+    int rc = write_all(f, &h, sizeof h, nullptr);
+    Fnv fnv;
+    std::vector<float> buf;
+    if (rc == PS_OK && h.n_learner_ts)
+        rc = write_all(f, ps->learner_ts.data(), h.n_learner_ts * sizeof(uint64_t), &fnv);
+    if (rc == PS_OK) {
+        buf.resize(std::min(kChunk, ps->n));
+        rc = save_array(f, ps->w, ps->n, buf, fnv);
+    }
+    if (rc == PS_OK && ps->v) rc = save_array(f, ps->v, ps->n, buf, fnv);
+    if (rc == PS_OK) {
+        h.checksum = fnv.h;
+        if (std::fseek(f, 0, SEEK_SET) != 0) rc = fail(PS_EIO, "checkpoint seek failed");
+        else rc = write_all(f, &h, sizeof h, nullptr);
+    }
+    if (std::fclose(f) != 0 && rc == PS_OK) rc = fail(PS_EIO, "checkpoint close failed");
+    return rc;
+}
+
+int ps_load(ps_server *ps, const char *path) {
+    if (int rc = check(ps)) return rc;
+    if (path == nullptr) return fail(PS_EINVAL, "null path");
+    if (pending(ps) != 0) return fail(PS_ESTATE, "gradients pending");
+    FILE *f = std::fopen(path, "rb");
+    if (f == nullptr) return fail(PS_EIO, "cannot open %s", path);
+    CkptHeader h;
+    int rc = PS_OK;
+    if (std::fread(&h, 1, sizeof h, f) != sizeof h || std::memcmp(h.magic, kMagic, 8) != 0 ||
+        h.version != 1)
+        rc = fail(PS_EIO, "%s is not a parameter-server checkpoint", path);
+    else if (h.n != ps->n || (h.has_v != 0) != (ps->v != nullptr))
+        rc = fail(PS_EINVAL, "checkpoint holds %llu params%s; server has %zu%s",
+                  static_cast<unsigned long long>(h.n), h.has_v ? " with momentum" : "", ps->n,
+                  ps->v ? " with momentum" : "");
+    else if (std::memcmp(&h.lr, &ps->lr, sizeof(float)) != 0 ||
+             std::memcmp(&h.m, &ps->m, sizeof(float)) != 0)
+        rc = fail(PS_EINVAL, "checkpoint lr/momentum differ from the server's");
+    else if (h.n_learner_ts > static_cast<uint64_t>(PS_MAX_LEARNERS))
+        rc = fail(PS_EIO, "corrupt checkpoint (learner table)");
+    // read and verify everything before touching the server
+    std::vector<uint64_t> lts;
+    std::vector<float> w, v;
+    Fnv fnv;
+    if (rc == PS_OK) {
+        lts.resize(h.n_learner_ts);
+        w.resize(h.n);
+        if (h.has_v) v.resize(h.n);
+        const size_t lb = lts.size() * sizeof(uint64_t), wb = w.size() * sizeof(float);
+        if (std::fread(lts.data(), 1, lb, f) != lb || std::fread(w.data(), 1, wb, f) != wb ||
+            (h.has_v && std::fread(v.data(), 1, wb, f) != wb))
+            rc = fail(PS_EIO, "checkpoint truncated");
+        else {
+            fnv.add(lts.data(), lb);
+            fnv.add(w.data(), wb);
+            if (h.has_v) fnv.add(v.data(), wb);
+            if (fnv.h != h.checksum) rc = fail(PS_EIO, "checkpoint checksum mismatch");
+        }
+    }
+    std::fclose(f);
+    if (rc != PS_OK) return rc;
+    if (int rc2 = use_device(ps)) return rc2;
+    hipError_t e = hipStreamSynchronize(ps->stream);
+    if (e == hipSuccess) e = hipMemcpy(ps->w, w.data(), h.n * sizeof(float), hipMemcpyHostToDevice);
+    if (e == hipSuccess && ps->v)
+        e = hipMemcpy(ps->v, v.data(), h.n * sizeof(float), hipMemcpyHostToDevice);
+    if (e != hipSuccess) return fail_hip(e, "checkpoint upload");
+    ps->ts = h.ts;
+    ps->last_served = static_cast<int>(h.last_served);
+    ps->learner_ts.assign(lts.begin(), lts.end());
+    ps->last_pull.assign(lts.size(), PullKey{});
+    clear_last(ps);
+    ps->stats = ps_stats{};
+    ps->stats.timestamp = ps->ts;
     return PS_OK;
 }
 

@@ -17,6 +17,7 @@ PS_EFULL = -2
 PS_ENOMEM = -3
 PS_EHIP = -4
 PS_ESTATE = -5
+PS_EIO = -6
 
 PS_F32 = 0
 PS_BF16 = 1
@@ -38,7 +39,8 @@ _u64 = ctypes.c_uint64
 class ps_stats(ctypes.Structure):
     _fields_ = [
         ("timestamp", _u64), ("pushes_accepted", _u64), ("pushes_rejected", _u64),
-        ("pushes_applied", _u64), ("applies", _u64), ("pulls", _u64), ("pulls_skipped", _u64),
+        ("pushes_applied", _u64), ("pushes_dropped", _u64), ("applies", _u64), ("pulls", _u64),
+        ("pulls_skipped", _u64),
         ("staleness_max", _u64), ("staleness_sum", _u64),
         ("staleness_hist", _u64 * PS_STALENESS_BINS),
     ]
@@ -71,6 +73,9 @@ _SIGS = {
     "ps_timestamp": (_u64, [_VP]),
     "ps_pending": (ctypes.c_int, [_VP]),
     "ps_last_staleness": (ctypes.c_int, [_VP, ctypes.POINTER(ctypes.c_int64), ctypes.c_int]),
+    "ps_drop_learner": (ctypes.c_int, [_VP, ctypes.c_int]),
+    "ps_save": (ctypes.c_int, [_VP, ctypes.c_char_p]),
+    "ps_load": (ctypes.c_int, [_VP, ctypes.c_char_p]),
     "ps_sync": (ctypes.c_int, [_VP]),
     "ps_get_stats": (ctypes.c_int, [_VP, ctypes.POINTER(ps_stats)]),
     "ps_last_error": (ctypes.c_char_p, []),
@@ -220,6 +225,18 @@ def ps_last_staleness(h: int, cap: int = PS_MAX_QUEUE_DEPTH):
     return [int(out[i]) for i in range(min(n, cap))]
 
 
+def ps_drop_learner(h: int, learner_id: int) -> int:
+    return load_library().ps_drop_learner(h, learner_id)
+
+
+def ps_save(h: int, path: str) -> int:
+    return load_library().ps_save(h, os.fsencode(path))
+
+
+def ps_load(h: int, path: str) -> int:
+    return load_library().ps_load(h, os.fsencode(path))
+
+
 def ps_sync(h: int) -> int:
     return load_library().ps_sync(h)
 
@@ -336,6 +353,16 @@ class ParameterServer:
         ptrs = [self._tensor(d, "apply_pull") for d in dsts]
         self._check(ps_apply_pull(self.h, list(learners), ptrs, dt), "apply_pull")
         self._pending = []
+
+    def drop_learner(self, learner: int) -> int:
+        n = self._check(ps_drop_learner(self.h, learner), "drop_learner")
+        return n
+
+    def save(self, path: str) -> None:
+        self._check(ps_save(self.h, path), "save")
+
+    def load(self, path: str) -> None:
+        self._check(ps_load(self.h, path), "load")
 
     def sync(self) -> None:
         self._check(ps_sync(self.h), "sync")

@@ -39,13 +39,13 @@ def test_every_declared_symbol_is_exported(lib):
 def test_header_constants_match_binding():
     text = open(os.path.join(ROOT, "include", "ps.h")).read()
     for name in ("PS_OK", "PS_EINVAL", "PS_EFULL", "PS_ENOMEM", "PS_EHIP", "PS_ESTATE",
-                 "PS_F32", "PS_BF16", "PS_QUEUE_FIFO", "PS_QUEUE_ROUND_ROBIN"):
+                 "PS_EIO", "PS_F32", "PS_BF16", "PS_QUEUE_FIFO", "PS_QUEUE_ROUND_ROBIN"):
         m = re.search(rf"\b{name}\s*=\s*(-?\d+)", text)
         assert m and int(m.group(1)) == getattr(ps, name), name
     for name in ("PS_MAX_QUEUE_DEPTH", "PS_MAX_REPLICAS", "PS_MAX_LEARNERS", "PS_STALENESS_BINS"):
         m = re.search(rf"#define {name} (\d+)", text)
         assert m and int(m.group(1)) == getattr(ps, name), name
-    assert ctypes.sizeof(ps.ps_stats) == 8 * (9 + ps.PS_STALENESS_BINS)
+    assert ctypes.sizeof(ps.ps_stats) == 8 * (10 + ps.PS_STALENESS_BINS)
 
 
 def test_validation_without_device(lib):
@@ -60,6 +60,8 @@ def test_validation_without_device(lib):
     assert lib.ps_set_queue_depth(None, 4) == ps.PS_EINVAL
     assert lib.ps_sync(None) == ps.PS_EINVAL
     assert lib.ps_pending(None) == ps.PS_EINVAL
+    assert lib.ps_save(None, b"/tmp/x") == ps.PS_EINVAL and lib.ps_load(None, b"/tmp/x") == ps.PS_EINVAL
+    assert lib.ps_drop_learner(None, 0) == ps.PS_EINVAL
     assert lib.ps_timestamp(None) == 0 and lib.ps_num_params(None) == 0
     assert not lib.ps_weights(None)
     lib.ps_destroy(None)   # no-op

@@ -606,3 +606,159 @@ def test_queue_mode_rules(torch):
         srv.apply_pending()
     assert srv.timestamp == 66
     srv.close()
+
+
+# ---------------------------------------------------------------- fault tolerance
+
+def _ft_schedule(cfg):
+    ev = wl.schedule(cfg)
+    applies = [i for i, e in enumerate(ev) if isinstance(e, wl.Apply)]
+    return ev, applies
+
+
+def _drive(srv, ev, pool, replicas, stale, learners_dead=(), start=0, stop=None):
+    for e in ev[start:stop]:
+        if isinstance(e, wl.Push):
+            if e.learner not in learners_dead:
+                assert srv.push(e.learner, pool[e.buf])
+        elif isinstance(e, wl.Apply):
+            srv.apply_pending()
+            stale += srv.last_staleness()
+        else:
+            for rnd in parity.pull_rounds(e.learners):
+                srv.pull_many(rnd, [replicas[l] for l in rnd])
+
+
+@pytest.mark.parametrize("mode", [ps.PS_QUEUE_FIFO, ps.PS_QUEUE_ROUND_ROBIN])
+def test_checkpoint_restart_is_bitwise_uninterrupted(torch, tmp_path, mode):
+    """Sec. 4.3: run half the AlexNet-shaped schedule, checkpoint, destroy the
+    server, create a new one, load, run the rest: weights, velocity, replicas
+    and staleness equal the uninterrupted run bit for bit."""
+    cfg = wl.CONFIGS["alexnet"].scaled(300007, pushes=320, pool=24)
+    ev, applies = _ft_schedule(cfg)
+    cut = applies[len(applies) // 2] + 1
+    pool = wl.make_pool(cfg, "cuda")
+    w0 = wl.make_w0(cfg, "cuda")
+
+    def fresh():
+        s = ps.ParameterServer(cfg.n, cfg.lr, cfg.momentum, queue_depth=cfg.depth)
+        if mode == ps.PS_QUEUE_ROUND_ROBIN:
+            s.set_queue_mode(mode, cfg.depth)
+        return s
+
+    ra = wl.Rows(cfg.replicas, cfg.n, torch.float32, "cuda")
+    a = fresh()
+    a.set_weights(w0)
+    sa = []
+    _drive(a, ev, pool, ra, sa)
+    wa, va = parity.np_bits(a.weights_copy()), parity.np_bits(a.velocity_copy())
+    a.close()
+
+    rb = wl.Rows(cfg.replicas, cfg.n, torch.float32, "cuda")
+    b = fresh()
+    b.set_weights(w0)
+    sb = []
+    _drive(b, ev, pool, rb, sb, stop=cut)
+    path = str(tmp_path / "ps.ckpt")
+    b.save(path)
+    ts_cut = b.timestamp
+    b.close()
+    c = fresh()
+    c.load(path)
+    assert c.timestamp == ts_cut
+    _drive(c, ev, pool, rb, sb, start=cut)
+    assert parity.bitwise(parity.np_bits(c.weights_copy()), wa)
+    assert parity.bitwise(parity.np_bits(c.velocity_copy()), va)
+    assert sb == sa
+    for l in range(cfg.replicas):
+        assert parity.bitwise(parity.np_bits(rb[l]), parity.np_bits(ra[l]))
+    c.close()
+
+
+def test_checkpoint_errors_leave_server_unchanged(torch, tmp_path):
+    n = 100003
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(9)
+    w0 = torch.rand(n, generator=gen, device="cuda")
+    a = ps.ParameterServer(n, 0.01, 0.9)
+    a.set_weights(w0)
+    a.push(0, torch.ones(n, device="cuda"))
+    path = str(tmp_path / "a.ckpt")
+    assert ps.ps_save(a.h, path) == ps.PS_ESTATE            # gradients pending
+    a.apply_pending()
+    a.save(path)
+    w_saved = parity.np_bits(a.weights_copy())
+    b = ps.ParameterServer(n, 0.01, 0.9)
+    b.set_weights(torch.zeros(n, device="cuda"))
+    raw = bytearray(open(path, "rb").read())
+    bad = str(tmp_path / "bad.ckpt")
+    raw[200] ^= 1
+    open(bad, "wb").write(bytes(raw))
+    assert ps.ps_load(b.h, bad) == ps.PS_EIO and "checksum" in ps.ps_last_error()
+    open(bad, "wb").write(bytes(raw[:1000]))
+    assert ps.ps_load(b.h, bad) == ps.PS_EIO
+    assert ps.ps_load(b.h, str(tmp_path / "missing.ckpt")) == ps.PS_EIO
+    assert torch.all(b.weights_copy() == 0) and b.timestamp == 0     # unchanged
+    other = ps.ParameterServer(n + 1, 0.01, 0.9)
+    assert ps.ps_load(other.h, path) == ps.PS_EINVAL
+    other2 = ps.ParameterServer(n, 0.02, 0.9)
+    assert ps.ps_load(other2.h, path) == ps.PS_EINVAL
+    nomom = ps.ParameterServer(n, 0.01, 0.0)
+    assert ps.ps_load(nomom.h, path) == ps.PS_EINVAL
+    b.load(path)
+    assert parity.bitwise(parity.np_bits(b.weights_copy()), w_saved) and b.timestamp == 1
+    for s in (a, b, other, other2, nomom):
+        s.close()
+
+
+@pytest.mark.parametrize("mode", [ps.PS_QUEUE_FIFO, ps.PS_QUEUE_ROUND_ROBIN])
+def test_dead_learner_isolated(torch, mode):
+    """Sec. 4.3 / 6.4: learner 3 dies mid-run with gradients queued; they are
+    dropped and it pushes no more; the server keeps applying the others'.
+    The oracle does the same; weights, staleness and order agree bitwise."""
+    cfg = wl.CONFIGS["vgg16"].scaled(200003, pushes=160, pool=20)
+    ev = wl.schedule(cfg)
+    die_at = len(ev) // 2
+    while not isinstance(ev[die_at], wl.Push):
+        die_at += 1
+    pool = wl.make_pool(cfg, "cuda")
+    w0 = wl.make_w0(cfg, "cuda")
+    host = [parity.np_bits(pool[b]) for b in range(cfg.pool)]
+    srv = ps.ParameterServer(cfg.n, cfg.lr, cfg.momentum, queue_depth=cfg.depth)
+    o = orc.OracleServer(parity.np_bits(w0), cfg.lr, cfg.momentum, depth=cfg.depth)
+    if mode == ps.PS_QUEUE_ROUND_ROBIN:
+        srv.set_queue_mode(mode, 8)
+        o.set_queue_mode(orc.ROUND_ROBIN, 8)
+    srv.set_weights(w0)
+    dead, stale, order, dropped = set(), [], [], 0
+    reps = wl.Rows(cfg.replicas, cfg.n, torch.float32, "cuda")
+    for i, e in enumerate(ev):
+        if i == die_at:
+            dead.add(3)
+            d = srv.drop_learner(3)
+            assert d == o.drop_learner(3)
+            dropped += d
+        if isinstance(e, wl.Push):
+            if e.learner in dead:
+                continue
+            ok = srv.push(e.learner, pool[e.buf])
+            assert ok == (o.push(e.learner, host[e.buf]) == orc.OK)
+            if not ok:   # round-robin slots full: apply, then push again
+                srv.apply_pending(); o.apply_pending()
+                order += srv.last_applied(); stale += srv.last_staleness()
+                assert srv.push(e.learner, pool[e.buf]) and o.push(e.learner, host[e.buf]) == orc.OK
+        elif isinstance(e, wl.Apply):
+            srv.apply_pending(); o.apply_pending()
+            order += srv.last_applied(); stale += srv.last_staleness()
+        else:
+            live = [l for l in e.learners if l not in dead]
+            srv.pull_many(live, [reps[l] for l in live])
+            for l in live:
+                o.pull(l, l, orc.F32)
+    while srv.pending:
+        srv.apply_pending(); o.apply_pending()
+        order += srv.last_applied(); stale += srv.last_staleness()
+    assert order == o.applied_order and stale == o.staleness
+    assert 3 not in order[-20:] and srv.stats().pushes_dropped == dropped
+    assert parity.bitwise(parity.np_bits(srv.weights_copy()), o.w)
+    srv.close()
