@@ -123,6 +123,14 @@ int ps_push(ps_server *ps, int learner_id, const void *grad);
  * gradient holds n_params 16-bit values). */
 int ps_push_dtype(ps_server *ps, int learner_id, const void *grad, int dtype);
 
+/* ps_push_dtype for a gradient that a producer may still be writing on
+ * another stream (the paper's push thread works on its own stream, Sec.
+ * 4.1): `ready_event` is a hipEvent_t the producer recorded after its last
+ * write, and the apply that consumes the gradient makes the server's stream
+ * wait for it on the device -- the host never blocks. NULL = ready now. The
+ * event must stay valid until that apply has been enqueued. */
+int ps_push_async(ps_server *ps, int learner_id, const void *grad, int dtype, void *ready_event);
+
 /* Apply the pending gradients -- FIFO mode: all of them, oldest first;
  * round-robin mode: up to `depth` in service order (ps_set_queue_mode) --
  * each as one step of Eq. "asgd", and remove them from their queues. Enqueues one kernel per run of equal-dtype
@@ -170,6 +178,27 @@ int ps_set_pull_fusion(ps_server *ps, int max_replicas);
 /* Use hip_stream (a hipStream_t; NULL = the null stream) for all later device
  * work. The caller orders it against work already on the previous stream. */
 int ps_set_stream(ps_server *ps, void *hip_stream);
+
+/* Record `event` (a hipEvent_t) on the server's stream after all work
+ * enqueued so far: when it completes, every gradient consumed by an earlier
+ * apply may be overwritten and every earlier ordered pull is complete. A
+ * producer stream can wait for it instead of the host (double buffering). */
+int ps_record(ps_server *ps, void *event);
+
+/* Lock-free pulls (the paper's default HogWild! mode, Sec. 4.1): with a
+ * non-NULL hip_stream, ps_pull / ps_pull_many run there, not ordered after
+ * applies on the server's stream, so a pull concurrent with an apply may
+ * write, coordinate by coordinate, the weights from before or after it
+ * (each coordinate is one of the two; the replica as a whole may mix them).
+ * The caller orders such pulls against earlier applies itself if it needs
+ * to (ps_record + hipStreamWaitEvent). A lock-free pull never makes a copy
+ * count as current, so the next pull of that learner is not skipped; the
+ * learner's timestamp is taken at the call. ps_apply_pull still orders its
+ * pull after its apply. NULL (default)
+ * restores ordered pulls -- the paper's read-write-lock option. Waits for
+ * earlier lock-free pulls before switching; ps_sync, ps_set_weights,
+ * ps_save, ps_load and ps_destroy wait for them too. */
+int ps_set_pull_stream(ps_server *ps, void *hip_stream);
 
 /* Queue depth K, 1..PS_MAX_QUEUE_DEPTH: the FIFO's slots, and the most
  * gradients one asynchronous apply takes. PS_ESTATE if (FIFO mode) more

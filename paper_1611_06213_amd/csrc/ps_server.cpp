@@ -53,6 +53,7 @@ struct PushDesc {
     int dtype;
     const void *grad;
     uint64_t learner_ts;   // timestamp of the weights the learner held at push
+    hipEvent_t ready;      // producer's event the apply waits for, or null
 };
 
 struct PullKey {
@@ -82,6 +83,8 @@ struct ps_server {
     float *v = nullptr;
     int device = 0;
     hipStream_t stream = nullptr;
+    hipStream_t pull_stream = nullptr;   // lock-free pulls when pull_lock_free
+    bool pull_lock_free = false;
     int depth = PS_MAX_QUEUE_DEPTH / 2;
     bool pull_skip = true;
     int fuse_max_r = 1;   // ps_apply_pull writes up to this many replicas in the apply pass
@@ -252,8 +255,12 @@ int plan_pulls(ps_server *ps, int n, const int *ids, void *const *dsts, int dtyp
     return PS_OK;
 }
 
+// `ordered`: the replicas were written after every earlier apply, so they
+// hold the weights at the current timestamp and a repeat can be skipped. A
+// lock-free pull may have raced an apply: its replicas never count as
+// current.
 void commit_pulls(ps_server *ps, int n, const int *ids, void *const *dsts, int dtype,
-                  const std::vector<int> &write) {
+                  const std::vector<int> &write, bool ordered) {
     ps->stats.pulls += n;
     ps->stats.pulls_skipped += n - static_cast<int>(write.size());
     for (int i = 0; i < n; ++i) {
@@ -265,7 +272,7 @@ void commit_pulls(ps_server *ps, int n, const int *ids, void *const *dsts, int d
         k.dst = dsts[i];
         k.dtype = dtype;
         k.ts = ps->ts;
-        k.valid = true;
+        k.valid = ordered;
     }
 }
 
@@ -293,10 +300,34 @@ void commit_async(ps_server *ps, const Batch &b) {
     consume(ps, b);
 }
 
+// Make the server's stream wait (on the device) for every producer event of
+// the batch, each once.
+int wait_ready(ps_server *ps, const std::vector<PushDesc> &items) {
+    std::vector<hipEvent_t> seen;
+    for (const PushDesc &d : items) {
+        if (d.ready == nullptr || std::find(seen.begin(), seen.end(), d.ready) != seen.end())
+            continue;
+        seen.push_back(d.ready);
+        hipError_t e = hipStreamWaitEvent(ps->stream, d.ready, 0);
+        if (e != hipSuccess) return fail_hip(e, "waiting for a producer event");
+    }
+    return PS_OK;
+}
+
+// Host-side wait for lock-free pulls still reading w (before w is reset,
+// saved, loaded or freed).
+int drain_pulls(ps_server *ps) {
+    if (!ps->pull_lock_free) return PS_OK;
+    hipError_t e = hipStreamSynchronize(ps->pull_stream);
+    if (e != hipSuccess) return fail_hip(e, "hipStreamSynchronize (pull stream)");
+    return PS_OK;
+}
+
 // Launch a batch as runs of equal gradient dtype, in order. The last run
 // also writes the replicas listed in `write` when pull_dtype >= 0.
 int launch_batch(ps_server *ps, const std::vector<PushDesc> &items, int pull_dtype,
                  void *const *dsts, const std::vector<int> &write) {
+    if (int rc = wait_ready(ps, items)) return rc;
     gadei::ApplyArgs a;
     std::memset(&a, 0, sizeof a);
     a.w = ps->w;
@@ -333,8 +364,12 @@ int launch_batch(ps_server *ps, const std::vector<PushDesc> &items, int pull_dty
     return PS_OK;
 }
 
-int launch_pulls(ps_server *ps, void *const *dsts, int dtype, const std::vector<int> &write) {
+// `ordered`: on the server's stream, after every earlier apply; otherwise on
+// the lock-free pull stream when that mode is on.
+int launch_pulls(ps_server *ps, void *const *dsts, int dtype, const std::vector<int> &write,
+                 bool ordered) {
     if (write.empty()) return PS_OK;
+    hipStream_t s = (!ordered && ps->pull_lock_free) ? ps->pull_stream : ps->stream;
     gadei::PullArgs a;
     std::memset(&a, 0, sizeof a);
     a.w = ps->w;
@@ -345,7 +380,7 @@ int launch_pulls(ps_server *ps, void *const *dsts, int dtype, const std::vector<
         a.dst[j] = dsts[write[j]];
         level = std::min(level, level_of(a.dst[j], dtype));
     }
-    hipError_t e = gadei::launch_pull(a, dtype, level, ps->geo, ps->stream);
+    hipError_t e = gadei::launch_pull(a, dtype, level, ps->geo, s);
     if (e != hipSuccess) return fail_hip(e, "pull kernel launch");
     return PS_OK;
 }
@@ -452,20 +487,27 @@ void ps_destroy(ps_server *ps) {
     if (ps == nullptr) return;
     if (use_device(ps) == PS_OK) {
         (void)hipStreamSynchronize(ps->stream);
+        if (ps->pull_lock_free) (void)hipStreamSynchronize(ps->pull_stream);
         if (ps->w) (void)hipFree(ps->w);
         if (ps->v) (void)hipFree(ps->v);
     }
     delete ps;
 }
 
+int ps_push_async(ps_server *ps, int learner_id, const void *grad, int dtype, void *ready_event);
+
 int ps_push_dtype(ps_server *ps, int learner_id, const void *grad, int dtype) {
+    return ps_push_async(ps, learner_id, grad, dtype, nullptr);
+}
+
+int ps_push_async(ps_server *ps, int learner_id, const void *grad, int dtype, void *ready_event) {
     if (int rc = check(ps)) return rc;
     if (int rc = check_learner(learner_id)) return rc;
     if (grad == nullptr) return fail(PS_EINVAL, "null gradient");
     if (dtype != PS_F32 && dtype != PS_BF16) return fail(PS_EINVAL, "bad gradient dtype %d", dtype);
     const uint64_t lts =
         static_cast<size_t>(learner_id) < ps->learner_ts.size() ? ps->learner_ts[learner_id] : 0;
-    const PushDesc d{learner_id, dtype, grad, lts};
+    const PushDesc d{learner_id, dtype, grad, lts, static_cast<hipEvent_t>(ready_event)};
     if (ps->mode == PS_QUEUE_FIFO) {
         if (static_cast<int>(ps->fifo.size()) >= ps->depth) {
             ps->stats.pushes_rejected += 1;
@@ -521,6 +563,7 @@ int ps_apply_sync(ps_server *ps) {
     for (const PushDesc &d : b.items)
         if (d.dtype != gdt) return fail(PS_EINVAL, "synchronous step needs one gradient dtype");
     if (int rc = use_device(ps)) return rc;
+    if (int rc = wait_ready(ps, b.items)) return rc;
     gadei::ApplyArgs a;
     std::memset(&a, 0, sizeof a);
     a.w = ps->w;
@@ -554,9 +597,9 @@ int ps_pull_many(ps_server *ps, int n, const int *learner_ids, void *const *dsts
     if (int rc = plan_pulls(ps, n, learner_ids, dsts, dst_dtype, ps->ts, write)) return rc;
     if (!write.empty()) {
         if (int rc = use_device(ps)) return rc;
-        if (int rc = launch_pulls(ps, dsts, dst_dtype, write)) return rc;
+        if (int rc = launch_pulls(ps, dsts, dst_dtype, write, false)) return rc;
     }
-    commit_pulls(ps, n, learner_ids, dsts, dst_dtype, write);
+    commit_pulls(ps, n, learner_ids, dsts, dst_dtype, write, !ps->pull_lock_free);
     return PS_OK;
 }
 
@@ -582,10 +625,10 @@ int ps_apply_pull(ps_server *ps, int n, const int *learner_ids, void *const *dst
     } else {
         static const std::vector<int> none;
         if (int rc = launch_batch(ps, b.items, -1, nullptr, none)) return rc;
-        if (int rc = launch_pulls(ps, dsts, dst_dtype, write)) return rc;
+        if (int rc = launch_pulls(ps, dsts, dst_dtype, write, true)) return rc;
     }
     commit_async(ps, b);
-    commit_pulls(ps, n, learner_ids, dsts, dst_dtype, write);
+    commit_pulls(ps, n, learner_ids, dsts, dst_dtype, write, true);
     return PS_OK;
 }
 
@@ -689,6 +732,7 @@ int ps_load(ps_server *ps, const char *path) {
     std::fclose(f);
     if (rc != PS_OK) return rc;
     if (int rc2 = use_device(ps)) return rc2;
+    if (int rc2 = drain_pulls(ps)) return rc2;
     hipError_t e = hipStreamSynchronize(ps->stream);
     if (e == hipSuccess) e = hipMemcpy(ps->w, w.data(), h.n * sizeof(float), hipMemcpyHostToDevice);
     if (e == hipSuccess && ps->v)
@@ -753,6 +797,7 @@ int ps_set_weights(ps_server *ps, const float *src) {
     if (src == nullptr) return fail(PS_EINVAL, "null source");
     if (pending(ps) != 0) return fail(PS_ESTATE, "gradients pending");
     if (int rc = use_device(ps)) return rc;
+    if (int rc = drain_pulls(ps)) return rc;
     hipError_t e = hipMemcpyAsync(ps->w, src, ps->n * sizeof(float), hipMemcpyDeviceToDevice,
                                   ps->stream);
     if (e != hipSuccess) return fail_hip(e, "weights copy");
@@ -801,6 +846,24 @@ int ps_sync(ps_server *ps) {
     if (int rc = use_device(ps)) return rc;
     hipError_t e = hipStreamSynchronize(ps->stream);
     if (e != hipSuccess) return fail_hip(e, "hipStreamSynchronize");
+    return drain_pulls(ps);
+}
+
+int ps_record(ps_server *ps, void *event) {
+    if (int rc = check(ps)) return rc;
+    if (event == nullptr) return fail(PS_EINVAL, "null event");
+    if (int rc = use_device(ps)) return rc;
+    hipError_t e = hipEventRecord(static_cast<hipEvent_t>(event), ps->stream);
+    if (e != hipSuccess) return fail_hip(e, "hipEventRecord");
+    return PS_OK;
+}
+
+int ps_set_pull_stream(ps_server *ps, void *hip_stream) {
+    if (int rc = check(ps)) return rc;
+    if (int rc = use_device(ps)) return rc;
+    if (int rc = drain_pulls(ps)) return rc;
+    ps->pull_lock_free = hip_stream != nullptr;
+    ps->pull_stream = static_cast<hipStream_t>(hip_stream);
     return PS_OK;
 }
 

@@ -53,6 +53,9 @@ _SIGS = {
     "ps_destroy": (None, [_VP]),
     "ps_push": (ctypes.c_int, [_VP, ctypes.c_int, _VP]),
     "ps_push_dtype": (ctypes.c_int, [_VP, ctypes.c_int, _VP, ctypes.c_int]),
+    "ps_push_async": (ctypes.c_int, [_VP, ctypes.c_int, _VP, ctypes.c_int, _VP]),
+    "ps_record": (ctypes.c_int, [_VP, _VP]),
+    "ps_set_pull_stream": (ctypes.c_int, [_VP, _VP]),
     "ps_apply_pending": (ctypes.c_int, [_VP]),
     "ps_apply_sync": (ctypes.c_int, [_VP]),
     "ps_pull": (ctypes.c_int, [_VP, ctypes.c_int, _VP]),
@@ -141,6 +144,18 @@ def ps_push(h: int, learner_id: int, grad_ptr: int) -> int:
 
 def ps_push_dtype(h: int, learner_id: int, grad_ptr: int, dtype: int) -> int:
     return load_library().ps_push_dtype(h, learner_id, grad_ptr, dtype)
+
+
+def ps_push_async(h: int, learner_id: int, grad_ptr: int, dtype: int, ready_event: int) -> int:
+    return load_library().ps_push_async(h, learner_id, grad_ptr, dtype, ready_event)
+
+
+def ps_record(h: int, event: int) -> int:
+    return load_library().ps_record(h, event)
+
+
+def ps_set_pull_stream(h: int, stream_ptr: int) -> int:
+    return load_library().ps_set_pull_stream(h, stream_ptr)
 
 
 def ps_apply_pending(h: int) -> int:
@@ -327,6 +342,29 @@ class ParameterServer:
         self._check(rc, "push")
         self._pending.append(grad)
         return True
+
+    def push_async(self, learner: int, grad, ready_event) -> bool:
+        """Push a gradient still being written on another stream; the apply
+        waits for `ready_event` (a recorded torch.cuda.Event) on the device."""
+        rc = ps_push_async(self.h, learner, self._tensor(grad, "push_async"), _dtype_code(grad),
+                           ready_event.cuda_event)
+        if rc == PS_EFULL:
+            return False
+        self._check(rc, "push_async")
+        self._pending.append((grad, ready_event))
+        return True
+
+    def record(self, event) -> None:
+        """Record a torch.cuda.Event on the server's stream."""
+        if not event.cuda_event:
+            # torch creates the HIP event on first record; make it exist
+            import torch
+            event.record(torch.cuda.current_stream())
+        self._check(ps_record(self.h, event.cuda_event), "record")
+
+    def set_pull_stream(self, stream) -> None:
+        ptr = 0 if stream is None else (stream if isinstance(stream, int) else stream.cuda_stream)
+        self._check(ps_set_pull_stream(self.h, ptr), "set_pull_stream")
 
     def apply_pending(self) -> None:
         self._check(ps_apply_pending(self.h), "apply_pending")

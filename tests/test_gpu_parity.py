@@ -762,3 +762,121 @@ def test_dead_learner_isolated(torch, mode):
     assert 3 not in order[-20:] and srv.stats().pushes_dropped == dropped
     assert parity.bitwise(parity.np_bits(srv.weights_copy()), o.w)
     srv.close()
+
+
+# ---------------------------------------------------------------- concurrency
+
+def test_push_async_waits_for_producer_stream(torch):
+    """A learner writes its gradient on its own stream after a few ms of other
+    work; it pushes with a ready event and the apply is enqueued at once, the
+    host never waiting. The apply must see the finished gradient."""
+    n = 4_000_003
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(50)
+    w0 = (torch.rand(n, generator=gen, device="cuda") - 0.5) * 0.1
+    truth = [torch.randn(n, generator=gen, device="cuda") * 1e-2 for _ in range(3)]
+    grads = [torch.full((n,), float("nan"), device="cuda") for _ in range(3)]
+    busy = torch.randn(1 << 24, generator=gen, device="cuda")
+    producer = torch.cuda.Stream()
+    srv = ps.ParameterServer(n, 0.01, 0.9, queue_depth=4)
+    srv.set_stream(torch.cuda.current_stream())
+    srv.set_weights(w0)
+    torch.cuda.synchronize()
+    events = []
+    with torch.cuda.stream(producer):
+        for j in range(3):
+            for _ in range(100):
+                busy.mul_(1.0000001)      # the learner's "training" before its push
+            grads[j].copy_(truth[j])
+            ev = torch.cuda.Event()
+            ev.record(producer)
+            events.append(ev)
+    for j in range(3):
+        assert srv.push_async(j, grads[j], events[j])
+    srv.apply_pending()
+    w = parity.np_bits(srv.weights_copy())
+    o = orc.OracleServer(parity.np_bits(w0), 0.01, 0.9, depth=4)
+    for j in range(3):
+        o.push(j, parity.np_bits(truth[j]))
+    o.apply_pending()
+    assert parity.bitwise(w, o.w)
+    srv.close()
+
+
+def test_record_lets_producer_reuse_its_buffer(torch):
+    """After ps_record, a producer stream that waits for the event may
+    overwrite the gradient buffer; the apply already read the old values."""
+    n = 8_000_001
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(51)
+    w0 = (torch.rand(n, generator=gen, device="cuda") - 0.5) * 0.1
+    g = torch.randn(n, generator=gen, device="cuda") * 1e-2
+    g_host = parity.np_bits(g)
+    srv = ps.ParameterServer(n, 0.01, 0.0, queue_depth=2)
+    srv.set_stream(torch.cuda.current_stream())
+    srv.set_weights(w0)
+    torch.cuda.synchronize()
+    srv.push(0, g)
+    srv.apply_pending()
+    done = torch.cuda.Event()
+    srv.record(done)
+    producer = torch.cuda.Stream()
+    with torch.cuda.stream(producer):
+        producer.wait_event(done)
+        g.fill_(123.0)                    # the next gradient goes into the same buffer
+    torch.cuda.synchronize()
+    o = orc.OracleServer(parity.np_bits(w0), 0.01, 0.0, depth=2)
+    o.push(0, g_host)
+    o.apply_pending()
+    assert parity.bitwise(parity.np_bits(srv.weights_copy()), o.w)
+    srv.close()
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_lock_free_pull_sees_before_or_after(torch, dtype):
+    """HogWild! mode (Sec. 4.1): a pull on its own stream, concurrent with an
+    apply, writes for every coordinate either the weights before the apply
+    or after it (bitwise one of the two; which one may vary by coordinate).
+    Nondeterministic by design, so checked by this bound, not by bits."""
+    n = 50_000_003
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(52)
+    w0 = (torch.rand(n, generator=gen, device="cuda") - 0.5) * 0.1
+    pool = wl.Rows(32, n, torch.float32, "cuda")
+    for j in range(32):
+        pool[j].normal_(0, 1e-2, generator=gen)
+    srv = ps.ParameterServer(n, 0.01, 0.9, queue_depth=32)
+    srv.set_stream(torch.cuda.current_stream())
+    srv.set_weights(w0)
+    for j in range(32):
+        srv.push(j % 8, pool[j])
+    srv.apply_pending()
+    before = srv.weights_copy()
+    side = torch.cuda.Stream()
+    srv.set_pull_stream(side)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    dst = wl.Rows(1, n, tdt, "cuda")
+    torch.cuda.synchronize()
+    for j in range(32):
+        srv.push(j % 8, pool[31 - j])
+    srv.apply_pending()                   # long apply on the server's stream ...
+    srv.pull_many([3], [dst[0]])          # ... and a pull racing it
+    srv.sync()
+    after = srv.weights_copy()
+    d = parity.np_bits(dst[0])
+    a = parity.np_bits(before)
+    b = parity.np_bits(after)
+    if dtype == "bf16":
+        a, b = orc.f32_to_bf16(a), orc.f32_to_bf16(b)
+    else:
+        a, b, d = a.view(np.uint32), b.view(np.uint32), d.view(np.uint32)
+    assert np.all((d == a) | (d == b))
+    say(f"[lock-free pull] {np.mean(d == b):.3f} of coordinates saw the new weights")
+    # back to ordered pulls: a pull then sees exactly the latest weights
+    srv.set_pull_stream(None)
+    srv.pull_many([3], [dst[0]])
+    srv.sync()
+    want = parity.np_bits(after)
+    got = parity.np_bits(dst[0])
+    assert parity.bitwise(got, want if dtype == "f32" else orc.f32_to_bf16(want))
+    srv.close()
