@@ -38,14 +38,17 @@ def algorithmic_bytes(cfg, mode: str, r: int):
     replica writes): K gradient reads, w read+write, v read+write (momentum),
     R replica writes, plus one more read of w when the pull is its own
     kernel. Returns (per step, per dominant-kernel launch)."""
-    n, k = cfg.n, cfg.depth
+    from paper_1611_06213_amd import accounting as acc
     gb = 2 if cfg.grad_dtype == 1 else 4
     rb = 2 if cfg.pull_dtype == 1 else 4
-    apply_b = k * n * gb + 8 * n + (8 * n if cfg.momentum else 0)
+    apply_b = acc.apply_bytes(cfg.n, cfg.depth, gb, cfg.momentum != 0)
     if mode == "fused":
-        step = apply_b + r * n * rb
+        # one ps_apply_pull call: a single pass up to the fusion limit (one
+        # replica), otherwise the apply kernel and the tiled pull; the events
+        # bracket the whole call
+        step = apply_b + acc.pull_bytes(cfg.n, r, rb, separate=r > 1)
         return step, step
-    return apply_b + 4 * n + r * n * rb, apply_b
+    return apply_b + acc.pull_bytes(cfg.n, r, rb), apply_b
 
 
 def batches(cfg, wl):
@@ -181,6 +184,7 @@ def main():
     import torch
     from paper_1611_06213_amd import ps
     from paper_1611_06213_amd import workloads as wl
+    from paper_1611_06213_amd.accounting import learner_ps_bytes_per_push
 
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
@@ -312,6 +316,10 @@ def main():
         },
         "gbps": round(gbps, 1),
         "pct_peak": round(100 * gbps / PEAK_GBPS, 2),
+        # the paper's accounting (2 x fp32 model per push, Sec. 3), comparable to
+        # its Table "bandwidth_utilized"; not an HBM figure
+        "learner_ps_gbps_paper_accounting": round(
+            pushes / elapsed * learner_ps_bytes_per_push(n) / 1e9, 1),
         "bytes_per_step": round(step_bytes / args.steps),
         "pushes_per_s_device": round(pushes / ((k_ms + p_ms) * args.steps * 1e-3), 2),
         "kernel_ms": {"apply": round(k_ms, 4), **({"pull": round(p_ms, 4)} if p_ms else {})},

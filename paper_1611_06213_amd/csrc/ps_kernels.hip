@@ -326,7 +326,7 @@ __global__ void __launch_bounds__(kBlock) pull_vec(const PullArgs a) {
     if (tid < a.n - (chunks << 2)) pull_chunk<PDT, 1, true>(a, (chunks << 2) + tid);
 }
 
-// Tiled fan-out for R >= 2 replicas. w is cut into tiles of kTileBytes; the
+// Tiled fan-out for R >= 2 replicas. w is cut into tiles (tile_coords); the
 // block index enumerates (tile, replica, block within the tile) with the last
 // fastest, so in-order dispatch walks replica 0 of tile 0, replica 1 of tile
 // 0, ... The R re-reads of a tile then hit the memory-side cache (the tile
@@ -334,12 +334,16 @@ __global__ void __launch_bounds__(kBlock) pull_vec(const PullArgs a) {
 // write stream at a time instead of R interleaved ones, which the memory
 // system serves markedly faster. HBM traffic stays one read of w plus the R
 // replica writes.
-constexpr uint64_t kTileBytes = 8u << 20;   // of w
+// A tile is the coordinates whose replica data fill 8 MiB: 2 Mi coordinates
+// for fp32 replicas, 4 Mi for bf16 (measured best for both).
+constexpr uint64_t kTileReplicaBytes = 8u << 20;
+template <int PDT>
+constexpr uint64_t tile_coords() { return kTileReplicaBytes / (PDT == PS_BF16 ? 2 : 4); }
 constexpr unsigned kTileBlocks = 1024;      // blocks per (tile, replica)
 
 template <int PDT, int E>
 __global__ void __launch_bounds__(kBlock) pull_tiled(const PullArgs a, unsigned bpt) {
-    constexpr uint64_t kTileChunksE = kTileBytes / (4 * E);
+    constexpr uint64_t kTileChunksE = tile_coords<PDT>() / E;
     const uint64_t chunks = a.n / E;
     const unsigned b = blockIdx.x % bpt;
     const unsigned tr = blockIdx.x / bpt;
@@ -463,7 +467,7 @@ hipError_t launch_apply(const ApplyArgs &a, int grad_dtype, int pull_dtype, int 
 template <int PDT, int E>
 void go_pull_tiled(const PullArgs &a, const Geometry &geo, hipStream_t s) {
     // tiles * R * bpt blocks; a tile smaller than a full one needs fewer blocks
-    constexpr uint64_t kTileChunksE = kTileBytes / (4 * E);
+    constexpr uint64_t kTileChunksE = tile_coords<PDT>() / E;
     const uint64_t chunks = a.n / E;
     const uint64_t tiles = chunks == 0 ? 1 : (chunks + kTileChunksE - 1) / kTileChunksE;
     const uint64_t per_tile = chunks < kTileChunksE ? chunks : kTileChunksE;

@@ -1,0 +1,63 @@
+"""The paper's bandwidth accounting (Sec. 3, Table "bandwidth_requirement")
+reproduced from its own printed inputs, and the HBM byte formulas."""
+import os
+
+import pytest
+
+from paper_1611_06213_amd import accounting as acc
+from tests import golden_script
+
+
+def load_table():
+    rows, meta = [], {}
+    for line in open(os.path.join(golden_script.GOLDEN, "bandwidth_requirement.txt")):
+        line = line.split("#", 1)[0].strip()
+        if not line:
+            continue
+        tok = line.split()
+        if tok[0] == "mu":
+            rows.append((int(tok[1]), tok[2:]))
+        else:
+            meta[tok[0]] = tok[1:]
+    return meta, rows
+
+
+# printed RB values that the printed (rounded) TPE reproduces only to 0.3%
+NEAR = {("Watt", 16), ("Watt", 32)}
+
+
+def test_required_bandwidth_reproduces_table():
+    """RB = 2 * ModelSize * (N / mu) / TPE, rounded to two decimals, equals the
+    printed RB for 36 of the 38 entries of Watt, Age, Yelp, CIFAR and
+    ImageNet; Watt at mu = 16 and 32 come within 0.3% (the printed TPE is
+    itself rounded). Joule does not reproduce: its header lists 2.46K
+    samples, its corpus table 2.4k, and neither gives the printed values
+    (6.74 or 6.58 vs 7.00 GB/s at mu = 1), an inconsistency of the table."""
+    meta, rows = load_table()
+    names = meta["workloads"]
+    exact = near = 0
+    for mu, vals in rows:
+        for i, name in enumerate(names):
+            tpe, rb = vals[2 * i], vals[2 * i + 1]
+            if tpe == "-" or name == "Joule":
+                continue
+            got = acc.required_bandwidth(float(meta["model_mb"][i]) * 1e6, float(meta["samples"][i]),
+                                         mu, float(tpe)) / 1e9
+            if (name, mu) in NEAR:
+                assert abs(got / float(rb) - 1) < 0.003, (name, mu, got, rb)
+                near += 1
+            else:
+                assert f"{got:.2f}" == rb, (name, mu, got, rb)
+                exact += 1
+    assert (exact, near) == (36, 2)
+    joule = acc.required_bandwidth(7.69e6, 2460, 1, 5.61) / 1e9
+    assert abs(joule - 7.00) > 0.2
+
+
+def test_byte_formulas():
+    n = 138_357_544
+    assert acc.apply_bytes(n, 32, 4, True) == 19_923_486_336
+    assert acc.pull_bytes(n, 16, 4) == 9_408_312_992
+    assert acc.pull_bytes(n, 16, 4, separate=False) == 16 * 4 * n
+    assert acc.apply_bytes(200_000_000, 32, 2, True) == 16_000_000_000
+    assert acc.learner_ps_bytes_per_push(n) == 8 * n

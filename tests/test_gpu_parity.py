@@ -229,9 +229,10 @@ def test_misaligned_buffers_scalar_path(torch, og, od):
 
 @pytest.mark.parametrize("r", [2, 3, 16, 64])
 def test_tiled_pull_many_tiles_ragged(torch, r):
-    """The tiled fan-out over several full tiles (8 MiB of w each), a partial
-    tile and a ragged tail: every replica equals w (fp32) or RNE(w) (bf16)."""
-    n = 2 * (8 << 20) // 4 + 1234567 + 3
+    """The tiled fan-out over several full tiles (8 MiB of replica data each:
+    2 Mi coordinates for fp32, 4 Mi for bf16), a partial tile and a ragged
+    tail: every replica equals w (fp32) or RNE(w) (bf16)."""
+    n = 2 * (4 << 20) + 1234567 + 3
     gen = torch.Generator(device="cuda")
     gen.manual_seed(r)
     w0 = (torch.rand(n, generator=gen, device="cuda") - 0.5) * 0.1
