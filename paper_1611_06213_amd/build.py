@@ -17,6 +17,10 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libgadeips.so")
+# the same source with contraction allowed (fused multiply-adds); within 1e-6
+# relative of the oracle instead of bitwise
+LIB_FMA = os.path.join(HERE, "libgadeips_fma.so")
+FMA_FLAGS = ["-ffp-contract=fast", "-DPS_FP_CONTRACT=1"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 SOURCES = [os.path.join(CSRC, "ps_server.cpp"), os.path.join(CSRC, "ps_kernels.hip")]
@@ -32,7 +36,10 @@ FLAGS = [
 
 def build(verbose: bool = False, out: str = LIB, extra=()) -> str:
     tmp = out + ".tmp"
-    cmd = [HIPCC, *FLAGS, *extra, *SOURCES, "-o", tmp]
+    flags = list(FLAGS)
+    if any(x.startswith("-ffp-contract=") for x in extra):
+        flags = [f for f in flags if not f.startswith("-ffp-contract=")]
+    cmd = [HIPCC, *flags, *extra, *SOURCES, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -43,5 +50,10 @@ def build(verbose: bool = False, out: str = LIB, extra=()) -> str:
     return out
 
 
+def build_all(verbose: bool = False):
+    """Both flavours: the bitwise default and the contraction-allowed one."""
+    return build(verbose), build(verbose, out=LIB_FMA, extra=FMA_FLAGS)
+
+
 if __name__ == "__main__":
-    print(build(verbose=True))
+    print(build_all(verbose=True))

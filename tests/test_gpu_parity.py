@@ -881,3 +881,80 @@ def test_lock_free_pull_sees_before_or_after(torch, dtype):
     got = parity.np_bits(dst[0])
     assert parity.bitwise(got, want if dtype == "f32" else orc.f32_to_bf16(want))
     srv.close()
+
+
+# ---------------------------------------------------------------- contraction-allowed build
+
+@pytest.fixture
+def fma_library(torch):
+    """Swap the binding to libgadeips_fma.so (the same source built with
+    -ffp-contract=fast) for one test."""
+    from paper_1611_06213_amd import build as lib_build
+    if not os.path.exists(lib_build.LIB_FMA):
+        pytest.fail("libgadeips_fma.so is not built")
+    saved = ps.load_library()
+    ps._lib = ps.load_library(lib_build.LIB_FMA)
+    yield
+    ps._lib = saved
+
+
+@pytest.mark.parametrize("name", list(wl.CONFIGS))
+def test_fma_flavour_within_1e6_per_apply(torch, fma_library, name):
+    """Built with contraction allowed, one apply of a full batch (K gradients,
+    with momentum where the workload has it) from the same starting state
+    stays within 1e-6 relative (R12: max|a-b| / max(|b|, RMS(w0))) of the
+    oracle's sequential binary32 result, for the weights and the replicas."""
+    cfg = wl.CONFIGS[name].scaled(SMALL_N, pool=min(wl.CONFIGS[name].pool, 64))
+    pool = wl.make_pool(cfg, "cuda")
+    w0 = wl.make_w0(cfg, "cuda")
+    rdt = torch.bfloat16 if cfg.pull_dtype == wl.BF16 else torch.float32
+    reps = wl.Rows(2, cfg.n, rdt, "cuda")
+    srv = ps.ParameterServer(cfg.n, cfg.lr, cfg.momentum, queue_depth=cfg.depth)
+    srv.set_weights(w0)
+    o = orc.OracleServer(parity.np_bits(w0), cfg.lr, cfg.momentum, depth=cfg.depth)
+    for j in range(cfg.depth):
+        srv.push(j % cfg.learners, pool[j])
+        o.push(j % cfg.learners, parity.np_bits(pool[j]))
+    srv.apply_pull([0, 1], reps.rows)
+    o.apply_pending()
+    tau = float(np.sqrt(np.mean(parity.np_bits(w0).astype(np.float64) ** 2)))
+    a = parity.np_bits(srv.weights_copy()).astype(np.float64)
+    b = o.w.astype(np.float64)
+    err = float(np.max(np.abs(a - b) / np.maximum(np.abs(b), tau)))
+    say(f"[fma] {name}: one apply of {cfg.depth}, R12 error {err:.2e}")
+    assert err <= 1e-6
+    if cfg.pull_dtype == wl.F32:
+        r = parity.np_bits(reps[1]).astype(np.float64)
+        assert np.max(np.abs(r - b) / np.maximum(np.abs(b), tau)) <= 1e-6
+    srv.close()
+    del pool, reps
+    free(torch)
+
+
+@pytest.mark.parametrize("name", list(wl.CONFIGS))
+def test_fma_flavour_whole_schedule_drift_bounded(torch, fma_library, name):
+    """Over a whole schedule the fused and the separately rounded runs drift
+    apart like a random walk of per-step rounding differences: each step
+    differs by at most about one ulp of the weight, so after T steps
+    |a-b| <= 2*T*ulp(max|w|). Checked, and the R12 drift reported; with
+    momentum the runs do differ (contraction really happened)."""
+    cfg = wl.CONFIGS[name].scaled(SMALL_N, pool=min(wl.CONFIGS[name].pool, 64))
+    ev = wl.schedule(cfg)
+    pool = wl.make_pool(cfg, "cuda")
+    w0 = wl.make_w0(cfg, "cuda")
+    ranges = [(0, cfg.n)]
+    g = parity.gpu_replay(cfg, ev, pool, w0, ranges, fused=True)
+    ps_, w0s = parity.host_inputs(cfg, pool, w0, ranges)
+    o = parity.oracle_replay(cfg, ev, ps_, w0s, ranges)
+    tau = float(np.sqrt(np.mean(w0s[0].astype(np.float64) ** 2)))
+    a, b = g["w"][0].astype(np.float64), o["w"][0].astype(np.float64)
+    T = o["ts"]
+    ulp = float(np.spacing(np.float32(max(np.abs(b).max(), np.abs(w0s[0]).max()) * 1.5)))
+    assert np.max(np.abs(a - b)) <= 2 * T * ulp
+    err = float(np.max(np.abs(a - b) / np.maximum(np.abs(b), tau)))
+    say(f"[fma] {name}: {T} sequential pushes, R12 drift {err:.2e}")
+    if cfg.momentum:
+        assert not parity.bitwise(g["w"][0], o["w"][0])
+    assert g["staleness"] == o["staleness"] and g["ts"] == o["ts"]
+    del pool
+    free(torch)
