@@ -316,27 +316,3 @@ class OracleServer:
             return ESTATE
         self.depth = depth
         return OK
-
-
-def replay(server: OracleServer, events, grads, pull_dtype: int = F32, on_pull=None):
-    """Drive `server` through a workload schedule.
-
-    grads(buf) returns the gradient slice of pool buffer `buf`; learner r
-    pulls into replica key r. on_pull(learners, server) is called after each
-    pull event (the caller may snapshot replicas there)."""
-    for ev in events:
-        kind = type(ev).__name__
-        if kind == "Push":
-            rc = server.push(ev.learner, grads(ev.buf))
-            if rc != OK:
-                raise RuntimeError(f"oracle push failed: {rc}")
-        elif kind == "Apply":
-            server.apply_pending()
-        elif kind == "Pull":
-            for l in ev.learners:
-                server.pull(l, l, pull_dtype)
-            if on_pull is not None:
-                on_pull(ev.learners, server)
-        else:
-            raise ValueError(kind)
-    return server
