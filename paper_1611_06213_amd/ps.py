@@ -97,6 +97,14 @@ def load_library(path: Optional[str] = None):
         raise RuntimeError(
             f"{p} is not built: run `python -c 'import __graft_entry__ as g; g.build()'` "
             "(the parameter server has no CPU fallback)")
+    # torch bundles its own HIP runtime. Loading torch first makes the
+    # library bind to that one (same soname); loading the library first would
+    # put a second HIP runtime in the process, and torch's streams and
+    # allocations would not be valid in it.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     L = ctypes.CDLL(p)
     for name, (res, args) in _SIGS.items():
         f = getattr(L, name)

@@ -70,3 +70,22 @@ def test_validation_without_device(lib):
 def test_binding_refuses_missing_library(tmp_path):
     with pytest.raises(RuntimeError, match="not built"):
         ps.load_library(str(tmp_path / "missing.so"))
+
+
+def test_one_hip_runtime_whatever_the_import_order():
+    """Loading the library through the binding before anything else imports
+    torch must still leave a single HIP runtime in the process (torch's), so
+    torch streams and allocations are valid in the library."""
+    import ast
+    import subprocess
+    import sys
+    code = ("import sys; sys.path.insert(0, %r)\n"
+            "from paper_1611_06213_amd import ps\n"
+            "ps.load_library()\n"
+            "import torch\n"
+            "maps = open('/proc/self/maps').read().splitlines()\n"
+            "print(sorted({l.split()[-1] for l in maps if 'libamdhip64' in l}))\n") % ROOT
+    out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=300)
+    assert out.returncode == 0, out.stderr[-2000:]
+    libs = ast.literal_eval(out.stdout.strip().splitlines()[-1])
+    assert len(libs) == 1, libs
