@@ -130,8 +130,19 @@ def cpu_baseline(cfg, pool, w0, pulls_per_step: int, seconds: float, distinct: i
         "kind": "oracle",
         "sample": (f"{steps} whole steps ({cfg.depth} pushes + apply + {pulls_per_step} pulls) "
                    f"over the full {cfg.n:,}-parameter vector, 1 thread, pushes cycling over "
-                   f"{distinct} host copies of pool buffers; {t1 - t0:.1f} s of CPU work"),
+                   f"{distinct} host copies of pool buffers; {t1 - t0:.1f} s of CPU work on "
+                   f"{cpu_model()} ({os.cpu_count()} logical CPUs visible)"),
     }
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown CPU"
 
 
 def copy_ceiling(torch, ps, lib, n: int = 1 << 28, reps: int = 10):
@@ -162,19 +173,21 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="vgg16")
-    ap.add_argument("--mode", choices=["fused", "separate"], default="separate",
+    ap.add_argument("--mode", choices=["fused", "separate", "hogwild"], default="separate",
                     help="separate: ps_apply_pending + ps_pull_many (one kernel each, timed "
-                         "apart); fused: ps_apply_pull (the same kernels above one replica)")
+                         "apart); fused: ps_apply_pull (the same kernels above one replica); "
+                         "hogwild: pulls lock-free on a second stream, overlapping the next "
+                         "apply (Sec. 4.1)")
     ap.add_argument("--apply", choices=["asgd", "sync"], default="asgd",
                     help="asgd: the workload's K-gradient asynchronous applies; sync: one "
                          "synchronous step (Eq. ssgd) per step over one gradient per learner")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=8.0)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run a plain 1 GiB copy (known bytes) for counter calibration")
     args = ap.parse_args()
 
-    if args.apply == "sync" and args.mode == "fused":
+    if args.apply == "sync" and args.mode != "separate":
         ap.error("--apply sync runs apply and pull as separate calls (--mode separate)")
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the parameter server here runs on a single "
@@ -213,6 +226,11 @@ def main():
     assert ps.ps_set_stream(h, stream.cuda_stream) == 0
     assert ps.ps_set_weights(h, w0.data_ptr()) == 0
 
+    pstream = None
+    if args.mode == "hogwild":
+        pstream = torch.cuda.Stream(device=stream.device)     # default priority
+        assert ps.ps_set_pull_stream(h, pstream.cuda_stream) == 0
+
     gptr = [pool[j].data_ptr() for j in range(cfg.pool)]
     calls = []
     for pushes_b, pulls_b in plan:
@@ -238,11 +256,13 @@ def main():
                 ev[1].record(stream)
         else:
             rc = lib.ps_apply_sync(h) if args.apply == "sync" else lib.ps_apply_pending(h)
+            ps_ = pstream if pstream is not None else stream
             if ev is not None:
                 ev[1].record(stream)
+                ev[2].record(ps_)
             rc = rc or lib.ps_pull_many(h, r, ids, dptr, pdt)
             if ev is not None:
-                ev[2].record(stream)
+                ev[3].record(ps_)
         if rc != 0:
             raise RuntimeError(ps.ps_last_error())
         return r
@@ -251,7 +271,7 @@ def main():
         step()
     torch.cuda.synchronize()
 
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     rs = []
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -264,8 +284,10 @@ def main():
     pushes = K * args.steps
     step_bytes = sum(algorithmic_bytes(cfg, args.mode, r)[0] for r in rs)
     launch_bytes = sum(algorithmic_bytes(cfg, args.mode, r)[1] for r in rs) / args.steps
-    k_ms = sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps
-    p_ms = (sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps) if args.mode == "separate" else 0.0
+    k_each = sorted(e[0].elapsed_time(e[1]) for e in evs)
+    k_ms = sum(k_each) / args.steps
+    p_each = sorted(e[2].elapsed_time(e[3]) for e in evs) if args.mode != "fused" else [0.0]
+    p_ms = sum(p_each) / len(p_each)
     gbps = step_bytes / elapsed / 1e9
     achieved = launch_bytes / (k_ms * 1e-3) / 1e9
     label = f"{args.config}-{args.mode}" + ("-sync" if args.apply == "sync" else "")
@@ -321,8 +343,11 @@ def main():
         "learner_ps_gbps_paper_accounting": round(
             pushes / elapsed * learner_ps_bytes_per_push(n) / 1e9, 1),
         "bytes_per_step": round(step_bytes / args.steps),
+        # kernel time summed over both streams (with hogwild the two overlap)
         "pushes_per_s_device": round(pushes / ((k_ms + p_ms) * args.steps * 1e-3), 2),
         "kernel_ms": {"apply": round(k_ms, 4), **({"pull": round(p_ms, 4)} if p_ms else {})},
+        "kernel_ms_median": {"apply": round(k_each[len(k_each) // 2], 4),
+                             **({"pull": round(p_each[len(p_each) // 2], 4)} if p_ms else {})},
         **({"pull_kernel_gbps": round(pull_bytes / (p_ms * 1e-3) / 1e9, 1)} if p_ms else {}),
         "roofline": {
             "bound": "hbm", "kernel": kern,
