@@ -30,7 +30,7 @@ sys.path.insert(0, ROOT)
 PEAK_GBPS = 8000.0          # MI355X HBM3E, published
 METRIC = "gradient pushes applied/sec + achieved HBM GB/s (% of peak), 1 MI355X"
 KERNEL_SRC = os.path.join(ROOT, "paper_1611_06213_amd", "csrc", "ps_kernels.hip")
-COUNTERS = os.path.join(ROOT, "profiles", "traffic_vgg16.txt")
+COUNTERS = os.path.join(ROOT, "profiles", "traffic_apply_vec_vgg16.txt")
 
 
 def algorithmic_bytes(cfg, mode: str, r: int):
