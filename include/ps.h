@@ -49,6 +49,12 @@
  *
  * Status codes: every int-returning call returns PS_OK (0) or a negative
  * PS_E* code; ps_last_error() then describes the failure (per thread).
+ * Argument errors (PS_EINVAL, PS_EFULL, PS_ESTATE) are found before any
+ * state changes or device work. A PS_EHIP from a launch means the device or
+ * runtime has failed: the gradients of an apply whose kernels were all
+ * enqueued count as applied, but if an apply over gradients of both dtypes
+ * fails between its two launches the weights hold part of the batch, and
+ * the handle should only be destroyed.
  */
 #ifndef GADEI_PS_H
 #define GADEI_PS_H
@@ -133,9 +139,9 @@ int ps_push_async(ps_server *ps, int learner_id, const void *grad, int dtype, vo
 
 /* Apply the pending gradients -- FIFO mode: all of them, oldest first;
  * round-robin mode: up to `depth` in service order (ps_set_queue_mode) --
- * each as one step of Eq. "asgd", and remove them from their queues. Enqueues one kernel per run of equal-dtype
- * gradients (one in the usual case) on the server's stream; returns without
- * waiting. The timestamp grows by the number applied; staleness of each is
+ * each as one step of Eq. "asgd", and remove them from their queues.
+ * Enqueues one kernel per run of equal-dtype gradients (one in the usual
+ * case) on the server's stream; returns without waiting. The timestamp grows by the number applied; staleness of each is
  * recorded (ps_last_staleness, ps_last_applied, ps_get_stats). With nothing
  * pending no device work is done and the last-apply queries report 0. */
 int ps_apply_pending(ps_server *ps);
@@ -238,8 +244,9 @@ uint64_t ps_timestamp(const ps_server *ps);
 int ps_pending(const ps_server *ps);
 
 /* Staleness of each gradient applied by the most recent apply call
- * (ps_apply_pending, ps_apply_pull, ps_apply_sync), in the order applied. Writes min(count, cap) values to out and returns count (or
- * a negative status). */
+ * (ps_apply_pending, ps_apply_pull, ps_apply_sync), in the order applied.
+ * Writes min(count, cap) values to out and returns count (or a negative
+ * status). */
 int ps_last_staleness(const ps_server *ps, int64_t *out, int cap);
 
 /* Learner ids of the gradients applied by the most recent apply call, in
@@ -257,10 +264,10 @@ int ps_drop_learner(ps_server *ps, int learner_id);
 /* Checkpoint (Sec. 4.3: the server checkpoints its parameters so that a
  * restart resumes from the last checkpoint). ps_save writes w, v, the
  * timestamp, the round-robin position and every learner's timestamp to
- * `path` (waits for the server's stream first); ps_load restores them into
+ * `path` (waits for the server's stream and lock-free pulls first); ps_load restores them into
  * a server created with the same n_params, lr and momentum, after checking
- * the whole file (format, sizes, checksum) -- on any failure the server is
- * unchanged. Pull history and statistics start afresh after a load (learners
+ * the whole file (format version, sizes, a checksum over header and data)
+ * -- on any failure the server is unchanged. Pull history and statistics start afresh after a load (learners
  * pull again after a restart). Both need an empty queue (PS_ESTATE
  * otherwise); file errors give PS_EIO, mismatched servers PS_EINVAL.
  * Continuing from a loaded checkpoint gives the bits of the uninterrupted

@@ -23,7 +23,8 @@ LIB_FMA = os.path.join(HERE, "libgadeips_fma.so")
 FMA_FLAGS = ["-ffp-contract=fast", "-DPS_FP_CONTRACT=1"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = [os.path.join(CSRC, "ps_server.cpp"), os.path.join(CSRC, "ps_kernels.hip")]
+SOURCES = [os.path.join(CSRC, "ps_server.cpp"), os.path.join(CSRC, "ps_protocol.cpp"),
+           os.path.join(CSRC, "ps_kernels.hip")]
 
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

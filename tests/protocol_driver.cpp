@@ -1,0 +1,148 @@
+// Drives the parameter server's host protocol (gadei::Protocol: queues,
+// timestamps, pull skipping, staleness) from a command script on stdin, the
+// way the C ABI drives it around its kernel launches, and prints one line per
+// command. Built with the host sanitizers by tests/test_protocol.py, which
+// runs the same script through the oracle's server and compares the lines.
+//
+// Commands (one per line):
+//   push L DT ID          gradient ID of learner L, dtype DT
+//   apply                 asynchronous apply (ps_apply_pending)
+//   sync                  synchronous step (ps_apply_sync)
+//   pull DT L1 D1 ...     ordered pulls of learners Li into buffers Di (ps_pull_many)
+//   applypull DT L1 D1 .. ps_apply_pull
+//   drop L | depth K | mode M S | skip 0|1 | state
+#include <cstdio>
+#include <iostream>
+#include <sstream>
+#include <string>
+#include <vector>
+
+#include "ps_protocol.h"
+
+namespace {
+
+const void *grad_ptr(long id) { return reinterpret_cast<const void *>((id + 1) * 64); }
+void *dst_ptr(long d) { return reinterpret_cast<void *>((d + 1) * 4096); }
+
+void print_applied(const gadei::Protocol &p) {
+    std::printf(" ts=%llu", static_cast<unsigned long long>(p.ts));
+    for (size_t i = 0; i < p.last_applied.size(); ++i)
+        std::printf(" %d:%lld", p.last_applied[i], static_cast<long long>(p.last_staleness[i]));
+}
+
+void read_pulls(std::istringstream &in, int &dt, std::vector<int> &ids, std::vector<void *> &dsts) {
+    in >> dt;
+    long l, d;
+    while (in >> l >> d) {
+        ids.push_back(static_cast<int>(l));
+        dsts.push_back(dst_ptr(d));
+    }
+}
+
+void print_written(const std::vector<int> &write) {
+    std::printf(" w=");
+    for (size_t i = 0; i < write.size(); ++i) std::printf(i ? ",%d" : "%d", write[i]);
+}
+
+}  // namespace
+
+int main() {
+    gadei::Protocol p;
+    std::string line;
+    while (std::getline(std::cin, line)) {
+        std::istringstream in(line);
+        std::string cmd;
+        if (!(in >> cmd)) continue;
+        if (cmd == "push") {
+            long l, dt, id;
+            in >> l >> dt >> id;
+            std::printf("push %d", p.push(static_cast<int>(l), static_cast<int>(dt), grad_ptr(id),
+                                          nullptr));
+        } else if (cmd == "apply") {
+            if (p.pending() == 0) {
+                p.clear_last();
+            } else {
+                gadei::Batch b;
+                p.plan_async(b);
+                p.commit_async(b);
+            }
+            std::printf("apply 0");
+            print_applied(p);
+        } else if (cmd == "sync") {
+            int rc = 0;
+            if (p.pending() == 0) {
+                p.clear_last();
+            } else {
+                gadei::Batch b;
+                rc = p.plan_sync(b);
+                if (rc == 0) p.commit_sync(b);
+            }
+            std::printf("sync %d", rc);
+            print_applied(p);
+        } else if (cmd == "pull") {
+            int dt = 0;
+            std::vector<int> ids;
+            std::vector<void *> dsts;
+            read_pulls(in, dt, ids, dsts);
+            std::vector<int> write;
+            const int n = static_cast<int>(ids.size());
+            int rc = p.plan_pulls(n, ids.data(), dsts.data(), dt, p.ts, write);
+            if (rc == 0) p.commit_pulls(n, ids.data(), dsts.data(), dt, write, true);
+            std::printf("pull %d", rc);
+            print_written(write);
+        } else if (cmd == "applypull") {
+            int dt = 0;
+            std::vector<int> ids;
+            std::vector<void *> dsts;
+            read_pulls(in, dt, ids, dsts);
+            const int n = static_cast<int>(ids.size());
+            std::vector<int> write;
+            int rc;
+            if (p.pending() == 0) {
+                rc = p.plan_pulls(n, ids.data(), dsts.data(), dt, p.ts, write);
+                if (rc == 0) {
+                    p.commit_pulls(n, ids.data(), dsts.data(), dt, write, true);
+                    p.clear_last();
+                }
+            } else {
+                gadei::Batch b;
+                p.plan_async(b);
+                rc = p.plan_pulls(n, ids.data(), dsts.data(), dt, p.ts + b.items.size(), write);
+                if (rc == 0) {
+                    p.commit_async(b);
+                    p.commit_pulls(n, ids.data(), dsts.data(), dt, write, true);
+                }
+            }
+            std::printf("applypull %d", rc);
+            print_applied(p);
+            print_written(write);
+        } else if (cmd == "drop") {
+            long l;
+            in >> l;
+            std::printf("drop %d", p.drop_learner(static_cast<int>(l)));
+        } else if (cmd == "depth") {
+            long k;
+            in >> k;
+            std::printf("depth %d", p.set_depth(static_cast<int>(k)));
+        } else if (cmd == "mode") {
+            long m, s;
+            in >> m >> s;
+            std::printf("mode %d", p.set_mode(static_cast<int>(m), static_cast<int>(s)));
+        } else if (cmd == "skip") {
+            long on;
+            in >> on;
+            p.pull_skip = on != 0;
+            std::printf("skip");
+        } else if (cmd == "state") {
+            std::printf("state ts=%llu pending=%zu pulls=%llu skipped=%llu",
+                        static_cast<unsigned long long>(p.ts), p.pending(),
+                        static_cast<unsigned long long>(p.stats.pulls),
+                        static_cast<unsigned long long>(p.stats.pulls_skipped));
+        } else {
+            std::fprintf(stderr, "unknown command: %s\n", cmd.c_str());
+            return 2;
+        }
+        std::printf("\n");
+    }
+    return 0;
+}

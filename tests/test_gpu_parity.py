@@ -696,6 +696,15 @@ def test_checkpoint_errors_leave_server_unchanged(torch, tmp_path):
     raw[200] ^= 1
     open(bad, "wb").write(bytes(raw))
     assert ps.ps_load(b.h, bad) == ps.PS_EIO and "checksum" in ps.ps_last_error()
+    # the header is checksummed too: a flipped timestamp bit (bytes 32..39)
+    hdr = bytearray(open(path, "rb").read())
+    hdr[32] ^= 1
+    open(bad, "wb").write(bytes(hdr))
+    assert ps.ps_load(b.h, bad) == ps.PS_EIO and "checksum" in ps.ps_last_error()
+    hdr[32] ^= 1
+    hdr[8] = 1                                               # format version field
+    open(bad, "wb").write(bytes(hdr))
+    assert ps.ps_load(b.h, bad) == ps.PS_EIO and "version" in ps.ps_last_error()
     open(bad, "wb").write(bytes(raw[:1000]))
     assert ps.ps_load(b.h, bad) == ps.PS_EIO
     assert ps.ps_load(b.h, str(tmp_path / "missing.ckpt")) == ps.PS_EIO

@@ -1,0 +1,169 @@
+"""The library's host protocol (gadei::Protocol: FIFO and round-robin queues,
+timestamps and staleness, pull skipping, dead learners, queue settings)
+against the oracle's server, on the CPU under AddressSanitizer and
+UndefinedBehaviorSanitizer.
+
+tests/protocol_driver.cpp feeds a command script to the protocol code the C
+ABI uses; the same script runs through oracle.server.OracleServer (on a
+one-coordinate model, whose arithmetic is irrelevant here) and the printed
+lines must match exactly: every push status, which learner each applied
+gradient came from and its staleness (Sec. 2.1), the timestamp, which pulls
+write and which are skipped as current (Sec. 4.1), drop counts and error
+codes. Scripts are seeded random mixes of every command."""
+import os
+import shutil
+import subprocess
+
+import numpy as np
+import pytest
+
+from oracle import server as orc
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+CSRC = os.path.join(ROOT, "paper_1611_06213_amd", "csrc")
+
+
+@pytest.fixture(scope="module")
+def driver(tmp_path_factory):
+    if shutil.which("g++") is None:
+        pytest.skip("g++ not available")
+    exe = str(tmp_path_factory.mktemp("protocol") / "protocol_driver")
+    cmd = ["g++", "-std=c++17", "-O1", "-g", "-fno-omit-frame-pointer", "-Wall", "-Wextra",
+           "-Werror", "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
+           "-I", os.path.join(ROOT, "include"), "-I", CSRC,
+           os.path.join(CSRC, "ps_protocol.cpp"), os.path.join(ROOT, "tests", "protocol_driver.cpp"),
+           "-o", exe]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0 and "asan" in (r.stderr + r.stdout).lower():
+        pytest.skip("sanitizer runtime not installed: " + r.stderr[-200:])
+    assert r.returncode == 0, r.stderr
+    return exe
+
+
+def run_driver(exe, lines):
+    env = dict(os.environ, ASAN_OPTIONS="detect_leaks=1:abort_on_error=1:verify_asan_link_order=0",
+               UBSAN_OPTIONS="print_stacktrace=1:halt_on_error=1")
+    r = subprocess.run([exe], input="\n".join(lines) + "\n", capture_output=True, text=True,
+                       env=env, timeout=120)
+    assert r.returncode == 0, r.stderr[-3000:]
+    return r.stdout.splitlines()
+
+
+def run_oracle(lines):
+    o = orc.OracleServer(np.zeros(1, np.float32), 0.01, 0.0, depth=32)
+    last = []
+    out = []
+
+    def applied():
+        return f" ts={o.ts}" + "".join(f" {l}:{s}" for l, s in last)
+
+    def pulls(t):
+        dt = int(t[1])
+        pairs = [(int(t[i]), int(t[i + 1])) for i in range(2, len(t), 2)]
+        return ",".join(str(i) for i, (l, d) in enumerate(pairs) if o.pull(l, d, dt))
+
+    for line in lines:
+        t = line.split()
+        c = t[0]
+        if c == "push":
+            l, dt, gid = int(t[1]), int(t[2]), int(t[3])
+            g = (np.array([gid], np.uint16) if dt == orc.BF16
+                 else np.array([gid * 1e-3], np.float32))
+            out.append(f"push {o.push(l, g)}")
+        elif c in ("apply", "sync", "applypull"):
+            n0 = len(o.staleness)
+            rc = o.apply_sync() if c == "sync" else o.apply_pending()
+            if rc == orc.OK:
+                last = list(zip(o.applied_order[n0:], o.staleness[n0:]))
+            line_out = f"{c} {rc}" + applied()
+            if c == "applypull":
+                line_out += " w=" + pulls(t)
+            out.append(line_out)
+        elif c == "pull":
+            out.append("pull 0 w=" + pulls(t))
+        elif c == "drop":
+            out.append(f"drop {o.drop_learner(int(t[1]))}")
+        elif c == "depth":
+            out.append(f"depth {o.set_depth(int(t[1]))}")
+        elif c == "mode":
+            out.append(f"mode {o.set_queue_mode(int(t[1]), int(t[2]))}")
+        elif c == "skip":
+            o.pull_skip = t[1] != "0"
+            out.append("skip")
+        elif c == "state":
+            out.append(f"state ts={o.ts} pending={o.pending()} pulls={o.pulls} "
+                       f"skipped={o.pulls_skipped}")
+        else:
+            raise ValueError(c)
+    return out
+
+
+def script(seed, learners, n_cmds=700, bf16_rate=0.1):
+    rng = np.random.default_rng(seed)
+    lines = []
+    gid = 0
+    kinds = ["push", "apply", "sync", "pull", "applypull", "drop", "depth", "mode", "skip", "state"]
+    p = np.array([44, 10, 5, 12, 8, 3, 5, 4, 3, 6], float)
+    for _ in range(n_cmds):
+        c = kinds[rng.choice(len(kinds), p=p / p.sum())]
+        if c == "push":
+            dt = orc.BF16 if rng.random() < bf16_rate else orc.F32
+            lines.append(f"push {rng.integers(learners)} {dt} {gid}")
+            gid += 1
+        elif c in ("pull", "applypull"):
+            k = int(rng.integers(1, min(learners, 6) + 1))
+            ls = rng.choice(learners, size=k, replace=False)
+            dt = int(rng.integers(2))
+            pairs = " ".join(f"{l} {2 * l + int(rng.random() < 0.2)}" for l in ls)
+            lines.append(f"{c} {dt} {pairs}")
+        elif c == "drop":
+            lines.append(f"drop {rng.integers(learners)}")
+        elif c == "depth":
+            lines.append(f"depth {rng.choice([0, 1, 2, 4, 8, 16, 32, 64, 65])}")
+        elif c == "mode":
+            lines.append(f"mode {rng.choice([0, 1, 1, 2])} {rng.choice([1, 2, 3, 8, 64])}")
+        elif c == "skip":
+            lines.append(f"skip {int(rng.random() < 0.7)}")
+        else:
+            lines.append(c)
+    lines.append("state")
+    return lines
+
+
+@pytest.mark.parametrize("learners", [1, 3, 8, 40])
+@pytest.mark.parametrize("seed", range(6))
+def test_protocol_matches_oracle(driver, seed, learners):
+    lines = script(1000 * learners + seed, learners)
+    got = run_driver(driver, lines)
+    want = run_oracle(lines)
+    assert len(got) == len(want) == len(lines)
+    for i, (g, w) in enumerate(zip(got, want)):
+        assert g == w, f"command {i} `{lines[i]}`: library `{g}` vs oracle `{w}`"
+
+
+def test_scripts_reach_every_outcome(driver):
+    """The random scripts exercise what they are meant to: full queues,
+    skipped and written pulls, mixed-dtype synchronous steps refused, queue
+    settings refused while gradients wait, round-robin service."""
+    seen = set()
+    for learners in (1, 3, 8, 40):
+        for seed in range(6):
+            lines = script(1000 * learners + seed, learners)
+            for cmd, res in zip(lines, run_oracle(lines)):
+                c = cmd.split()[0]
+                if c == "push" and res == f"push {orc.EFULL}":
+                    seen.add("full")
+                if c == "sync" and res.startswith(f"sync {orc.EINVAL}"):
+                    seen.add("mixed sync")
+                if c in ("depth", "mode") and res.endswith(str(orc.ESTATE)):
+                    seen.add("state refused")
+                if c == "mode" and res == "mode 0" and cmd.split()[1] == "1":
+                    seen.add("round robin")
+                if c == "pull":
+                    written = res.split("w=")[1]
+                    if (len(cmd.split()) - 2) // 2 > len(written.split(",") if written else []):
+                        seen.add("skipped pull")
+                if c == "drop" and res != "drop 0":
+                    seen.add("dropped")
+    assert seen == {"full", "mixed sync", "state refused", "round robin", "skipped pull",
+                    "dropped"}, seen
