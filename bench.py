@@ -6,8 +6,9 @@ pushing Laplace(0, 1e-3) gradients in seeded random order; K = 32 gradients
 folded per apply; after each apply all 16 learners pull fp32 replicas).
 One step = 32 pushes + one apply + one 16-replica pull, i.e. one pass of the
 whole hot path over one batch. Inputs (64 distinct gradient buffers, 35 GB)
-are resident in HBM before timing starts, each buffer on its own 2 MiB-aligned
-row (as separately allocated learner buffers would be).
+are resident in HBM before timing starts. By default they and the replicas
+are the server's own rows (ps_alloc_rows: the queue slots learners fill);
+--layout torch puts every buffer in its own torch allocation instead.
 
 Prints one JSON line (rank 0, N = 1). Extra keys: the dominant kernel's
 roofline (algorithmic bytes per launch / mean launch time from HIP events on
@@ -181,6 +182,10 @@ def main():
     ap.add_argument("--apply", choices=["asgd", "sync"], default="asgd",
                     help="asgd: the workload's K-gradient asynchronous applies; sync: one "
                          "synchronous step (Eq. ssgd) per step over one gradient per learner")
+    ap.add_argument("--layout", choices=["server", "torch"], default="server",
+                    help="server: gradient pool and replicas in the server's own rows "
+                         "(ps_alloc_rows, distinct offsets within 2 MiB); torch: each "
+                         "buffer its own torch allocation, as plain user code would make them")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--calib-copy", action="store_true",
@@ -210,10 +215,24 @@ def main():
     n, K, R = cfg.n, cfg.depth, cfg.replicas
     stream = torch.cuda.current_stream()
 
-    pool = wl.make_pool(cfg, "cuda")
-    w0 = wl.make_w0(cfg, "cuda")
+    h = ps.ps_create(n, cfg.lr, cfg.momentum)
+    if not h:
+        raise RuntimeError(ps.ps_last_error())
+    gdt_t = torch.bfloat16 if cfg.grad_dtype == wl.BF16 else torch.float32
     rdt = torch.bfloat16 if cfg.pull_dtype == wl.BF16 else torch.float32
-    replicas = wl.Rows(R, n, rdt, "cuda")
+    if args.layout == "server":
+        rc, gp = ps.ps_alloc_rows(h, cfg.pool, cfg.grad_dtype)
+        rc2, rp = ps.ps_alloc_rows(h, R, cfg.pull_dtype)
+        if rc or rc2:
+            raise RuntimeError(ps.ps_last_error())
+        pool = ps.rows_as_tensors(gp, n, gdt_t)
+        replicas = ps.rows_as_tensors(rp, n, rdt)
+    else:
+        pool = [torch.empty(n, dtype=gdt_t, device="cuda") for _ in range(cfg.pool)]
+        replicas = [torch.empty(n, dtype=rdt, device="cuda") for _ in range(R)]
+    for j in range(cfg.pool):
+        pool[j].copy_(wl.make_grad(cfg, j, "cuda"))
+    w0 = wl.make_w0(cfg, "cuda")
     if args.apply == "sync":
         plan = [([(l, (s * cfg.learners + l) % cfg.pool) for l in range(cfg.learners)],
                  list(range(cfg.replicas))) for s in range(cfg.pool)]
@@ -221,7 +240,6 @@ def main():
         plan = batches(cfg, wl)
     torch.cuda.synchronize()
 
-    h = ps.ps_create(n, cfg.lr, cfg.momentum)
     assert ps.ps_set_queue_depth(h, K) == 0
     assert ps.ps_set_stream(h, stream.cuda_stream) == 0
     assert ps.ps_set_weights(h, w0.data_ptr()) == 0
@@ -290,7 +308,8 @@ def main():
     p_ms = sum(p_each) / len(p_each)
     gbps = step_bytes / elapsed / 1e9
     achieved = launch_bytes / (k_ms * 1e-3) / 1e9
-    label = f"{args.config}-{args.mode}" + ("-sync" if args.apply == "sync" else "")
+    label = (f"{args.config}-{args.mode}" + ("-sync" if args.apply == "sync" else "")
+             + ("-torch-buffers" if args.layout == "torch" else ""))
     traffic = recorded_traffic(label)
 
     if args.calib_copy:
@@ -302,14 +321,13 @@ def main():
         del a, b
 
     ts = ps.ps_timestamp(h)
-    ps.ps_destroy(h)
     ceiling = copy_ceiling(torch, ps, lib)
 
     cpu = None
     if not args.no_cpu_baseline:
-        del replicas
-        torch.cuda.empty_cache()
         cpu = cpu_baseline(cfg, pool, w0, round(sum(rs) / len(rs)), args.cpu_seconds)
+    del pool, replicas            # views of the server's rows (server layout)
+    ps.ps_destroy(h)
 
     kern = ("ps_apply_pull (apply + pull kernels)" if args.mode == "fused"
             else "sync_vec (synchronous step)" if args.apply == "sync"
@@ -335,6 +353,8 @@ def main():
                          f"{args.mode} apply+pull"),
             "params": n, "queue_depth": K, "replicas_per_apply": round(sum(rs) / len(rs), 2),
             "mode": args.mode, "apply": args.apply,
+            "layout": ("server rows (ps_alloc_rows)" if args.layout == "server"
+                       else "separate torch allocations"),
         },
         "gbps": round(gbps, 1),
         "pct_peak": round(100 * gbps / PEAK_GBPS, 2),

@@ -90,6 +90,7 @@ enum {
 #define PS_MAX_REPLICAS 64      /* replica buffers written by one pull call */
 #define PS_MAX_LEARNERS 65536   /* learner ids are 0 .. PS_MAX_LEARNERS-1   */
 #define PS_STALENESS_BINS 64    /* histogram bins; the last one is ">= 63"  */
+#define PS_MAX_ROWS 4096        /* buffers one ps_alloc_rows call may carve */
 
 typedef struct ps_stats {
     uint64_t timestamp;        /* applied gradients so far (Sec. 2.1)       */
@@ -225,6 +226,14 @@ int ps_set_queue_depth(ps_server *ps, int depth);
  * if any gradient is pending; slots_per_learner is ignored for FIFO. */
 int ps_set_queue_mode(ps_server *ps, int mode, int slots_per_learner);
 
+/* How the apply kernels sweep the weights: 2^fronts_log2 evenly spaced
+ * fronts (0..3), or -1 (default) to choose per apply from the buffers'
+ * offsets within 2 MiB -- four fronts when most of the gradient, w and v
+ * buffers share one offset (as separately allocated, 2 MiB-aligned buffers
+ * do), one front otherwise (ps_alloc_rows buffers). Results are identical
+ * either way; only the order in which the grid visits coordinates changes. */
+int ps_set_fronts(ps_server *ps, int fronts_log2);
+
 /* Enable (1) or disable (0) skipping of pulls that are already current. */
 int ps_set_pull_skip(ps_server *ps, int enabled);
 
@@ -274,6 +283,25 @@ int ps_drop_learner(ps_server *ps, int learner_id);
  * run. */
 int ps_save(ps_server *ps, const char *path);
 int ps_load(ps_server *ps, const char *path);
+
+/* Server-owned device buffers for gradients or replicas: the paper's queue
+ * slots, which the server holds and learners fill (Sec. 4.1). Allocates
+ * `count` (1..PS_MAX_ROWS) buffers of n_params values of `dtype` in one
+ * device allocation and writes their addresses to rows[0..count). Row i
+ * starts on a 2 MiB boundary plus (i + 2) * 4 KiB (mod 2 MiB); w and v sit
+ * at phases 0 and 4 KiB. An apply then streams its gradients, w and v from
+ * distinct offsets within 2 MiB, which the DRAM serves fastest. Buffers
+ * allocated one by one (2 MiB-aligned, all at one phase) are served slower;
+ * for them the apply kernels switch to a schedule that recovers part of the
+ * difference. Contents are uninitialised. The buffers belong to the server
+ * until ps_free_rows(ps, rows[0]) or ps_destroy. PS_ENOMEM if the device
+ * allocation fails. */
+int ps_alloc_rows(ps_server *ps, int count, int dtype, void **rows);
+
+/* Free the buffers of one ps_alloc_rows call, named by its first row, after
+ * waiting for the server's streams. PS_ESTATE (nothing freed) if a pending
+ * gradient lies in them; PS_EINVAL if first_row is not such a row. */
+int ps_free_rows(ps_server *ps, void *first_row);
 
 /* Block until all work enqueued by the server has completed. */
 int ps_sync(ps_server *ps);

@@ -285,23 +285,37 @@ __device__ __forceinline__ void sync_chunk(const ApplyArgs &a, uint64_t i) {
     if constexpr (MOM) st_f32<E, kNtWV>(a.v + i, v);
 }
 
+// Blocks are dispatched in index order. With F = 2^f fronts, block b works
+// at position b / F of front b % F, the fronts spaced evenly over the grid's
+// blocks: at any moment the resident blocks sit in F regions far apart
+// instead of one. A bijection on the first F * floor(nb / F) blocks, the
+// identity on the rest, so every chunk is still covered exactly once.
+__device__ __forceinline__ uint64_t front_block(unsigned b, unsigned nb, int f) {
+    const unsigned q = nb >> f;
+    if (f > 0 && b < (q << f)) return static_cast<uint64_t>(b & ((1u << f) - 1)) * q + (b >> f);
+    return b;
+}
+
 template <bool MOM, int GDT, int E>
 __global__ void __launch_bounds__(kBlock) sync_vec(const ApplyArgs a) {
     const uint64_t chunks = a.n / E;
     const uint64_t tid = static_cast<uint64_t>(blockIdx.x) * kBlock + threadIdx.x;
+    const uint64_t vtid = front_block(blockIdx.x, gridDim.x, a.fronts_log2) * kBlock + threadIdx.x;
     const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kBlock;
-    for (uint64_t c = tid; c < chunks; c += stride) sync_chunk<MOM, GDT, E>(a, c * E);
+    for (uint64_t c = vtid; c < chunks; c += stride) sync_chunk<MOM, GDT, E>(a, c * E);
     if (tid < a.n - chunks * E) sync_chunk<MOM, GDT, 1>(a, chunks * E + tid);
 }
 
-// Vector path: lane t of the grid owns E-coordinate chunks t, t + stride, ...
-// The n mod E trailing coordinates go to the first lanes of the grid.
+// Vector path: lane t of the grid owns E-coordinate chunks t', t' + stride,
+// ... where t' is t with its block renumbered by front_block. The n mod E
+// trailing coordinates go to the first lanes of the grid.
 template <bool MOM, int GDT, int PDT, int E>
 __global__ void __launch_bounds__(kBlock) apply_vec(const ApplyArgs a) {
     const uint64_t chunks = a.n / E;
     const uint64_t tid = static_cast<uint64_t>(blockIdx.x) * kBlock + threadIdx.x;
+    const uint64_t vtid = front_block(blockIdx.x, gridDim.x, a.fronts_log2) * kBlock + threadIdx.x;
     const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kBlock;
-    for (uint64_t c = tid; c < chunks; c += stride) apply_chunk<MOM, GDT, PDT, E>(a, c * E);
+    for (uint64_t c = vtid; c < chunks; c += stride) apply_chunk<MOM, GDT, PDT, E>(a, c * E);
     if (tid < a.n - chunks * E) apply_chunk<MOM, GDT, PDT, 1>(a, chunks * E + tid);
 }
 
@@ -532,6 +546,22 @@ unsigned one_block_per_cu_lds() {
         return 0;
     const unsigned want = static_cast<unsigned>(per_cu) / 2 + 1024;   // two blocks cannot fit
     return want <= static_cast<unsigned>(per_block) ? want : 0;
+}
+
+int fronts_log2_for(const void *const *ptrs, int count) {
+    // distinct 4 KiB phases within 2 MiB among the streams
+    constexpr uintptr_t kPhase = uintptr_t(2) << 20, kGrain = 4096;
+    uintptr_t seen[PS_MAX_QUEUE_DEPTH + 2];
+    int distinct = 0, streams = 0;
+    for (int i = 0; i < count && streams < PS_MAX_QUEUE_DEPTH + 2; ++i) {
+        if (ptrs[i] == nullptr) continue;
+        ++streams;
+        const uintptr_t ph = (reinterpret_cast<uintptr_t>(ptrs[i]) % kPhase) / kGrain;
+        bool dup = false;
+        for (int j = 0; j < distinct; ++j) dup = dup || seen[j] == ph;
+        if (!dup) seen[distinct++] = ph;
+    }
+    return (streams >= 8 && 2 * distinct < streams) ? 2 : 0;
 }
 
 hipError_t launch_zero(float *p, uint64_t n, hipStream_t s) {

@@ -228,6 +228,19 @@ void Protocol::commit_pulls(int n, const int *ids, void *const *dsts, int dtype,
     }
 }
 
+bool Protocol::references(const void *lo, const void *hi) const {
+    const auto in = [&](const PushDesc &d) {
+        const char *g = static_cast<const char *>(d.grad);
+        return g >= static_cast<const char *>(lo) && g < static_cast<const char *>(hi);
+    };
+    for (const PushDesc &d : fifo_)
+        if (in(d)) return true;
+    for (const auto &q : rr_)
+        for (const PushDesc &d : q)
+            if (in(d)) return true;
+    return false;
+}
+
 int Protocol::drop_learner(int learner) {
     if (int rc = check_learner(learner)) return rc;
     int dropped = 0;

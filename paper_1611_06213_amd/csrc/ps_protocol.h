@@ -109,6 +109,9 @@ struct Protocol {
     void commit_pulls(int n, const int *ids, void *const *dsts, int dtype,
                       const std::vector<int> &write, bool ordered);
 
+    // Whether a queued gradient starts in [lo, hi).
+    bool references(const void *lo, const void *hi) const;
+
     // Discard a dead learner's queued gradients (Sec. 4.3); returns the count.
     int drop_learner(int learner);
     int set_depth(int new_depth);

@@ -24,12 +24,37 @@ using gadei::Batch;
 using gadei::fail;
 using gadei::PushDesc;
 
+namespace {
+
+// One device allocation carved into staggered rows (ps_alloc_rows).
+struct RowSet {
+    void *base;          // what hipMalloc returned
+    char *first;         // row 0
+    char *end;           // one past the last row's data
+};
+
+// Row layout: starts on a 2 MiB boundary plus a phase; consecutive rows
+// step by the 2 MiB-rounded row size plus kRowStagger, so each row starts
+// at a different offset within 2 MiB. w sits at phase 0, v at one stagger,
+// rows from ps_alloc_rows start at two.
+constexpr size_t kRowAlign = size_t(2) << 20;
+constexpr size_t kRowStagger = 4096;
+
+size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+char *align_up(void *p, size_t a) {
+    return reinterpret_cast<char *>(round_up(reinterpret_cast<uintptr_t>(p), a));
+}
+
+}  // namespace
+
 struct ps_server {
     size_t n = 0;
     float lr = 0.0f;
     float m = 0.0f;
+    void *wv_base = nullptr;   // one allocation holding w and v
     float *w = nullptr;
     float *v = nullptr;
+    std::vector<RowSet> row_sets;
     int device = 0;
     hipStream_t stream = nullptr;
     hipStream_t pull_stream = nullptr;   // lock-free pulls when pull_lock_free
@@ -94,6 +119,18 @@ int drain_pulls(ps_server *ps) {
     return PS_OK;
 }
 
+// Fronts for an apply over a.g[0..k), w and v: the server's setting, or
+// chosen from the buffers' offsets (fronts_log2_for).
+int fronts_for(const ps_server *ps, const gadei::ApplyArgs &a) {
+    if (ps->geo.fronts_log2 >= 0) return ps->geo.fronts_log2;
+    const void *p[PS_MAX_QUEUE_DEPTH + 2];
+    int c = 0;
+    for (int j = 0; j < a.k; ++j) p[c++] = a.g[j];
+    p[c++] = a.w;
+    p[c++] = a.v;   // null without momentum: not a stream
+    return gadei::fronts_log2_for(p, c);
+}
+
 // Launch a batch as runs of equal gradient dtype, in order. The last run
 // also writes the replicas listed in `write` when pull_dtype >= 0.
 int launch_batch(ps_server *ps, const std::vector<PushDesc> &items, int pull_dtype,
@@ -119,6 +156,7 @@ int launch_batch(ps_server *ps, const std::vector<PushDesc> &items, int pull_dty
         }
         a.k = static_cast<int>(end - start);
         a.r = 0;
+        a.fronts_log2 = fronts_for(ps, a);
         int pdt = -1;
         if (end == q && pull_dtype >= 0 && !write.empty()) {
             pdt = pull_dtype;
@@ -231,16 +269,22 @@ ps_server *ps_create(size_t n_params, float lr, float momentum) {
     ps->n = n_params;
     ps->lr = lr;
     ps->m = momentum;
+    // w and v in one allocation, v one stagger after w's 2 MiB-rounded end
+    const size_t bytes = n_params * sizeof(float);
+    const size_t v_off = round_up(bytes, kRowAlign) + kRowStagger;
     hipError_t e = hipGetDevice(&ps->device);
-    if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void **>(&ps->w), n_params * sizeof(float));
-    if (e == hipSuccess && momentum != 0.0f)
-        e = hipMalloc(reinterpret_cast<void **>(&ps->v), n_params * sizeof(float));
-    if (e == hipSuccess) e = hipMemset(ps->w, 0, n_params * sizeof(float));
-    if (e == hipSuccess && ps->v) e = hipMemset(ps->v, 0, n_params * sizeof(float));
+    if (e == hipSuccess)
+        e = hipMalloc(&ps->wv_base, (momentum != 0.0f ? v_off + bytes : bytes) + kRowAlign);
+    if (e == hipSuccess) {
+        char *w = align_up(ps->wv_base, kRowAlign);
+        ps->w = reinterpret_cast<float *>(w);
+        if (momentum != 0.0f) ps->v = reinterpret_cast<float *>(w + v_off);
+        e = hipMemset(ps->w, 0, bytes);
+    }
+    if (e == hipSuccess && ps->v) e = hipMemset(ps->v, 0, bytes);
     if (e != hipSuccess) {
         fail(e == hipErrorOutOfMemory ? PS_ENOMEM : PS_EHIP, "ps_create: %s", hipGetErrorString(e));
-        if (ps->w) (void)hipFree(ps->w);
-        if (ps->v) (void)hipFree(ps->v);
+        if (ps->wv_base) (void)hipFree(ps->wv_base);
         delete ps;
         return nullptr;
     }
@@ -253,10 +297,53 @@ void ps_destroy(ps_server *ps) {
     if (use_device(ps) == PS_OK) {
         (void)hipStreamSynchronize(ps->stream);
         if (ps->pull_lock_free) (void)hipStreamSynchronize(ps->pull_stream);
-        if (ps->w) (void)hipFree(ps->w);
-        if (ps->v) (void)hipFree(ps->v);
+        for (const RowSet &r : ps->row_sets) (void)hipFree(r.base);
+        (void)hipFree(ps->wv_base);
     }
     delete ps;
+}
+
+int ps_alloc_rows(ps_server *ps, int count, int dtype, void **rows) {
+    if (int rc = check(ps)) return rc;
+    if (count < 1 || count > PS_MAX_ROWS)
+        return fail(PS_EINVAL, "row count %d outside [1, %d]", count, PS_MAX_ROWS);
+    if (dtype != PS_F32 && dtype != PS_BF16) return fail(PS_EINVAL, "bad row dtype %d", dtype);
+    if (rows == nullptr) return fail(PS_EINVAL, "null rows output");
+    if (int rc = use_device(ps)) return rc;
+    const size_t row_bytes = ps->n * (dtype == PS_BF16 ? 2 : 4);
+    const size_t stride = round_up(row_bytes, kRowAlign) + kRowStagger;
+    const size_t head = 2 * kRowStagger;
+    const size_t span = head + (static_cast<size_t>(count) - 1) * stride + row_bytes;
+    void *base = nullptr;
+    hipError_t e = hipMalloc(&base, span + kRowAlign);
+    if (e != hipSuccess)
+        return fail(e == hipErrorOutOfMemory ? PS_ENOMEM : PS_EHIP, "ps_alloc_rows: %s",
+                    hipGetErrorString(e));
+    char *first = align_up(base, kRowAlign) + head;
+    try {
+        ps->row_sets.push_back(RowSet{base, first, first - head + span});
+    } catch (...) {
+        (void)hipFree(base);
+        return fail(PS_ENOMEM, "host allocation failed");
+    }
+    for (int i = 0; i < count; ++i) rows[i] = first + static_cast<size_t>(i) * stride;
+    return PS_OK;
+}
+
+int ps_free_rows(ps_server *ps, void *first_row) {
+    if (int rc = check(ps)) return rc;
+    auto it = std::find_if(ps->row_sets.begin(), ps->row_sets.end(),
+                           [&](const RowSet &r) { return r.first == first_row; });
+    if (it == ps->row_sets.end()) return fail(PS_EINVAL, "not the first row of a row set");
+    if (ps->proto.references(it->first, it->end))
+        return fail(PS_ESTATE, "a pending gradient lies in these rows");
+    if (int rc = use_device(ps)) return rc;
+    if (int rc = drain_pulls(ps)) return rc;
+    hipError_t e = hipStreamSynchronize(ps->stream);
+    if (e == hipSuccess) e = hipFree(it->base);
+    if (e != hipSuccess) return fail_hip(e, "ps_free_rows");
+    ps->row_sets.erase(it);
+    return PS_OK;
 }
 
 int ps_push_async(ps_server *ps, int learner_id, const void *grad, int dtype, void *ready_event) {
@@ -311,6 +398,7 @@ int ps_apply_sync(ps_server *ps) {
         a.g[j] = b.items[j].grad;
         level = std::min(level, level_of(a.g[j], gdt));
     }
+    a.fronts_log2 = fronts_for(ps, a);
     hipError_t e = gadei::launch_sync(a, gdt, level, ps->geo, ps->stream);
     if (e != hipSuccess) return fail_hip(e, "synchronous step launch");
     ps->proto.commit_sync(b);
@@ -488,6 +576,14 @@ int ps_set_pull_fusion(ps_server *ps, int max_replicas) {
     if (max_replicas < 0 || max_replicas > PS_MAX_REPLICAS)
         return fail(PS_EINVAL, "fusion limit %d outside [0, %d]", max_replicas, PS_MAX_REPLICAS);
     ps->fuse_max_r = max_replicas;
+    return PS_OK;
+}
+
+int ps_set_fronts(ps_server *ps, int fronts_log2) {
+    if (int rc = check(ps)) return rc;
+    if (fronts_log2 < -1 || fronts_log2 > 3)
+        return fail(PS_EINVAL, "fronts_log2 %d outside [-1, 3]", fronts_log2);
+    ps->geo.fronts_log2 = fronts_log2;
     return PS_OK;
 }
 

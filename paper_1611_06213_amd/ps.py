@@ -29,6 +29,7 @@ PS_MAX_QUEUE_DEPTH = 64
 PS_MAX_REPLICAS = 64
 PS_MAX_LEARNERS = 65536
 PS_STALENESS_BINS = 64
+PS_MAX_ROWS = 4096
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libgadeips.so")
@@ -66,6 +67,7 @@ _SIGS = {
     "ps_set_stream": (ctypes.c_int, [_VP, _VP]),
     "ps_set_queue_depth": (ctypes.c_int, [_VP, ctypes.c_int]),
     "ps_set_pull_skip": (ctypes.c_int, [_VP, ctypes.c_int]),
+    "ps_set_fronts": (ctypes.c_int, [_VP, ctypes.c_int]),
     "ps_set_queue_mode": (ctypes.c_int, [_VP, ctypes.c_int, ctypes.c_int]),
     "ps_last_applied": (ctypes.c_int, [_VP, ctypes.POINTER(ctypes.c_int), ctypes.c_int]),
     "ps_set_pull_fusion": (ctypes.c_int, [_VP, ctypes.c_int]),
@@ -81,6 +83,8 @@ _SIGS = {
     "ps_load": (ctypes.c_int, [_VP, ctypes.c_char_p]),
     "ps_sync": (ctypes.c_int, [_VP]),
     "ps_get_stats": (ctypes.c_int, [_VP, ctypes.POINTER(ps_stats)]),
+    "ps_alloc_rows": (ctypes.c_int, [_VP, ctypes.c_int, ctypes.c_int, ctypes.POINTER(_VP)]),
+    "ps_free_rows": (ctypes.c_int, [_VP, _VP]),
     "ps_last_error": (ctypes.c_char_p, []),
 }
 
@@ -264,6 +268,21 @@ def ps_sync(h: int) -> int:
     return load_library().ps_sync(h)
 
 
+def ps_set_fronts(h: int, fronts_log2: int) -> int:
+    return load_library().ps_set_fronts(h, fronts_log2)
+
+
+def ps_alloc_rows(h: int, count: int, dtype: int):
+    """(status, [row addresses])."""
+    out = (_VP * max(1, count))()
+    rc = load_library().ps_alloc_rows(h, count, dtype, out)
+    return rc, ([int(out[i]) for i in range(count)] if rc == PS_OK else [])
+
+
+def ps_free_rows(h: int, first_row: int) -> int:
+    return load_library().ps_free_rows(h, first_row)
+
+
 def ps_get_stats(h: int):
     s = ps_stats()
     rc = load_library().ps_get_stats(h, ctypes.byref(s))
@@ -326,6 +345,9 @@ class ParameterServer:
 
     def set_weights(self, w0) -> None:
         self._check(ps_set_weights(self.h, self._tensor(w0, "set_weights")), "set_weights")
+
+    def set_fronts(self, fronts_log2: int) -> None:
+        self._check(ps_set_fronts(self.h, fronts_log2), "set_fronts")
 
     def set_pull_skip(self, enabled: bool) -> None:
         self._check(ps_set_pull_skip(self.h, enabled), "set_pull_skip")
@@ -430,6 +452,20 @@ class ParameterServer:
             self._check(s, "get_stats")
         return s
 
+    def alloc_rows(self, count: int, dtype=None):
+        """`count` server-owned device buffers of n elements (ps_alloc_rows)
+        as torch tensors viewing that memory. They stay valid until
+        free_rows(rows) or close(); the server does not keep them alive."""
+        import torch
+        dtype = torch.float32 if dtype is None else dtype
+        code = PS_BF16 if dtype == torch.bfloat16 else PS_F32
+        rc, ptrs = ps_alloc_rows(self.h, count, code)
+        self._check(rc, "alloc_rows")
+        return rows_as_tensors(ptrs, self.n, dtype)
+
+    def free_rows(self, rows) -> None:
+        self._check(ps_free_rows(self.h, rows[0].data_ptr()), "free_rows")
+
     def weights_copy(self):
         """A new device tensor holding w (waits for the server's stream)."""
         return self._copy(ps_weights(self.h))
@@ -443,7 +479,7 @@ class ParameterServer:
         self.sync()
         out = torch.empty(self.n, dtype=torch.float32, device="cuda")
         stream = torch.cuda.current_stream().cuda_stream
-        rc = _hip().hipMemcpyAsync(ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ptr),
+        rc = _hip()(ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ptr),
                                    ctypes.c_size_t(4 * self.n), 3,   # device to device
                                    ctypes.c_void_p(stream))
         if rc != 0:
@@ -454,11 +490,36 @@ class ParameterServer:
 _hip_rt = None
 
 
+def rows_as_tensors(ptrs: Sequence[int], n: int, dtype):
+    """Torch tensors of n elements viewing device memory at `ptrs` (rows from
+    ps_alloc_rows); no copy, no ownership."""
+    import torch
+    bf16 = dtype == torch.bfloat16
+    out = []
+    for p in ptrs:
+        iface = {"shape": (n,), "typestr": "<i2" if bf16 else "<f4", "data": (p, False),
+                 "version": 2}
+        t = torch.as_tensor(_DeviceArray(iface), device="cuda")
+        out.append(t.view(torch.bfloat16) if bf16 else t)
+    return out
+
+
+class _DeviceArray:
+    """Device memory described by the CUDA array interface (torch imports it
+    without copying)."""
+
+    def __init__(self, iface):
+        self.__cuda_array_interface__ = iface
+
+
 def _hip():
-    """The HIP runtime the library links (for the plain copy above)."""
+    """hipMemcpyAsync of the HIP runtime the library itself is bound to
+    (looked up through the library's handle, which searches its
+    dependencies), for the plain copy above."""
     global _hip_rt
     if _hip_rt is None:
-        _hip_rt = ctypes.CDLL("libamdhip64.so")
-        _hip_rt.hipMemcpyAsync.restype = ctypes.c_int
-        _hip_rt.hipMemcpyAsync.argtypes = [_VP, _VP, ctypes.c_size_t, ctypes.c_int, _VP]
+        f = load_library().hipMemcpyAsync
+        f.restype = ctypes.c_int
+        f.argtypes = [_VP, _VP, ctypes.c_size_t, ctypes.c_int, _VP]
+        _hip_rt = f
     return _hip_rt

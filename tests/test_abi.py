@@ -42,7 +42,8 @@ def test_header_constants_match_binding():
                  "PS_EIO", "PS_F32", "PS_BF16", "PS_QUEUE_FIFO", "PS_QUEUE_ROUND_ROBIN"):
         m = re.search(rf"\b{name}\s*=\s*(-?\d+)", text)
         assert m and int(m.group(1)) == getattr(ps, name), name
-    for name in ("PS_MAX_QUEUE_DEPTH", "PS_MAX_REPLICAS", "PS_MAX_LEARNERS", "PS_STALENESS_BINS"):
+    for name in ("PS_MAX_QUEUE_DEPTH", "PS_MAX_REPLICAS", "PS_MAX_LEARNERS", "PS_STALENESS_BINS",
+                 "PS_MAX_ROWS"):
         m = re.search(rf"#define {name} (\d+)", text)
         assert m and int(m.group(1)) == getattr(ps, name), name
     assert ctypes.sizeof(ps.ps_stats) == 8 * (10 + ps.PS_STALENESS_BINS)
@@ -62,6 +63,9 @@ def test_validation_without_device(lib):
     assert lib.ps_pending(None) == ps.PS_EINVAL
     assert lib.ps_save(None, b"/tmp/x") == ps.PS_EINVAL and lib.ps_load(None, b"/tmp/x") == ps.PS_EINVAL
     assert lib.ps_drop_learner(None, 0) == ps.PS_EINVAL
+    assert ps.ps_alloc_rows(None, 2, ps.PS_F32)[0] == ps.PS_EINVAL
+    assert lib.ps_free_rows(None, None) == ps.PS_EINVAL
+    assert lib.ps_set_fronts(None, 0) == ps.PS_EINVAL
     assert lib.ps_timestamp(None) == 0 and lib.ps_num_params(None) == 0
     assert not lib.ps_weights(None)
     lib.ps_destroy(None)   # no-op

@@ -967,3 +967,118 @@ def test_fma_flavour_whole_schedule_drift_bounded(torch, fma_library, name):
     assert g["staleness"] == o["staleness"] and g["ts"] == o["ts"]
     del pool
     free(torch)
+
+
+# ---------------------------------------------------------------- layout
+
+def _oracle_apply(torch, w0, grads, lr, m, k, pulls_bf16=False):
+    o = orc.OracleServer(w0.cpu().numpy(), lr, m, depth=k)
+    for j, g in enumerate(grads):
+        h = g.cpu()
+        h = h.view(torch.int16).numpy().view(np.uint16) if g.dtype == torch.bfloat16 else h.numpy()
+        assert o.push(j % 7, h) == orc.OK
+    o.apply_pending()
+    return o
+
+
+def test_alloc_rows_layout_and_parity(torch):
+    """Server-owned rows: distinct 4 KiB phases within 2 MiB (w at 0, v at
+    4 KiB, row i at (i + 2) * 4 KiB), no overlap, usable as fp32 and bf16
+    gradients and replicas with results bitwise equal to the oracle; freeing
+    refuses rows a pending gradient lies in."""
+    n, k, lr, m = 3 * (1 << 20) + 5, 32, 0.01, 0.9
+    say(f"[case] alloc_rows n={n} K={k}")
+    two_mib = 2 << 20
+    srv = ps.ParameterServer(n, lr, m, queue_depth=k)
+    assert ps.ps_weights(srv.h) % two_mib == 0 and ps.ps_velocity(srv.h) % two_mib == 4096
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(31)
+    w0 = (torch.rand(n, generator=gen, device="cuda") - 0.5) * 0.1
+    srv.set_weights(w0)
+    rows = srv.alloc_rows(k + 3)
+    addrs = [r.data_ptr() for r in rows]
+    assert [a % two_mib for a in addrs] == [((i + 2) * 4096) % two_mib for i in range(k + 3)]
+    assert all(b - a >= 4 * n for a, b in zip(addrs, addrs[1:]))
+    for r in rows[:k]:
+        r.copy_(torch.randn(n, generator=gen, device="cuda") * 1e-3)
+    for j in range(k):
+        assert srv.push(j % 7, rows[j])
+    with pytest.raises(ps.PSError) as e:
+        srv.free_rows(rows)                       # pending gradients live there
+    assert e.value.code == ps.PS_ESTATE
+    reps16 = srv.alloc_rows(2, torch.bfloat16)
+    assert [t.data_ptr() % two_mib for t in reps16] == [8192, 12288]
+    srv.apply_pull([0, 1, 2], rows[k:k + 3])
+    srv.pull_many([3, 4], reps16)
+    torch.cuda.synchronize()
+    o = _oracle_apply(torch, w0, rows[:k], lr, m, k)
+    wbits = parity.np_bits(srv.weights_copy())
+    assert parity.bitwise(wbits, o.w.view(np.uint32))
+    for r in rows[k:k + 3]:
+        assert parity.bitwise(parity.np_bits(r), o.w.view(np.uint32))
+    want16 = orc.f32_to_bf16(o.w)
+    for r in reps16:
+        assert np.array_equal(r.cpu().view(torch.int16).numpy().view(np.uint16), want16)
+    # bf16 gradients in server rows
+    g16 = srv.alloc_rows(4, torch.bfloat16)
+    for r in g16:
+        r.copy_((torch.randn(n, generator=gen, device="cuda") * 1e-3).to(torch.bfloat16))
+    for j, r in enumerate(g16):
+        assert srv.push(j, r)
+    srv.apply_pending()
+    for j, r in enumerate(g16):
+        h = r.cpu().view(torch.int16).numpy().view(np.uint16)
+        o.push(j, h)
+    o.apply_pending()
+    assert parity.bitwise(parity.np_bits(srv.weights_copy()), o.w.view(np.uint32))
+    srv.free_rows(rows)
+    with pytest.raises(ps.PSError):
+        srv.free_rows(rows)                       # already freed
+    assert ps.ps_free_rows(srv.h, g16[1].data_ptr()) == ps.PS_EINVAL   # not a first row
+    srv.close()                                   # frees the remaining row sets
+    free(torch)
+
+
+@pytest.mark.parametrize("layout", ["separate", "server_rows"])
+def test_fronts_give_identical_bits(torch, layout):
+    """Every front count (and the automatic choice) folds the same
+    gradients into the same bits, for separately allocated buffers (one
+    phase) and for server rows (distinct phases); the synchronous step
+    too."""
+    n, k, lr, m = 5 * (1 << 20) + 3, 32, 0.01, 0.9
+    say(f"[case] fronts layout={layout} n={n}")
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(37)
+    w0 = (torch.rand(n, generator=gen, device="cuda") - 0.5) * 0.1
+    holder = ps.ParameterServer(n, lr, m)
+    if layout == "separate":
+        grads = [torch.empty(n, device="cuda") for _ in range(k)]
+    else:
+        grads = holder.alloc_rows(k)
+    for g in grads:
+        g.copy_(torch.randn(n, generator=gen, device="cuda") * 1e-3)
+    o = _oracle_apply(torch, w0, grads, lr, m, k)
+    want = o.w.view(np.uint32).copy()
+    so = orc.OracleServer(w0.cpu().numpy(), lr, m, depth=16)
+    for j in range(16):
+        so.push(j, grads[j].cpu().numpy())
+    so.apply_sync()
+    want_sync = so.w.view(np.uint32).copy()
+    for f in (-1, 0, 1, 2, 3):
+        srv = ps.ParameterServer(n, lr, m, queue_depth=k)
+        srv.set_fronts(f)
+        srv.set_weights(w0)
+        for j, g in enumerate(grads):
+            assert srv.push(j % 7, g)
+        srv.apply_pending()
+        assert parity.bitwise(parity.np_bits(srv.weights_copy()), want), f
+        srv.set_weights(w0)
+        for j in range(16):
+            assert srv.push(j, grads[j])
+        srv.apply_sync()
+        assert parity.bitwise(parity.np_bits(srv.weights_copy()), want_sync), f
+        srv.close()
+    with pytest.raises(ps.PSError):
+        holder.set_fronts(4)
+    holder.close()
+    free(torch)
