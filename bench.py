@@ -186,6 +186,9 @@ def main():
                     help="server: gradient pool and replicas in the server's own rows "
                          "(ps_alloc_rows, distinct offsets within 2 MiB); torch: each "
                          "buffer its own torch allocation, as plain user code would make them")
+    ap.add_argument("--queue", choices=["fifo", "rr"], default="fifo",
+                    help="fifo: one queue of K slots; rr: a queue per learner served "
+                         "round-robin, one gradient per visit (Sec. 4.1), K slots each")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--calib-copy", action="store_true",
@@ -241,6 +244,8 @@ def main():
     torch.cuda.synchronize()
 
     assert ps.ps_set_queue_depth(h, K) == 0
+    if args.queue == "rr":
+        assert ps.ps_set_queue_mode(h, ps.PS_QUEUE_ROUND_ROBIN, K) == 0
     assert ps.ps_set_stream(h, stream.cuda_stream) == 0
     assert ps.ps_set_weights(h, w0.data_ptr()) == 0
 
@@ -309,7 +314,8 @@ def main():
     gbps = step_bytes / elapsed / 1e9
     achieved = launch_bytes / (k_ms * 1e-3) / 1e9
     label = (f"{args.config}-{args.mode}" + ("-sync" if args.apply == "sync" else "")
-             + ("-torch-buffers" if args.layout == "torch" else ""))
+             + ("-torch-buffers" if args.layout == "torch" else "")
+             + ("-rr" if args.queue == "rr" else ""))
     traffic = recorded_traffic(label)
 
     if args.calib_copy:
@@ -352,7 +358,7 @@ def main():
                          f"lr={cfg.lr}, momentum={cfg.momentum}, {cfg.learners} learners, "
                          f"{args.mode} apply+pull"),
             "params": n, "queue_depth": K, "replicas_per_apply": round(sum(rs) / len(rs), 2),
-            "mode": args.mode, "apply": args.apply,
+            "mode": args.mode, "apply": args.apply, "queue": args.queue,
             "layout": ("server rows (ps_alloc_rows)" if args.layout == "server"
                        else "separate torch allocations"),
         },
