@@ -312,15 +312,17 @@ def make_grad(cfg: Config, buf: int, device="cpu"):
 
 
 ROW_ALIGN = 2 << 20     # bytes: each buffer starts on a 2 MiB boundary ...
-ROW_STAGGER = 4096      # ... plus 4 KiB per row, so rows do not share a phase
+ROW_STAGGER = 4096      # ... plus 4 KiB per row, so rows do not share a DRAM phase
 
 
 class Rows:
-    """`count` device buffers of n elements, carved from one allocation on
-    aligned, staggered row starts (row r at r * stride). Buffers laid out
-    back to back at n*4 bytes apart would start at arbitrary 32-byte offsets
-    for most n, which costs streaming kernels a tenth of their bandwidth;
-    separately allocated buffers are aligned like this anyway."""
+    """`count` buffers of n elements, carved from one allocation on aligned,
+    staggered row starts (row r at r * stride): each starts on a 2 MiB
+    boundary plus r * 4 KiB, the layout of the server's own rows, here
+    without a server (tests, oracle-side copies). Buffers laid out back to
+    back n*4 bytes apart would start at arbitrary 32-byte offsets for most n,
+    and separately allocated ones all at one offset within 2 MiB; streaming
+    kernels lose bandwidth on both."""
 
     def __init__(self, count: int, n: int, dtype, device="cpu", align: int = ROW_ALIGN,
                  stagger: int = ROW_STAGGER):
