@@ -125,14 +125,49 @@ def cpu_baseline(cfg, pool, w0, pulls_per_step: int, seconds: float, distinct: i
         t1 = time.perf_counter()
         if t1 - t0 >= seconds:
             break
+    oracle_rate = steps * cfg.depth / (t1 - t0)
+    oracle_sample = (f"{steps} whole steps ({cfg.depth} pushes + apply + {pulls_per_step} pulls) "
+                     f"over the full {cfg.n:,}-parameter vector, 1 thread, pushes cycling over "
+                     f"{distinct} host copies of pool buffers; {t1 - t0:.1f} s of CPU work on "
+                     f"{cpu_model()} ({os.cpu_count()} logical CPUs visible)")
+    paper = paper_style_ps(cfg, host_g, s.w, pulls_per_step, seconds / 2)
     del host_g
     return {
-        "value": round(steps * cfg.depth / (t1 - t0), 4), "unit": "pushes/s", "cores": 1,
-        "kind": "oracle",
-        "sample": (f"{steps} whole steps ({cfg.depth} pushes + apply + {pulls_per_step} pulls) "
-                   f"over the full {cfg.n:,}-parameter vector, 1 thread, pushes cycling over "
-                   f"{distinct} host copies of pool buffers; {t1 - t0:.1f} s of CPU work on "
-                   f"{cpu_model()} ({os.cpu_count()} logical CPUs visible)"),
+        "value": round(oracle_rate, 4), "unit": "pushes/s", "cores": 1, "kind": "oracle",
+        "sample": oracle_sample,
+        "paper_style_ps": paper,
+    }
+
+
+def paper_style_ps(cfg, host_g, w_start, pulls_per_step: int, seconds: float):
+    """The paper's own CPU server design (oracle/cpu_ps.c: one OpenMP pass
+    over the weights per gradient, loop unrolled 8x, Sec. 4.1 and 4.4) on all
+    the host cores this process may use, over the same whole steps: context
+    for what that design does on this host. Bitwise equal to the oracle."""
+    import numpy as np
+    from oracle import cpu_ps
+
+    threads = len(os.sched_getaffinity(0))
+    w = np.array(w_start, dtype=np.float32, copy=True)
+    v = np.zeros_like(w) if cfg.momentum != 0 else None
+    dst = [np.empty_like(w) for _ in range(2)]
+    j = steps = 0
+    t0 = time.perf_counter()
+    while True:
+        for _ in range(cfg.depth):
+            cpu_ps.step(w, v, host_g[j % len(host_g)], cfg.lr, cfg.momentum, threads)
+            j += 1
+        for r in range(pulls_per_step):
+            cpu_ps.pull(dst[r % 2], w, threads)
+        steps += 1
+        t1 = time.perf_counter()
+        if t1 - t0 >= seconds:
+            break
+    return {
+        "value": round(steps * cfg.depth / (t1 - t0), 4), "unit": "pushes/s", "cores": threads,
+        "kind": "paper-style CPU parameter server (OpenMP, one pass per gradient)",
+        "sample": (f"{steps} whole steps over the full vector, {threads} threads, "
+                   f"{t1 - t0:.1f} s"),
     }
 
 
