@@ -24,7 +24,7 @@ FMA_FLAGS = ["-ffp-contract=fast", "-DPS_FP_CONTRACT=1"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 SOURCES = [os.path.join(CSRC, "ps_server.cpp"), os.path.join(CSRC, "ps_protocol.cpp"),
-           os.path.join(CSRC, "ps_kernels.hip")]
+           os.path.join(CSRC, "ps_layout.cpp"), os.path.join(CSRC, "ps_kernels.hip")]
 
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

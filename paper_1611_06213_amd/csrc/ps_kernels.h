@@ -39,7 +39,7 @@ struct PullArgs {
 // creation so that one block fits per compute unit.
 struct Geometry {
     int max_blocks = 0;
-    int fronts_log2 = -1;   // -1: chosen per apply by fronts_log2_for
+    int fronts_log2 = -1;   // -1: chosen per apply (fronts_log2_for, ps_layout.h)
     unsigned occupancy_cap_lds = 0;
     int occupancy_cap_min_k = 16;
 };
@@ -48,13 +48,6 @@ struct Geometry {
 // current device, or 0 if the device does not allow such a reservation.
 unsigned one_block_per_cu_lds();
 
-// How many fronts (log2) an apply over these streams should sweep: streams
-// that all start at the same offset within 2 MiB (separately allocated,
-// 2 MiB-aligned buffers) meet the same DRAM banks at the same time when the
-// whole grid sweeps one front; four fronts spread apart measured 15-20%
-// faster for them, and slower for streams that already start at distinct
-// offsets. `ptrs` are the gradient, weight and velocity buffers.
-int fronts_log2_for(const void *const *ptrs, int count);
 
 // grad_dtype: PS_F32 | PS_BF16. pull_dtype: -1 (no replicas), PS_F32, PS_BF16.
 // level: 2 = every buffer 16-byte aligned; 1 = fp32 buffers 16-byte and bf16

@@ -548,22 +548,6 @@ unsigned one_block_per_cu_lds() {
     return want <= static_cast<unsigned>(per_block) ? want : 0;
 }
 
-int fronts_log2_for(const void *const *ptrs, int count) {
-    // distinct 4 KiB phases within 2 MiB among the streams
-    constexpr uintptr_t kPhase = uintptr_t(2) << 20, kGrain = 4096;
-    uintptr_t seen[PS_MAX_QUEUE_DEPTH + 2];
-    int distinct = 0, streams = 0;
-    for (int i = 0; i < count && streams < PS_MAX_QUEUE_DEPTH + 2; ++i) {
-        if (ptrs[i] == nullptr) continue;
-        ++streams;
-        const uintptr_t ph = (reinterpret_cast<uintptr_t>(ptrs[i]) % kPhase) / kGrain;
-        bool dup = false;
-        for (int j = 0; j < distinct; ++j) dup = dup || seen[j] == ph;
-        if (!dup) seen[distinct++] = ph;
-    }
-    return (streams >= 8 && 2 * distinct < streams) ? 2 : 0;
-}
-
 hipError_t launch_zero(float *p, uint64_t n, hipStream_t s) {
     Geometry geo;
     geo.max_blocks = 4096;

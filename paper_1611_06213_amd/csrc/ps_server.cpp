@@ -18,10 +18,13 @@
 
 #include "ps.h"
 #include "ps_kernels.h"
+#include "ps_layout.h"
 #include "ps_protocol.h"
 
+using gadei::align_up;
 using gadei::Batch;
 using gadei::fail;
+using gadei::kRowAlign;
 using gadei::PushDesc;
 
 namespace {
@@ -32,18 +35,6 @@ struct RowSet {
     char *first;         // row 0
     char *end;           // one past the last row's data
 };
-
-// Row layout: starts on a 2 MiB boundary plus a phase; consecutive rows
-// step by the 2 MiB-rounded row size plus kRowStagger, so each row starts
-// at a different offset within 2 MiB. w sits at phase 0, v at one stagger,
-// rows from ps_alloc_rows start at two.
-constexpr size_t kRowAlign = size_t(2) << 20;
-constexpr size_t kRowStagger = 4096;
-
-size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
-char *align_up(void *p, size_t a) {
-    return reinterpret_cast<char *>(round_up(reinterpret_cast<uintptr_t>(p), a));
-}
 
 }  // namespace
 
@@ -271,7 +262,7 @@ ps_server *ps_create(size_t n_params, float lr, float momentum) {
     ps->m = momentum;
     // w and v in one allocation, v one stagger after w's 2 MiB-rounded end
     const size_t bytes = n_params * sizeof(float);
-    const size_t v_off = round_up(bytes, kRowAlign) + kRowStagger;
+    const size_t v_off = gadei::velocity_offset(bytes);
     hipError_t e = hipGetDevice(&ps->device);
     if (e == hipSuccess)
         e = hipMalloc(&ps->wv_base, (momentum != 0.0f ? v_off + bytes : bytes) + kRowAlign);
@@ -310,23 +301,20 @@ int ps_alloc_rows(ps_server *ps, int count, int dtype, void **rows) {
     if (dtype != PS_F32 && dtype != PS_BF16) return fail(PS_EINVAL, "bad row dtype %d", dtype);
     if (rows == nullptr) return fail(PS_EINVAL, "null rows output");
     if (int rc = use_device(ps)) return rc;
-    const size_t row_bytes = ps->n * (dtype == PS_BF16 ? 2 : 4);
-    const size_t stride = round_up(row_bytes, kRowAlign) + kRowStagger;
-    const size_t head = 2 * kRowStagger;
-    const size_t span = head + (static_cast<size_t>(count) - 1) * stride + row_bytes;
+    const gadei::RowLayout lay = gadei::row_layout(ps->n * (dtype == PS_BF16 ? 2 : 4), count);
     void *base = nullptr;
-    hipError_t e = hipMalloc(&base, span + kRowAlign);
+    hipError_t e = hipMalloc(&base, lay.span + kRowAlign);
     if (e != hipSuccess)
         return fail(e == hipErrorOutOfMemory ? PS_ENOMEM : PS_EHIP, "ps_alloc_rows: %s",
                     hipGetErrorString(e));
-    char *first = align_up(base, kRowAlign) + head;
+    char *first = align_up(base, kRowAlign) + lay.head;
     try {
-        ps->row_sets.push_back(RowSet{base, first, first - head + span});
+        ps->row_sets.push_back(RowSet{base, first, first - lay.head + lay.span});
     } catch (...) {
         (void)hipFree(base);
         return fail(PS_ENOMEM, "host allocation failed");
     }
-    for (int i = 0; i < count; ++i) rows[i] = first + static_cast<size_t>(i) * stride;
+    for (int i = 0; i < count; ++i) rows[i] = first + static_cast<size_t>(i) * lay.stride;
     return PS_OK;
 }
 

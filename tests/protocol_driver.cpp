@@ -11,12 +11,15 @@
 //   pull DT L1 D1 ...     ordered pulls of learners Li into buffers Di (ps_pull_many)
 //   applypull DT L1 D1 .. ps_apply_pull
 //   drop L | depth K | mode M S | skip 0|1 | state
+//   fronts A1 A2 ...      front choice for streams at addresses Ai (0 = none)
+//   rows B C              row layout of C rows of B bytes: head stride span
 #include <cstdio>
 #include <iostream>
 #include <sstream>
 #include <string>
 #include <vector>
 
+#include "ps_layout.h"
 #include "ps_protocol.h"
 
 namespace {
@@ -133,6 +136,18 @@ int main() {
             in >> on;
             p.pull_skip = on != 0;
             std::printf("skip");
+        } else if (cmd == "fronts") {
+            std::vector<const void *> ptrs;
+            unsigned long long a;
+            while (in >> a) ptrs.push_back(reinterpret_cast<const void *>(static_cast<uintptr_t>(a)));
+            std::printf("fronts %d", gadei::fronts_log2_for(ptrs.data(), static_cast<int>(ptrs.size())));
+        } else if (cmd == "rows") {
+            unsigned long long bytes;
+            long count;
+            in >> bytes >> count;
+            const gadei::RowLayout r = gadei::row_layout(bytes, static_cast<int>(count));
+            std::printf("rows %zu %zu %zu %zu", r.head, r.stride, r.span,
+                        gadei::velocity_offset(bytes));
         } else if (cmd == "state") {
             std::printf("state ts=%llu pending=%zu pulls=%llu skipped=%llu",
                         static_cast<unsigned long long>(p.ts), p.pending(),

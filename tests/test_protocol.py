@@ -31,7 +31,8 @@ def driver(tmp_path_factory):
     cmd = ["g++", "-std=c++17", "-O1", "-g", "-fno-omit-frame-pointer", "-Wall", "-Wextra",
            "-Werror", "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
            "-I", os.path.join(ROOT, "include"), "-I", CSRC,
-           os.path.join(CSRC, "ps_protocol.cpp"), os.path.join(ROOT, "tests", "protocol_driver.cpp"),
+           os.path.join(CSRC, "ps_protocol.cpp"), os.path.join(CSRC, "ps_layout.cpp"),
+           os.path.join(ROOT, "tests", "protocol_driver.cpp"),
            "-o", exe]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0 and "asan" in (r.stderr + r.stdout).lower():
@@ -167,3 +168,40 @@ def test_scripts_reach_every_outcome(driver):
                     seen.add("dropped")
     assert seen == {"full", "mixed sync", "state refused", "round robin", "skipped pull",
                     "dropped"}, seen
+
+
+MIB2 = 2 << 20
+
+
+def test_row_layout_phases(driver):
+    """Server rows start at distinct 4 KiB offsets within 2 MiB, after the
+    offsets of w (0) and v (4 KiB), never overlap, and fit the span."""
+    for row_bytes, count in ((4 * 138_357_544, 64), (2 * 200_000_000, 32), (4, 3),
+                             (MIB2, 5), (MIB2 + 1, 600)):
+        out = run_driver(driver, [f"rows {row_bytes} {count}"])[0].split()
+        head, stride, span, v_off = map(int, out[1:])
+        assert v_off % MIB2 == 4096 and v_off >= row_bytes
+        starts = [head + i * stride for i in range(count)]
+        assert all(b - a >= row_bytes for a, b in zip(starts, starts[1:]))
+        assert starts[-1] + row_bytes == span
+        phases = [x % MIB2 for x in starts]
+        assert phases[:510] == [(i + 2) * 4096 for i in range(min(count, 510))]
+        assert 0 not in phases[:510] and 4096 not in phases[:510]
+
+
+def test_front_choice(driver):
+    """Four fronts (log2 = 2) for many streams at one offset within 2 MiB
+    (separately allocated buffers), one front for staggered buffers, for few
+    streams, and when half or more of the offsets are distinct."""
+    base = 0x7f0000000000
+    aligned = [base + i * 265 * MIB2 for i in range(34)]
+    staggered = [base + i * (265 * MIB2 + 4096) for i in range(34)]
+    lines = ["fronts " + " ".join(map(str, aligned)),
+             "fronts " + " ".join(map(str, staggered)),
+             "fronts " + " ".join(map(str, aligned[:7])),
+             "fronts " + " ".join(map(str, aligned[:8])),
+             "fronts " + " ".join(map(str, aligned[:17] + staggered[17:])),
+             "fronts " + " ".join(map(str, aligned[:19] + staggered[19:])),
+             "fronts " + " ".join(map(str, aligned[:16] + [0] * 16))]
+    assert run_driver(driver, lines) == ["fronts 2", "fronts 0", "fronts 0", "fronts 2",
+                                         "fronts 0", "fronts 2", "fronts 2"]
