@@ -56,5 +56,27 @@ def build_all(verbose: bool = False):
     return build(verbose), build(verbose, out=LIB_FMA, extra=FMA_FLAGS)
 
 
+# a plain C program that drives the C ABI without Python (tests/test_c_abi.py)
+C_SMOKE_SRC = os.path.join(ROOT, "tests", "c_abi_smoke.c")
+C_SMOKE = os.path.join(ROOT, "tests", "c_abi_smoke")
+ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
+
+
+def build_c_smoke(verbose: bool = False) -> str:
+    cmd = ["gcc", "-std=c99", "-O2", "-Wall", "-Wextra", "-Werror", "-D__HIP_PLATFORM_AMD__",
+           "-I", INCLUDE, "-I", os.path.join(ROCM, "include"), C_SMOKE_SRC,
+           "-L", HERE, "-lgadeips", "-L", os.path.join(ROCM, "lib"), "-lamdhip64",
+           "-Wl,-rpath,$ORIGIN/../paper_1611_06213_amd", "-Wl,-rpath," + os.path.join(ROCM, "lib"),
+           "-o", C_SMOKE + ".tmp"]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        sys.stderr.write(r.stdout + r.stderr)
+        raise RuntimeError("gcc failed building the C ABI smoke program")
+    os.replace(C_SMOKE + ".tmp", C_SMOKE)
+    return C_SMOKE
+
+
 if __name__ == "__main__":
     print(build_all(verbose=True))

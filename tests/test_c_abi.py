@@ -1,0 +1,29 @@
+"""The C ABI from a plain C program (tests/c_abi_smoke.c): no Python and no
+torch in that process, device memory from the HIP runtime, results checked
+against closed forms that are exact in binary32."""
+import os
+import subprocess
+
+import pytest
+
+from paper_1611_06213_amd import build as lib_build
+
+
+@pytest.mark.gpu
+def test_c_program_drives_the_abi():
+    if not os.path.exists(lib_build.C_SMOKE):
+        pytest.fail("tests/c_abi_smoke is not built (run __graft_entry__.build())")
+    r = subprocess.run([lib_build.C_SMOKE], capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0, r.stderr[-2000:]
+    assert "c abi ok" in r.stdout
+
+
+def test_c_program_builds_and_links():
+    """On the CPU: the program compiles warning-free against include/ps.h and
+    links against the library (built by __graft_entry__.build)."""
+    if not os.path.exists(lib_build.LIB):
+        pytest.fail("libgadeips.so is not built (run __graft_entry__.build())")
+    lib_build.build_c_smoke()
+    assert os.access(lib_build.C_SMOKE, os.X_OK)
+    r = subprocess.run(["ldd", lib_build.C_SMOKE], capture_output=True, text=True)
+    assert "libgadeips.so" in r.stdout and "not found" not in r.stdout, r.stdout
