@@ -407,18 +407,21 @@ class ParameterServer:
     def pull(self, learner: int, dst) -> None:
         self.pull_many([learner], [dst])
 
-    def pull_many(self, learners: Sequence[int], dsts) -> None:
+    def _replicas(self, learners: Sequence[int], dsts, what: str):
+        """Pointers and the one dtype of a pull's replica tensors."""
         if len(dsts) != len(learners):
-            raise ValueError("one destination per learner")
-        dt = _dtype_code(dsts[0]) if len(dsts) else PS_F32
-        ptrs = [self._tensor(d, "pull") for d in dsts]
+            raise ValueError(f"{what}: one destination per learner")
+        codes = {_dtype_code(d) for d in dsts}
+        if len(codes) > 1:
+            raise ValueError(f"{what}: all replicas of one call must share a dtype")
+        return [self._tensor(d, what) for d in dsts], (codes.pop() if codes else PS_F32)
+
+    def pull_many(self, learners: Sequence[int], dsts) -> None:
+        ptrs, dt = self._replicas(learners, dsts, "pull_many")
         self._check(ps_pull_many(self.h, list(learners), ptrs, dt), "pull_many")
 
     def apply_pull(self, learners: Sequence[int], dsts) -> None:
-        if len(dsts) != len(learners):
-            raise ValueError("one destination per learner")
-        dt = _dtype_code(dsts[0]) if len(dsts) else PS_F32
-        ptrs = [self._tensor(d, "apply_pull") for d in dsts]
+        ptrs, dt = self._replicas(learners, dsts, "apply_pull")
         self._check(ps_apply_pull(self.h, list(learners), ptrs, dt), "apply_pull")
         self._pending = []
 
@@ -480,8 +483,8 @@ class ParameterServer:
         out = torch.empty(self.n, dtype=torch.float32, device="cuda")
         stream = torch.cuda.current_stream().cuda_stream
         rc = _hip()(ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ptr),
-                                   ctypes.c_size_t(4 * self.n), 3,   # device to device
-                                   ctypes.c_void_p(stream))
+                    ctypes.c_size_t(4 * self.n), 3,   # device to device
+                    ctypes.c_void_p(stream))
         if rc != 0:
             raise PSError(PS_EHIP, f"hipMemcpyAsync failed ({rc})")
         return out

@@ -93,3 +93,31 @@ def test_one_hip_runtime_whatever_the_import_order():
     assert out.returncode == 0, out.stderr[-2000:]
     libs = ast.literal_eval(out.stdout.strip().splitlines()[-1])
     assert len(libs) == 1, libs
+
+
+def test_binding_refuses_mixed_replica_dtypes():
+    """The binding passes one dtype per pull call, so it must refuse replica
+    lists that mix dtypes (a bf16 buffer written as fp32 would overflow)."""
+    import torch
+    srv = ps.ParameterServer.__new__(ps.ParameterServer)
+    srv.n = 4
+    srv.h = 0
+
+    class FakeDev:
+        def __init__(self, dtype):
+            self.dtype = dtype
+            self.is_cuda = True
+
+        def is_contiguous(self):
+            return True
+
+        def numel(self):
+            return 4
+
+        def data_ptr(self):
+            return 4096
+
+    with pytest.raises(ValueError, match="share a dtype"):
+        srv._replicas([0, 1], [FakeDev(torch.float32), FakeDev(torch.bfloat16)], "pull_many")
+    ptrs, dt = srv._replicas([0, 1], [FakeDev(torch.bfloat16)] * 2, "pull_many")
+    assert dt == ps.PS_BF16 and ptrs == [4096, 4096]
