@@ -110,8 +110,8 @@ typedef struct ps_stats {
  * Eq. "gd") and heavy-ball momentum (0 disables it and allocates no v).
  * Allocates w (and v) on the current device; w starts at zero, v at +0,
  * timestamp 0, queue depth PS_MAX_QUEUE_DEPTH / 2 = 32, pull skipping on.
- * Returns NULL on failure (n_params == 0, lr or momentum not finite,
- * allocation failure); see ps_last_error(). */
+ * Returns NULL on failure (n_params == 0 or above 2^48, lr or momentum not
+ * finite, allocation failure); see ps_last_error(). */
 ps_server *ps_create(size_t n_params, float lr, float momentum);
 
 /* Wait for the server's stream, then free w and v and the handle. NULL is a

@@ -244,8 +244,8 @@ extern "C" {
 const char *ps_last_error(void) { return gadei::last_error(); }
 
 ps_server *ps_create(size_t n_params, float lr, float momentum) {
-    if (n_params == 0) {
-        fail(PS_EINVAL, "n_params must be positive");
+    if (n_params == 0 || n_params > (size_t(1) << 48)) {
+        fail(PS_EINVAL, "n_params must be in [1, 2^48]");
         return nullptr;
     }
     if (!std::isfinite(lr) || !std::isfinite(momentum)) {

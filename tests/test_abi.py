@@ -51,7 +51,9 @@ def test_header_constants_match_binding():
 
 def test_validation_without_device(lib):
     assert lib.ps_create(0, 0.1, 0.0) is None
-    assert "positive" in ps.ps_last_error()
+    assert "n_params" in ps.ps_last_error()
+    assert lib.ps_create((1 << 48) + 1, 0.1, 0.0) is None     # sizes could overflow
+    assert lib.ps_create(1 << 62, 0.1, 0.0) is None
     assert lib.ps_create(10, float("nan"), 0.0) is None
     assert lib.ps_create(10, 0.1, float("inf")) is None
     assert lib.ps_push(None, 0, None) == ps.PS_EINVAL
