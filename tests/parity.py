@@ -42,9 +42,11 @@ def pull_rounds(learners: Sequence[int]) -> List[List[int]]:
 
 
 def gpu_replay(cfg: wl.Config, events, pool, w0, ranges: Sequence[Tuple[int, int]],
-               fused: bool = False, pull_skip: bool = True, stream=None, fusion=None):
+               fused: bool = False, pull_skip: bool = True, stream=None, fusion=None,
+               replicas=None):
     """fused: drive apply+pull through ps_apply_pull; fusion: the replica
-    count up to which that call writes replicas from the apply pass."""
+    count up to which that call writes replicas from the apply pass;
+    replicas: the replica tensors (default: workloads.Rows)."""
     import torch
     srv = ps.ParameterServer(cfg.n, cfg.lr, cfg.momentum, queue_depth=cfg.depth)
     srv.set_pull_skip(pull_skip)
@@ -53,8 +55,12 @@ def gpu_replay(cfg: wl.Config, events, pool, w0, ranges: Sequence[Tuple[int, int
     srv.set_stream(stream or torch.cuda.current_stream())
     srv.set_weights(w0)
     rdt = torch.bfloat16 if cfg.pull_dtype == wl.BF16 else torch.float32
-    replicas = wl.Rows(cfg.replicas, cfg.n, rdt, "cuda")
-    replicas.buf.zero_()
+    if replicas is None:
+        replicas = wl.Rows(cfg.replicas, cfg.n, rdt, "cuda")
+        replicas.buf.zero_()
+    else:
+        for r in replicas:
+            r.zero_()
     snaps, stale = [], []
 
     widths = [hi - lo for lo, hi in ranges]

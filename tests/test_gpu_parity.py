@@ -113,6 +113,36 @@ def test_workload_full_size_sampled(torch, name, fused, fusion):
     assert parity.compare(g, o, ranges) == []
 
 
+@pytest.mark.parametrize("layout", ["server", "torch"])
+def test_vgg16_full_size_bench_layouts(torch, layout):
+    """VGG-16 at full size with the gradient pool and replicas laid out as
+    bench.py lays them out: server rows (ps_alloc_rows; one front), or one
+    torch allocation per buffer (--layout torch; four fronts chosen). Sampled
+    ranges against the oracle, as above."""
+    cfg = wl.CONFIGS["vgg16"]
+    say(f"[full] vgg16 layout={layout}")
+    ev = wl.schedule(cfg)
+    rdt = torch.float32
+    holder = ps.ParameterServer(cfg.n, cfg.lr, cfg.momentum)
+    if layout == "server":
+        pool = holder.alloc_rows(cfg.pool)
+        reps = holder.alloc_rows(cfg.replicas, rdt)
+    else:
+        pool = [torch.empty(cfg.n, device="cuda") for _ in range(cfg.pool)]
+        reps = [torch.empty(cfg.n, dtype=rdt, device="cuda") for _ in range(cfg.replicas)]
+    for j in range(cfg.pool):
+        pool[j].copy_(wl.make_grad(cfg, j, "cuda"))
+    w0 = wl.make_w0(cfg, "cuda")
+    ranges = _full_ranges(cfg)
+    g = parity.gpu_replay(cfg, ev, pool, w0, ranges, replicas=reps)
+    ps_, w0s = parity.host_inputs(cfg, pool, w0, ranges)
+    del pool, reps
+    holder.close()
+    free(torch)
+    o = parity.oracle_replay(cfg, ev, ps_, w0s, ranges)
+    assert parity.compare(g, o, ranges) == []
+
+
 def test_mixed_bf16_quantisation_bound_vs_fp32_gradients(torch):
     """The bf16-gradient run against the oracle fed the original fp32
     gradients x (before rounding to bf16). Each push k changes the gradient
