@@ -1069,29 +1069,36 @@ def test_alloc_rows_layout_and_parity(torch):
     free(torch)
 
 
+def _host_grad(torch, g):
+    h = g.cpu()
+    return h.view(torch.int16).numpy().view(np.uint16) if g.dtype == torch.bfloat16 else h.numpy()
+
+
+@pytest.mark.parametrize("gdt", ["f32", "bf16"])
 @pytest.mark.parametrize("layout", ["separate", "server_rows"])
-def test_fronts_give_identical_bits(torch, layout):
+def test_fronts_give_identical_bits(torch, layout, gdt):
     """Every front count (and the automatic choice) folds the same
     gradients into the same bits, for separately allocated buffers (one
-    phase) and for server rows (distinct phases); the synchronous step
-    too."""
+    phase) and for server rows (distinct phases), fp32 gradients (4 per
+    lane) and bf16 gradients (8 per lane); the synchronous step too."""
     n, k, lr, m = 5 * (1 << 20) + 3, 32, 0.01, 0.9
-    say(f"[case] fronts layout={layout} n={n}")
+    say(f"[case] fronts layout={layout} gradients={gdt} n={n}")
+    tdt = torch.bfloat16 if gdt == "bf16" else torch.float32
     gen = torch.Generator(device="cuda")
     gen.manual_seed(37)
     w0 = (torch.rand(n, generator=gen, device="cuda") - 0.5) * 0.1
     holder = ps.ParameterServer(n, lr, m)
     if layout == "separate":
-        grads = [torch.empty(n, device="cuda") for _ in range(k)]
+        grads = [torch.empty(n, dtype=tdt, device="cuda") for _ in range(k)]
     else:
-        grads = holder.alloc_rows(k)
+        grads = holder.alloc_rows(k, tdt)
     for g in grads:
-        g.copy_(torch.randn(n, generator=gen, device="cuda") * 1e-3)
+        g.copy_((torch.randn(n, generator=gen, device="cuda") * 1e-3).to(tdt))
     o = _oracle_apply(torch, w0, grads, lr, m, k)
     want = o.w.view(np.uint32).copy()
     so = orc.OracleServer(w0.cpu().numpy(), lr, m, depth=16)
     for j in range(16):
-        so.push(j, grads[j].cpu().numpy())
+        so.push(j, _host_grad(torch, grads[j]))
     so.apply_sync()
     want_sync = so.w.view(np.uint32).copy()
     for f in (-1, 0, 1, 2, 3):
