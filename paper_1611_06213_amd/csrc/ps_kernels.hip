@@ -355,12 +355,17 @@ __global__ void __launch_bounds__(kBlock) pull_vec(const PullArgs a) {
 // write stream at a time instead of R interleaved ones, which the memory
 // system serves markedly faster. HBM traffic stays one read of w plus the R
 // replica writes.
-// A tile is the coordinates whose replica data fill 8 MiB: 2 Mi coordinates
-// for fp32 replicas, 4 Mi for bf16 (measured best for both).
-constexpr uint64_t kTileReplicaBytes = 8u << 20;
+// A tile is 4 Mi coordinates (16 MiB of w). fp32 replicas take one 16-byte
+// chunk per lane (4096 blocks per tile and replica), bf16 replicas two
+// 8-value chunks per lane (1024 blocks): with every block of a (tile,
+// replica) group resident at once, the chip writes one replica stream at a
+// time. Measured best of 4/8/16/32 MiB tiles and 1/2/4/8 chunks per lane for
+// each replica dtype.
 template <int PDT>
-constexpr uint64_t tile_coords() { return kTileReplicaBytes / (PDT == PS_BF16 ? 2 : 4); }
-constexpr unsigned kTileBlocks = 1024;      // blocks per (tile, replica)
+constexpr uint64_t tile_coords() { return uint64_t(4) << 20; }
+template <int PDT>
+constexpr uint64_t lane_chunks() { return PDT == PS_BF16 ? 2 : 1; }
+constexpr unsigned kTileBlocks = 4096;      // most blocks per (tile, replica)
 
 template <int PDT, int E>
 __global__ void __launch_bounds__(kBlock) pull_tiled(const PullArgs a, unsigned bpt) {
@@ -492,7 +497,7 @@ void go_pull_tiled(const PullArgs &a, const Geometry &geo, hipStream_t s) {
     const uint64_t chunks = a.n / E;
     const uint64_t tiles = chunks == 0 ? 1 : (chunks + kTileChunksE - 1) / kTileChunksE;
     const uint64_t per_tile = chunks < kTileChunksE ? chunks : kTileChunksE;
-    uint64_t bpt = (per_tile + 2 * kBlock - 1) / (2 * kBlock);
+    uint64_t bpt = (per_tile + lane_chunks<PDT>() * kBlock - 1) / (lane_chunks<PDT>() * kBlock);
     if (bpt < 1) bpt = 1;
     if (bpt > kTileBlocks) bpt = kTileBlocks;
     const uint64_t groups = tiles * static_cast<uint64_t>(a.r);
