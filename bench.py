@@ -73,9 +73,20 @@ def batches(cfg, wl):
     return out
 
 
+def kernel_source_digest(path: str = KERNEL_SRC) -> str:
+    """sha256 of the kernel source with comments and blank space removed, so
+    that a comment-only edit keeps recorded counters valid and any code
+    change invalidates them."""
+    import re
+    text = open(path).read()
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return hashlib.sha256(" ".join(text.split()).encode()).hexdigest()
+
+
 def recorded_traffic(kernel_label: str):
     """HBM bytes per launch from the committed counter summary, or None when
-    it is missing or was taken on a different kernel source."""
+    it is missing or was taken on different kernel code."""
     if not os.path.exists(COUNTERS):
         return None
     vals = {}
@@ -83,8 +94,7 @@ def recorded_traffic(kernel_label: str):
         if ":" in line and not line.startswith("#"):
             k, v = line.split(":", 1)
             vals[k.strip()] = v.strip()
-    src = hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
-    if vals.get("kernel_source_sha256") != src or vals.get("mode") != kernel_label:
+    if vals.get("kernel_code_digest") != kernel_source_digest() or vals.get("mode") != kernel_label:
         return None
     try:
         return float(vals["hbm_bytes_per_launch"])

@@ -1,10 +1,13 @@
 // HIP kernels of the parameter server for gfx950 (CDNA4).
 //
-// All three kernels are pure streams over HBM: every byte is read or written
-// once per launch and there is no reuse to stage in LDS and no contraction
-// for the matrix cores. What matters is that each wave moves whole, aligned
-// 16-byte (fp32) or 8-byte (bf16) lanes, that enough loads are in flight per
-// wave, and that nothing is re-read.
+// The kernels are pure streams over HBM: every byte is read or written once
+// per launch and there is no reuse to stage in LDS and no contraction for
+// the matrix cores. What matters is that each lane moves whole, aligned
+// 16-byte chunks (4 fp32 or 8 bf16 values; narrower only for misaligned
+// buffers), that enough loads are in flight, that nothing is re-read, and
+// which coordinates the resident blocks work on at the same time (the DRAM
+// serves some access patterns faster than others: see front_block and
+// pull_tiled).
 //
 // apply:  for each coordinate i and each pending gradient k = 0..K-1, oldest
 //         first, one ASGD step (Eq. "asgd" with the step of Eq. "gd"):
@@ -14,6 +17,8 @@
 //         registers, and the result stored once: K sequential steps cost one
 //         pass over w instead of K. Optionally the same pass writes R replica
 //         copies of the new w (a fused pull).
+// sync:   the synchronous step (Eq. "ssgd"): the K pending gradients summed
+//         per coordinate in push order, divided by K, applied as one step.
 // pull:   write w to R replica buffers (fp32, or bf16 rounded to nearest
 //         even). One replica: a streaming copy. Several: a tiled fan-out that
 //         keeps each tile of w in the memory-side cache while the replicas

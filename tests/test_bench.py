@@ -1,0 +1,26 @@
+"""bench.py's host-side pieces on the CPU: the kernel-code digest that keys
+recorded counters, and the multi-GPU refusal."""
+import os
+import subprocess
+import sys
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+import bench  # noqa: E402
+
+
+def test_kernel_digest_ignores_comments_not_code(tmp_path):
+    a = tmp_path / "a.hip"
+    a.write_text("// header\n__global__ void k(float *p) { p[0] = 1.0f; /* one */ }\n")
+    b = tmp_path / "b.hip"
+    b.write_text("/* another\n header */\n__global__ void k(float *p) {\n  p[0] = 1.0f; // one\n}\n")
+    c = tmp_path / "c.hip"
+    c.write_text("__global__ void k(float *p) { p[0] = 2.0f; }\n")
+    da, db, dc = (bench.kernel_source_digest(str(x)) for x in (a, b, c))
+    assert da == db != dc
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2 and "one GPU" in r.stderr
