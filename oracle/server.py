@@ -42,6 +42,11 @@ Readings where the paper is silent (each also listed in the design notes):
   * a pull is skipped iff the same learner pulls into the same buffer with
     the same dtype and the timestamp has not moved since its last pull.
 
+Parity unpinned against the paper (pinned only to the reading itself, by the
+tests' closed forms and hand-worked scripts): the momentum step, which the
+paper does not have, and round-robin service taking one gradient per visit,
+which the paper states in a listing that is not in its text.
+
 The oracle can be run on any coordinate range [lo, hi) of a workload: every
 step is per coordinate (Eq. "gd" is written for the k-th parameter), so the
 range run is exactly the full run restricted to those coordinates.
