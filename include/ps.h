@@ -37,8 +37,12 @@
  * A bf16 gradient is widened exactly to fp32 first. A bf16 pull writes w
  * rounded to nearest even bf16.
  *
- * Threading: calls on one handle must not overlap (one thread at a time).
- * Distinct handles are independent.
+ * Threading: every call takes the handle's lock, so several host threads
+ * may use one server, e.g. a push thread per learner beside a server thread
+ * that applies and serves pulls (the paper's thread layout, Sec. 4.1).
+ * Calls are served one at a time in lock order, and device work is enqueued
+ * in that order. ps_sync waits without holding the lock. ps_destroy must
+ * not race other calls on the handle. Distinct handles are independent.
  *
  * Pointers named "device" must point to device memory (hipMalloc or torch
  * CUDA tensors) on the device that was current at ps_create. Any alignment is

@@ -13,6 +13,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -53,7 +54,13 @@ struct ps_server {
     int fuse_max_r = 1;   // ps_apply_pull writes up to this many replicas in the apply pass
     gadei::Geometry geo;
     gadei::Protocol proto;
+    // Every call on the handle holds this lock, so several host threads (a
+    // push thread per learner, as in Sec. 4.1) may share one server; device
+    // work is enqueued in lock order. Recursive: some calls use others.
+    mutable std::recursive_mutex mu;
 };
+
+#define PS_LOCK(ps) std::lock_guard<std::recursive_mutex> ps_lock_(ps->mu)
 
 namespace {
 
@@ -285,17 +292,21 @@ ps_server *ps_create(size_t n_params, float lr, float momentum) {
 
 void ps_destroy(ps_server *ps) {
     if (ps == nullptr) return;
-    if (use_device(ps) == PS_OK) {
-        (void)hipStreamSynchronize(ps->stream);
-        if (ps->pull_lock_free) (void)hipStreamSynchronize(ps->pull_stream);
-        for (const RowSet &r : ps->row_sets) (void)hipFree(r.base);
-        (void)hipFree(ps->wv_base);
+    {
+        PS_LOCK(ps);   // waits for a call still running on another thread
+        if (use_device(ps) == PS_OK) {
+            (void)hipStreamSynchronize(ps->stream);
+            if (ps->pull_lock_free) (void)hipStreamSynchronize(ps->pull_stream);
+            for (const RowSet &r : ps->row_sets) (void)hipFree(r.base);
+            (void)hipFree(ps->wv_base);
+        }
     }
     delete ps;
 }
 
 int ps_alloc_rows(ps_server *ps, int count, int dtype, void **rows) {
     if (int rc = check(ps)) return rc;
+    PS_LOCK(ps);
     if (count < 1 || count > PS_MAX_ROWS)
         return fail(PS_EINVAL, "row count %d outside [1, %d]", count, PS_MAX_ROWS);
     if (dtype != PS_F32 && dtype != PS_BF16) return fail(PS_EINVAL, "bad row dtype %d", dtype);
@@ -320,6 +331,7 @@ int ps_alloc_rows(ps_server *ps, int count, int dtype, void **rows) {
 
 int ps_free_rows(ps_server *ps, void *first_row) {
     if (int rc = check(ps)) return rc;
+    PS_LOCK(ps);
     auto it = std::find_if(ps->row_sets.begin(), ps->row_sets.end(),
                            [&](const RowSet &r) { return r.first == first_row; });
     if (it == ps->row_sets.end()) return fail(PS_EINVAL, "not the first row of a row set");
@@ -336,6 +348,7 @@ int ps_free_rows(ps_server *ps, void *first_row) {
 
 int ps_push_async(ps_server *ps, int learner_id, const void *grad, int dtype, void *ready_event) {
     if (int rc = check(ps)) return rc;
+    PS_LOCK(ps);
     return ps->proto.push(learner_id, dtype, grad, ready_event);
 }
 
@@ -349,6 +362,7 @@ int ps_push(ps_server *ps, int learner_id, const void *grad) {
 
 int ps_apply_pending(ps_server *ps) {
     if (int rc = check(ps)) return rc;
+    PS_LOCK(ps);
     if (ps->proto.pending() == 0) {
         ps->proto.clear_last();
         return PS_OK;
@@ -364,6 +378,7 @@ int ps_apply_pending(ps_server *ps) {
 
 int ps_apply_sync(ps_server *ps) {
     if (int rc = check(ps)) return rc;
+    PS_LOCK(ps);
     if (ps->proto.pending() == 0) {
         ps->proto.clear_last();
         return PS_OK;
@@ -395,6 +410,7 @@ int ps_apply_sync(ps_server *ps) {
 
 int ps_pull_many(ps_server *ps, int n, const int *learner_ids, void *const *dsts, int dst_dtype) {
     if (int rc = check(ps)) return rc;
+    PS_LOCK(ps);
     std::vector<int> write;
     if (int rc = ps->proto.plan_pulls(n, learner_ids, dsts, dst_dtype, ps->proto.ts, write))
         return rc;
@@ -412,6 +428,7 @@ int ps_pull(ps_server *ps, int learner_id, void *dst) {
 
 int ps_apply_pull(ps_server *ps, int n, const int *learner_ids, void *const *dsts, int dst_dtype) {
     if (int rc = check(ps)) return rc;
+    PS_LOCK(ps);
     if (ps->proto.pending() == 0) {
         const int rc = ps_pull_many(ps, n, learner_ids, dsts, dst_dtype);
         if (rc == PS_OK) ps->proto.clear_last();
@@ -441,11 +458,13 @@ int ps_apply_pull(ps_server *ps, int n, const int *learner_ids, void *const *dst
 
 int ps_drop_learner(ps_server *ps, int learner_id) {
     if (int rc = check(ps)) return rc;
+    PS_LOCK(ps);
     return ps->proto.drop_learner(learner_id);
 }
 
 int ps_save(ps_server *ps, const char *path) {
     if (int rc = check(ps)) return rc;
+    PS_LOCK(ps);
     if (path == nullptr) return fail(PS_EINVAL, "null path");
     if (ps->proto.pending() != 0) return fail(PS_ESTATE, "gradients pending");
     if (int rc = use_device(ps)) return rc;
@@ -487,6 +506,7 @@ int ps_save(ps_server *ps, const char *path) {
 
 int ps_load(ps_server *ps, const char *path) {
     if (int rc = check(ps)) return rc;
+    PS_LOCK(ps);
     if (path == nullptr) return fail(PS_EINVAL, "null path");
     if (ps->proto.pending() != 0) return fail(PS_ESTATE, "gradients pending");
     FILE *f = std::fopen(path, "rb");
@@ -545,22 +565,26 @@ int ps_load(ps_server *ps, const char *path) {
 
 int ps_set_stream(ps_server *ps, void *hip_stream) {
     if (int rc = check(ps)) return rc;
+    PS_LOCK(ps);
     ps->stream = static_cast<hipStream_t>(hip_stream);
     return PS_OK;
 }
 
 int ps_set_queue_depth(ps_server *ps, int depth) {
     if (int rc = check(ps)) return rc;
+    PS_LOCK(ps);
     return ps->proto.set_depth(depth);
 }
 
 int ps_set_queue_mode(ps_server *ps, int mode, int slots_per_learner) {
     if (int rc = check(ps)) return rc;
+    PS_LOCK(ps);
     return ps->proto.set_mode(mode, slots_per_learner);
 }
 
 int ps_set_pull_fusion(ps_server *ps, int max_replicas) {
     if (int rc = check(ps)) return rc;
+    PS_LOCK(ps);
     if (max_replicas < 0 || max_replicas > PS_MAX_REPLICAS)
         return fail(PS_EINVAL, "fusion limit %d outside [0, %d]", max_replicas, PS_MAX_REPLICAS);
     ps->fuse_max_r = max_replicas;
@@ -569,6 +593,7 @@ int ps_set_pull_fusion(ps_server *ps, int max_replicas) {
 
 int ps_set_fronts(ps_server *ps, int fronts_log2) {
     if (int rc = check(ps)) return rc;
+    PS_LOCK(ps);
     if (fronts_log2 < -1 || fronts_log2 > 3)
         return fail(PS_EINVAL, "fronts_log2 %d outside [-1, 3]", fronts_log2);
     ps->geo.fronts_log2 = fronts_log2;
@@ -577,12 +602,14 @@ int ps_set_fronts(ps_server *ps, int fronts_log2) {
 
 int ps_set_pull_skip(ps_server *ps, int enabled) {
     if (int rc = check(ps)) return rc;
+    PS_LOCK(ps);
     ps->proto.pull_skip = enabled != 0;
     return PS_OK;
 }
 
 int ps_set_weights(ps_server *ps, const float *src) {
     if (int rc = check(ps)) return rc;
+    PS_LOCK(ps);
     if (src == nullptr) return fail(PS_EINVAL, "null source");
     if (ps->proto.pending() != 0) return fail(PS_ESTATE, "gradients pending");
     if (int rc = use_device(ps)) return rc;
@@ -601,15 +628,21 @@ int ps_set_weights(ps_server *ps, const float *src) {
 const float *ps_weights(const ps_server *ps) { return ps ? ps->w : nullptr; }
 const float *ps_velocity(const ps_server *ps) { return ps ? ps->v : nullptr; }
 size_t ps_num_params(const ps_server *ps) { return ps ? ps->n : 0; }
-uint64_t ps_timestamp(const ps_server *ps) { return ps ? ps->proto.ts : 0; }
+uint64_t ps_timestamp(const ps_server *ps) {
+    if (ps == nullptr) return 0;
+    PS_LOCK(ps);
+    return ps->proto.ts;
+}
 
 int ps_pending(const ps_server *ps) {
     if (int rc = check(ps)) return rc;
+    PS_LOCK(ps);
     return static_cast<int>(ps->proto.pending());
 }
 
 int ps_last_staleness(const ps_server *ps, int64_t *out, int cap) {
     if (int rc = check(ps)) return rc;
+    PS_LOCK(ps);
     if (cap < 0 || (cap > 0 && out == nullptr)) return fail(PS_EINVAL, "bad output buffer");
     const std::vector<int64_t> &s = ps->proto.last_staleness;
     const int count = static_cast<int>(s.size());
@@ -619,6 +652,7 @@ int ps_last_staleness(const ps_server *ps, int64_t *out, int cap) {
 
 int ps_last_applied(const ps_server *ps, int *learner_ids, int cap) {
     if (int rc = check(ps)) return rc;
+    PS_LOCK(ps);
     if (cap < 0 || (cap > 0 && learner_ids == nullptr)) return fail(PS_EINVAL, "bad output buffer");
     const std::vector<int> &a = ps->proto.last_applied;
     const int count = static_cast<int>(a.size());
@@ -628,14 +662,29 @@ int ps_last_applied(const ps_server *ps, int *learner_ids, int cap) {
 
 int ps_sync(ps_server *ps) {
     if (int rc = check(ps)) return rc;
-    if (int rc = use_device(ps)) return rc;
-    hipError_t e = hipStreamSynchronize(ps->stream);
+    hipStream_t s, ps_s;
+    bool lock_free;
+    {
+        // take the streams under the lock, wait without it so that pushes
+        // from other threads are not held up by the wait
+        PS_LOCK(ps);
+        if (int rc = use_device(ps)) return rc;
+        s = ps->stream;
+        ps_s = ps->pull_stream;
+        lock_free = ps->pull_lock_free;
+    }
+    hipError_t e = hipStreamSynchronize(s);
     if (e != hipSuccess) return fail_hip(e, "hipStreamSynchronize");
-    return drain_pulls(ps);
+    if (lock_free) {
+        e = hipStreamSynchronize(ps_s);
+        if (e != hipSuccess) return fail_hip(e, "hipStreamSynchronize (pull stream)");
+    }
+    return PS_OK;
 }
 
 int ps_record(ps_server *ps, void *event) {
     if (int rc = check(ps)) return rc;
+    PS_LOCK(ps);
     if (event == nullptr) return fail(PS_EINVAL, "null event");
     if (int rc = use_device(ps)) return rc;
     hipError_t e = hipEventRecord(static_cast<hipEvent_t>(event), ps->stream);
@@ -645,6 +694,7 @@ int ps_record(ps_server *ps, void *event) {
 
 int ps_set_pull_stream(ps_server *ps, void *hip_stream) {
     if (int rc = check(ps)) return rc;
+    PS_LOCK(ps);
     if (int rc = use_device(ps)) return rc;
     if (int rc = drain_pulls(ps)) return rc;
     ps->pull_lock_free = hip_stream != nullptr;
@@ -654,6 +704,7 @@ int ps_set_pull_stream(ps_server *ps, void *hip_stream) {
 
 int ps_get_stats(const ps_server *ps, ps_stats *out) {
     if (int rc = check(ps)) return rc;
+    PS_LOCK(ps);
     if (out == nullptr) return fail(PS_EINVAL, "null stats output");
     *out = ps->proto.stats;
     out->timestamp = ps->proto.ts;

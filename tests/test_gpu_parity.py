@@ -1119,3 +1119,68 @@ def test_fronts_give_identical_bits(torch, layout, gdt):
         holder.set_fronts(4)
     holder.close()
     free(torch)
+
+
+# ---------------------------------------------------------------- host threads
+
+def test_learner_threads_push_while_server_applies(torch):
+    """Eight learner threads push concurrently (ctypes drops the GIL, so the C
+    calls overlap) while the main thread applies and pulls, as in the paper's
+    thread layout (Sec. 4.1). Every accepted push is applied exactly once,
+    each learner's gradients in its own order (Theorem 2), and the weights
+    equal the oracle replaying the order the server reports."""
+    import threading
+    n, learners, per, lr, m = (1 << 20) + 3, 8, 24, 0.01, 0.9
+    say(f"[case] threads learners={learners} pushes={learners * per}")
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(61)
+    w0 = (torch.rand(n, generator=gen, device="cuda") - 0.5) * 0.1
+    grads = [[torch.randn(n, generator=gen, device="cuda") * 1e-3 for _ in range(per)]
+             for _ in range(learners)]
+    srv = ps.ParameterServer(n, lr, m, queue_depth=32)
+    srv.set_stream(torch.cuda.current_stream())
+    srv.set_weights(w0)
+    torch.cuda.synchronize()
+    h = srv.h
+    errors = []
+
+    def learner(l):
+        for j in range(per):
+            while True:
+                rc = ps.ps_push_dtype(h, l, grads[l][j].data_ptr(), ps.PS_F32)
+                if rc == ps.PS_OK:
+                    break
+                if rc != ps.PS_EFULL:
+                    errors.append((l, j, rc))
+                    return
+
+    threads = [threading.Thread(target=learner, args=(l,)) for l in range(learners)]
+    for t in threads:
+        t.start()
+    order = []
+    dst = torch.empty(n, device="cuda")
+    while len(order) < learners * per:
+        assert ps.ps_apply_pending(h) == ps.PS_OK
+        order += ps.ps_last_applied(h)
+        assert ps.ps_pull_many(h, [len(order) % learners], [dst.data_ptr()], ps.PS_F32) == 0
+        if not any(t.is_alive() for t in threads) and ps.ps_pending(h) == 0:
+            break
+    for t in threads:
+        t.join()
+    assert ps.ps_apply_pending(h) == ps.PS_OK
+    order += ps.ps_last_applied(h)
+    assert errors == []
+    assert len(order) == learners * per and all(order.count(l) == per for l in range(learners))
+    st = srv.stats()
+    assert st.pushes_accepted == st.pushes_applied == srv.timestamp == learners * per
+    # replay: the j-th time learner l appears is its j-th gradient
+    o = orc.OracleServer(w0.cpu().numpy(), lr, m, depth=1)
+    seen = [0] * learners
+    for l in order:
+        assert o.push(l, grads[l][seen[l]].cpu().numpy()) == orc.OK
+        o.apply_pending()
+        seen[l] += 1
+    assert parity.bitwise(parity.np_bits(srv.weights_copy()), o.w.view(np.uint32))
+    assert parity.bitwise(parity.np_bits(srv.velocity_copy()), o.v.view(np.uint32))
+    srv.close()
+    free(torch)
