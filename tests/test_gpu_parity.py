@@ -1184,3 +1184,20 @@ def test_learner_threads_push_while_server_applies(torch):
     assert parity.bitwise(parity.np_bits(srv.velocity_copy()), o.v.view(np.uint32))
     srv.close()
     free(torch)
+
+
+def test_alloc_rows_argument_errors(torch):
+    """ps_alloc_rows / ps_free_rows / ps_set_fronts refuse bad arguments with
+    PS_EINVAL and change nothing."""
+    srv = ps.ParameterServer(1000, 0.01, 0.0)
+    assert ps.ps_alloc_rows(srv.h, 0, ps.PS_F32)[0] == ps.PS_EINVAL
+    assert ps.ps_alloc_rows(srv.h, ps.PS_MAX_ROWS + 1, ps.PS_F32)[0] == ps.PS_EINVAL
+    assert ps.ps_alloc_rows(srv.h, 2, 7)[0] == ps.PS_EINVAL
+    assert ps.load_library().ps_alloc_rows(srv.h, 2, ps.PS_F32, None) == ps.PS_EINVAL
+    assert ps.ps_free_rows(srv.h, 0) == ps.PS_EINVAL
+    assert ps.ps_set_fronts(srv.h, -2) == ps.PS_EINVAL and ps.ps_set_fronts(srv.h, 4) == ps.PS_EINVAL
+    rc, rows = ps.ps_alloc_rows(srv.h, ps.PS_MAX_ROWS, ps.PS_BF16)   # 4096 rows of 1000 values
+    assert rc == ps.PS_OK and len(set(rows)) == ps.PS_MAX_ROWS
+    assert ps.ps_free_rows(srv.h, rows[1]) == ps.PS_EINVAL           # not a first row
+    assert ps.ps_free_rows(srv.h, rows[0]) == ps.PS_OK
+    srv.close()
