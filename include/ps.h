@@ -291,9 +291,10 @@ int ps_load(ps_server *ps, const char *path);
 /* Server-owned device buffers for gradients or replicas: the paper's queue
  * slots, which the server holds and learners fill (Sec. 4.1). Allocates
  * `count` (1..PS_MAX_ROWS) buffers of n_params values of `dtype` in one
- * device allocation and writes their addresses to rows[0..count). Row i
- * starts on a 2 MiB boundary plus (i + 2) * 4 KiB (mod 2 MiB); w and v sit
- * at phases 0 and 4 KiB. An apply then streams its gradients, w and v from
+ * device allocation and writes their addresses to rows[0..count). A row
+ * of 2 MiB or more starts on a 2 MiB boundary plus (i + 2) * 4 KiB (mod
+ * 2 MiB); w and v sit at phases 0 and 4 KiB. Smaller rows are packed on
+ * 4 KiB boundaries. An apply then streams its gradients, w and v from
  * distinct offsets within 2 MiB, which the DRAM serves fastest. Buffers
  * allocated one by one (2 MiB-aligned, all at one phase) are served slower;
  * for them the apply kernels switch to a schedule that recovers part of the

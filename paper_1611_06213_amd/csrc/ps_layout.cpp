@@ -14,7 +14,10 @@ size_t velocity_offset(size_t w_bytes) { return round_up(w_bytes, kRowAlign) + k
 RowLayout row_layout(size_t row_bytes, int count) {
     RowLayout r;
     r.head = 2 * kRowStagger;
-    r.stride = round_up(row_bytes, kRowAlign) + kRowStagger;
+    // rows under 2 MiB are packed on 4 KiB boundaries (their phases differ
+    // anyway, and rounding each up to 2 MiB would waste memory)
+    r.stride = row_bytes < kRowAlign ? round_up(row_bytes, kRowStagger)
+                                     : round_up(row_bytes, kRowAlign) + kRowStagger;
     r.span = r.head + (static_cast<size_t>(count) - 1) * r.stride + row_bytes;
     return r;
 }

@@ -25,9 +25,10 @@ char *align_up(void *p, size_t a);
 size_t velocity_offset(size_t w_bytes);
 
 // A set of `count` rows of row_bytes each, from a 2 MiB-aligned base: row i
-// at head + i * stride, so at offset (i + 2) * 4 KiB within 2 MiB (w and v
-// take the first two offsets). `span` = bytes from the base to the end of
-// the last row.
+// at head + i * stride. Rows of 2 MiB or more step by their 2 MiB-rounded
+// size plus 4 KiB, so row i sits at offset (i + 2) * 4 KiB within 2 MiB (w
+// and v take the first two offsets); smaller rows are packed on 4 KiB
+// boundaries. `span` = bytes from the base to the end of the last row.
 struct RowLayout {
     size_t head;
     size_t stride;

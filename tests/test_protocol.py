@@ -177,7 +177,7 @@ def test_row_layout_phases(driver):
     """Server rows start at distinct 4 KiB offsets within 2 MiB, after the
     offsets of w (0) and v (4 KiB), never overlap, and fit the span."""
     for row_bytes, count in ((4 * 138_357_544, 64), (2 * 200_000_000, 32), (4, 3),
-                             (MIB2, 5), (MIB2 + 1, 600)):
+                             (4096, 7), (MIB2, 5), (MIB2 + 1, 600)):
         out = run_driver(driver, [f"rows {row_bytes} {count}"])[0].split()
         head, stride, span, v_off = map(int, out[1:])
         assert v_off % MIB2 == 4096 and v_off >= row_bytes
@@ -205,3 +205,13 @@ def test_front_choice(driver):
              "fronts " + " ".join(map(str, aligned[:16] + [0] * 16))]
     assert run_driver(driver, lines) == ["fronts 2", "fronts 0", "fronts 0", "fronts 2",
                                          "fronts 0", "fronts 2", "fronts 2"]
+
+
+def test_small_rows_are_packed(driver):
+    """Rows under 2 MiB step by their size rounded to 4 KiB: no 2 MiB of
+    padding each, still disjoint and 4 KiB-aligned."""
+    for row_bytes, count in ((5000, 100), (2000, 4096), (MIB2 - 1, 3)):
+        out = run_driver(driver, [f"rows {row_bytes} {count}"])[0].split()
+        head, stride, span = map(int, out[1:4])
+        assert stride == (row_bytes + 4095) // 4096 * 4096 and head == 8192
+        assert span == head + (count - 1) * stride + row_bytes
