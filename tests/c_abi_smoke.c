@@ -10,14 +10,18 @@
  *
  * plus the queue contract (a full queue refuses the push, Sec. 4.1), the
  * timestamp (one per applied gradient, Sec. 2.1), a bf16 pull (w rounded to
- * nearest even) and server-owned rows. Built by the package build next to the
- * library and run by tests/test_c_abi.py on a GPU. Prints "c abi ok".
+ * nearest even) and server-owned rows. Then times 20,000 Tiny-shaped
+ * push + apply_pull steps (no Python in the loop). Built by the package
+ * build next to the library and run by tests/test_c_abi.py on a GPU.
+ * Prints "c abi ok".
  */
+#define _POSIX_C_SOURCE 199309L
 #include <hip/hip_runtime_api.h>
 #include <stdint.h>
 #include <stdio.h>
 #include <stdlib.h>
 #include <string.h>
+#include <time.h>
 
 #include "ps.h"
 
@@ -151,6 +155,35 @@ int main(void)
     CHECK(ps_free_rows(ps, rows[0]) == PS_OK, "ps_free_rows");
     CHECK(ps_free_rows(ps, rows[0]) == PS_EINVAL, "second ps_free_rows");
     ps_destroy(ps);
+
+    /* the Tiny shape (2^20 parameters, one gradient per apply, the pushing
+     * learner pulls after every push) driven from C: the library's own cost
+     * per push, with no Python in the loop; gradients cycle over 8 rows */
+    {
+        const size_t nt = (size_t)1 << 20;
+        ps = ps_create(nt, 0.01f, 0.0f);
+        CHECK(ps != NULL, "ps_create (tiny)");
+        CHECK(ps_set_queue_depth(ps, 1) == PS_OK, "depth 1");
+        void *g8[8];
+        CHECK(ps_alloc_rows(ps, 8, PS_F32, g8) == PS_OK, "rows (tiny)");
+        for (int j = 0; j < 8; ++j) HIPCHECK(hipMemset(g8[j], 0, nt * sizeof(float)));
+        void *d = rep;
+        const int steps = 20000;
+        struct timespec t0, t1;
+        CHECK(ps_sync(ps) == PS_OK, "sync");
+        clock_gettime(CLOCK_MONOTONIC, &t0);
+        for (int j = 0; j < steps; ++j) {
+            int l = j & 3;
+            CHECK(ps_push(ps, l, g8[j & 7]) == PS_OK, "tiny push");
+            CHECK(ps_apply_pull(ps, 1, &l, &d, PS_F32) == PS_OK, "tiny apply_pull");
+        }
+        CHECK(ps_sync(ps) == PS_OK, "sync");
+        clock_gettime(CLOCK_MONOTONIC, &t1);
+        const double s = (double)(t1.tv_sec - t0.tv_sec) + 1e-9 * (double)(t1.tv_nsec - t0.tv_nsec);
+        CHECK(ps_timestamp(ps) == (uint64_t)steps, "tiny timestamp");
+        printf("tiny loop: %.2f us per push+apply+pull, %.0f pushes/s\n", s / steps * 1e6, steps / s);
+        ps_destroy(ps);
+    }
 
     HIPCHECK(hipFree(w_init));
     HIPCHECK(hipFree(grad));

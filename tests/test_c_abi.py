@@ -16,6 +16,9 @@ def test_c_program_drives_the_abi():
     r = subprocess.run([lib_build.C_SMOKE], capture_output=True, text=True, timeout=120)
     assert r.returncode == 0, r.stderr[-2000:]
     assert "c abi ok" in r.stdout
+    for line in r.stdout.splitlines():
+        if line.startswith("tiny loop"):
+            print(line, flush=True)
 
 
 def test_c_program_builds_and_links():
