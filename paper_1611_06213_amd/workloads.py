@@ -146,6 +146,12 @@ CONFIGS = {
         name="mixed", n=200_000_000, learners=32, pushes=400, depth=32, lr=0.001, momentum=0.9,
         grad_dist="normal_heavy", grad_scale=1e-3, grad_dtype=BF16, pull_dtype=BF16,
         arrival="bursts", pulls="all", replicas=32, pool=64, index=4),
+    # one GPU's share of VGG-16 split eight ways by coordinates (a sharded
+    # server applies the same pushes to each contiguous eighth)
+    "vgg16_shard8": Config(
+        name="vgg16_shard8", n=(138_357_544 + 7) // 8, learners=16, pushes=500, depth=32,
+        lr=0.001, momentum=0.9, grad_dist="laplace", grad_scale=1e-3, grad_dtype=F32,
+        pull_dtype=F32, arrival="iid", pulls="all", replicas=16, pool=64, index=5),
 }
 
 
