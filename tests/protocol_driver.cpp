@@ -149,10 +149,15 @@ int main() {
             std::printf("rows %zu %zu %zu %zu", r.head, r.stride, r.span,
                         gadei::velocity_offset(bytes));
         } else if (cmd == "state") {
-            std::printf("state ts=%llu pending=%zu pulls=%llu skipped=%llu",
+            std::printf("state ts=%llu pending=%zu pulls=%llu skipped=%llu smax=%llu ssum=%llu hist=",
                         static_cast<unsigned long long>(p.ts), p.pending(),
                         static_cast<unsigned long long>(p.stats.pulls),
-                        static_cast<unsigned long long>(p.stats.pulls_skipped));
+                        static_cast<unsigned long long>(p.stats.pulls_skipped),
+                        static_cast<unsigned long long>(p.stats.staleness_max),
+                        static_cast<unsigned long long>(p.stats.staleness_sum));
+            for (int b = 0; b < PS_STALENESS_BINS; ++b)
+                if (p.stats.staleness_hist[b])
+                    std::printf("%d:%llu,", b, static_cast<unsigned long long>(p.stats.staleness_hist[b]));
         } else {
             std::fprintf(stderr, "unknown command: %s\n", cmd.c_str());
             return 2;

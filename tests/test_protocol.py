@@ -8,8 +8,8 @@ ABI uses; the same script runs through oracle.server.OracleServer (on a
 one-coordinate model, whose arithmetic is irrelevant here) and the printed
 lines must match exactly: every push status, which learner each applied
 gradient came from and its staleness (Sec. 2.1), the timestamp, which pulls
-write and which are skipped as current (Sec. 4.1), drop counts and error
-codes. Scripts are seeded random mixes of every command."""
+write and which are skipped as current (Sec. 4.1), drop counts, error codes,
+and the staleness statistics (maximum, sum, histogram). Scripts are seeded random mixes of every command."""
 import os
 import shutil
 import subprocess
@@ -92,8 +92,14 @@ def run_oracle(lines):
             o.pull_skip = t[1] != "0"
             out.append("skip")
         elif c == "state":
+            hist = {}
+            for st in o.staleness:
+                b = min(st, 63)
+                hist[b] = hist.get(b, 0) + 1
             out.append(f"state ts={o.ts} pending={o.pending()} pulls={o.pulls} "
-                       f"skipped={o.pulls_skipped}")
+                       f"skipped={o.pulls_skipped} smax={max(o.staleness, default=0)} "
+                       f"ssum={sum(o.staleness)} hist="
+                       + "".join(f"{b}:{hist[b]}," for b in sorted(hist)))
         else:
             raise ValueError(c)
     return out
