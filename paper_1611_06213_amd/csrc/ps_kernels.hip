@@ -366,6 +366,14 @@ __global__ void __launch_bounds__(kBlock) pull_vec(const PullArgs a) {
 // replica) group resident at once, the chip writes one replica stream at a
 // time. Measured best of 4/8/16/32 MiB tiles and 1/2/4/8 chunks per lane for
 // each replica dtype.
+// Blocks are dispatched round-robin over the chip's 8 XCDs (block index mod
+// 8). When a group's block count is a multiple of 8 (every full-size group),
+// block b of the group works on slice (b mod 8) * (bpt / 8) + b / 8, so each
+// XCD writes one contiguous eighth of the tile per replica instead of 4 KiB
+// pieces interleaved with the other seven: fewer pages per XCD and per DRAM
+// row at a time (VGG-16's 16 fp32 replicas: 1.39 ms vs 1.45 ms). The same
+// XCD handles the same eighth for every replica, so its re-reads of the tile
+// stay in its own L2.
 template <int PDT>
 constexpr uint64_t tile_coords() { return uint64_t(4) << 20; }
 template <int PDT>
@@ -376,7 +384,8 @@ template <int PDT, int E>
 __global__ void __launch_bounds__(kBlock) pull_tiled(const PullArgs a, unsigned bpt) {
     constexpr uint64_t kTileChunksE = tile_coords<PDT>() / E;
     const uint64_t chunks = a.n / E;
-    const unsigned b = blockIdx.x % bpt;
+    const unsigned b0 = blockIdx.x % bpt;
+    const unsigned b = (bpt & 7u) == 0 ? (b0 & 7u) * (bpt >> 3) + (b0 >> 3) : b0;
     const unsigned tr = blockIdx.x / bpt;
     const int r = static_cast<int>(tr % static_cast<unsigned>(a.r));
     const uint64_t t = tr / static_cast<unsigned>(a.r);
