@@ -406,6 +406,54 @@ __global__ void __launch_bounds__(kBlock) pull_tiled(const PullArgs a, unsigned 
     }
 }
 
+// The same fan-out on a 3-D grid (x: block within the tile, y: replica, z:
+// tile; dispatch order x fastest, as above). Each tile is cut into 8
+// contiguous slices, whole multiples of kBlock * M chunks (the last slices
+// short or empty for a short tile), and the blocks of XCD x (x = block mod 8,
+// the grid's x extent being a multiple of 8) stride through slice x, M chunks
+// per lane. Unlike pull_tiled's remap this keeps each XCD's writes in one
+// contiguous slice also when a lane takes two chunks, and spreads a short
+// last tile over all 8 XCDs. Used for bf16 replicas (32 Mixed replicas: 2.07-
+// 2.10 ms vs 2.31 ms) and for vectors of fewer than 8 tiles, where the short
+// tile is a large share (Text-CNN's 7 fp32 replicas: 0.045 vs 0.049 ms). For
+// fp32 replicas of many tiles pull_tiled's 1-D grid measured 2% faster.
+template <int PDT, int E, int M>
+__global__ void __launch_bounds__(kBlock) pull_slices(const PullArgs a) {
+    constexpr uint64_t kTileChunksE = tile_coords<PDT>() / E;
+    constexpr uint64_t kSliceUnit = static_cast<uint64_t>(kBlock) * M;
+    const uint64_t chunks = a.n / E;
+    const unsigned b = blockIdx.x;
+    const uint64_t t = blockIdx.z;
+    const uint64_t c0 = t * kTileChunksE;
+    const uint64_t c1 = c0 + kTileChunksE < chunks ? c0 + kTileChunksE : chunks;
+    uint64_t lo = c0, hi = c1, j = b, nj = gridDim.x;
+    if ((gridDim.x & 7u) == 0) {
+        const uint64_t per = (c1 - c0 + 8 * kSliceUnit - 1) / (8 * kSliceUnit) * kSliceUnit;
+        const uint64_t x = b & 7u;
+        lo = c0 + x * per < c1 ? c0 + x * per : c1;
+        hi = lo + per < c1 ? lo + per : c1;
+        j = b >> 3;
+        nj = gridDim.x >> 3;
+    }
+    void *d = a.dst[blockIdx.y];
+    const uint64_t step = nj * kBlock;
+    for (uint64_t base = lo + j * kBlock + threadIdx.x; base < hi; base += M * step) {
+        float w[M][E];
+#pragma unroll
+        for (int i = 0; i < M; ++i)
+            if (base + i * step < hi) ld_f32<E, false>(w[i], a.w + (base + i * step) * E);
+#pragma unroll
+        for (int i = 0; i < M; ++i)
+            if (base + i * step < hi) st_dst<PDT, E>(d, (base + i * step) * E, w[i]);
+    }
+    if (t == 0 && b == 0 && threadIdx.x < a.n - chunks * E) {
+        const uint64_t i = chunks * E + threadIdx.x;
+        float w[1];
+        ld_f32<1, false>(w, a.w + i);
+        st_dst<PDT, 1>(d, i, w);
+    }
+}
+
 // Scalar path for replicas without vector alignment.
 template <int PDT>
 __global__ void __launch_bounds__(kBlock) pull_scalar(const PullArgs a) {
@@ -514,6 +562,20 @@ void go_pull_tiled(const PullArgs &a, const Geometry &geo, hipStream_t s) {
     uint64_t bpt = (per_tile + lane_chunks<PDT>() * kBlock - 1) / (lane_chunks<PDT>() * kBlock);
     if (bpt < 1) bpt = 1;
     if (bpt > kTileBlocks) bpt = kTileBlocks;
+    if (PDT == PS_BF16 || tiles < 8) {
+        // pull_slices: x extent a multiple of 8 once there are more than 8 blocks
+        constexpr uint64_t M = lane_chunks<PDT>();
+        uint64_t bx = (per_tile + M * kBlock - 1) / (M * kBlock);
+        if (bx < 1) bx = 1;
+        if (bx > 8) bx = (bx + 7) / 8 * 8;
+        if (tiles <= 65535 && bx * tiles * static_cast<uint64_t>(a.r) <= kMaxBlocks) {
+            hipLaunchKernelGGL((pull_slices<PDT, E, static_cast<int>(M)>),
+                               dim3(static_cast<unsigned>(bx), static_cast<unsigned>(a.r),
+                                    static_cast<unsigned>(tiles)),
+                               dim3(kBlock), 0, s, a);
+            return;
+        }
+    }
     const uint64_t groups = tiles * static_cast<uint64_t>(a.r);
     if (groups * bpt > kMaxBlocks) bpt = kMaxBlocks / groups;   // lanes stride further
     if (bpt < 1) {
