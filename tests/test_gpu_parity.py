@@ -259,9 +259,9 @@ def test_misaligned_buffers_scalar_path(torch, og, od):
 
 @pytest.mark.parametrize("r", [2, 3, 16, 64])
 def test_tiled_pull_many_tiles_ragged(torch, r):
-    """The tiled fan-out over several full tiles (8 MiB of replica data each:
-    2 Mi coordinates for fp32, 4 Mi for bf16), a partial tile and a ragged
-    tail: every replica equals w (fp32) or RNE(w) (bf16)."""
+    """The tiled fan-out over two full tiles (4 Mi coordinates each), a
+    partial tile and a ragged tail: every replica equals w (fp32) or RNE(w)
+    (bf16)."""
     n = 2 * (4 << 20) + 1234567 + 3
     gen = torch.Generator(device="cuda")
     gen.manual_seed(r)
@@ -277,6 +277,33 @@ def test_tiled_pull_many_tiles_ragged(torch, r):
         want = w_host if dt == ps.PS_F32 else orc.f32_to_bf16(w_host)
         for j in range(r):
             assert parity.bitwise(parity.np_bits(reps[j]), want), (dt, j)
+        del reps
+    srv.close()
+
+
+@pytest.mark.parametrize("n,r", [
+    (7 * (4 << 20) - 3, 2),      # 7 tiles: the sliced 3-D fan-out for fp32 too
+    (7 * (4 << 20) + 5, 5),      # 8 tiles, the last of one chunk plus a 1-value tail: 1-D fan-out for fp32
+    (9 * (4 << 20) + 4097 * 4 + 2, 3),   # 10 tiles, the last short
+])
+def test_pull_paths_every_element(torch, n, r):
+    """Both tiled fan-outs (1-D for fp32 replicas of 8 tiles or more, sliced
+    3-D otherwise and for bf16) write every element of every replica exactly
+    as w (fp32) or RNE(w) (bf16): replicas start as a NaN sentinel and are
+    compared whole, bitwise, against the oracle's copy."""
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(n % 1000 + r)
+    w0 = (torch.rand(n, generator=gen, device="cuda") - 0.5) * 0.1
+    srv = ps.ParameterServer(n, 0.01, 0.0, queue_depth=1)
+    srv.set_weights(w0)
+    w_host = parity.np_bits(w0)
+    for dt, tdt in ((ps.PS_F32, torch.float32), (ps.PS_BF16, torch.bfloat16)):
+        reps = [torch.full((n,), float("nan"), dtype=tdt, device="cuda") for _ in range(r)]
+        srv.pull_many(list(range(r)), reps)
+        srv.sync()
+        want = w_host if dt == ps.PS_F32 else orc.f32_to_bf16(w_host)
+        for j in range(r):
+            assert parity.bitwise(parity.np_bits(reps[j]), want), (n, r, dt, j)
         del reps
     srv.close()
 
