@@ -6,8 +6,8 @@
 // 16-byte chunks (4 fp32 or 8 bf16 values; narrower only for misaligned
 // buffers), that enough loads are in flight, that nothing is re-read, and
 // which coordinates the resident blocks work on at the same time (the DRAM
-// serves some access patterns faster than others: see front_block and
-// pull_tiled).
+// serves some access patterns faster than others: see front_block,
+// pull_tiled and pull_slices).
 //
 // apply:  for each coordinate i and each pending gradient k = 0..K-1, oldest
 //         first, one ASGD step (Eq. "asgd" with the step of Eq. "gd"):
@@ -21,8 +21,9 @@
 //         per coordinate in push order, divided by K, applied as one step.
 // pull:   write w to R replica buffers (fp32, or bf16 rounded to nearest
 //         even). One replica: a streaming copy. Several: a tiled fan-out that
-//         keeps each tile of w in the memory-side cache while the replicas
-//         are written one after another (see pull_tiled).
+//         keeps each tile of w in cache while the replicas are written one
+//         after another, each XCD writing its own contiguous slice of the
+//         tile (see pull_tiled and pull_slices).
 //
 // Every product and sum is rounded on its own (no fused multiply-add), so
 // the result is bit-identical to sequential binary32 steps. Built with
