@@ -305,13 +305,17 @@ class ParameterServer:
 
     Pushed gradients are borrowed: the tensor is kept referenced until the
     apply that consumes it has been enqueued, and the caller must not write it
-    before that apply has run on the server's stream."""
+    before that apply has run on the server's stream. Gradients and replicas
+    are marked as used on the torch streams given to set_stream and
+    set_pull_stream (Tensor.record_stream), so a tensor the caller frees is not
+    reused by torch's allocator before the server's kernels on it have run."""
 
     def __init__(self, n_params: int, lr: float, momentum: float = 0.0,
                  queue_depth: Optional[int] = None, stream=None):
         self.h = ps_create(n_params, lr, momentum)
         self.n = n_params
         self._pending = []
+        self._streams = []   # torch streams the device work may run on (set_stream, set_pull_stream)
         if queue_depth is not None:
             self._check(ps_set_queue_depth(self.h, queue_depth), "set_queue_depth")
         if stream is not None:
@@ -339,9 +343,21 @@ class ParameterServer:
         except Exception:
             pass
 
+    def _track(self, stream) -> None:
+        if stream is not None and not isinstance(stream, int) and stream not in self._streams:
+            self._streams.append(stream)
+
+    def _uses(self, t) -> None:
+        """Tell torch's caching allocator that the server's streams use `t`,
+        so that freeing the tensor does not hand its memory to a new tensor
+        before the kernels enqueued there have run."""
+        for st in self._streams:
+            t.record_stream(st)
+
     def set_stream(self, stream) -> None:
         ptr = stream if isinstance(stream, int) else stream.cuda_stream
         self._check(ps_set_stream(self.h, ptr), "set_stream")
+        self._track(stream)
 
     def set_weights(self, w0) -> None:
         self._check(ps_set_weights(self.h, self._tensor(w0, "set_weights")), "set_weights")
@@ -370,6 +386,7 @@ class ParameterServer:
         if rc == PS_EFULL:
             return False
         self._check(rc, "push")
+        self._uses(grad)
         self._pending.append(grad)
         return True
 
@@ -381,6 +398,7 @@ class ParameterServer:
         if rc == PS_EFULL:
             return False
         self._check(rc, "push_async")
+        self._uses(grad)
         self._pending.append((grad, ready_event))
         return True
 
@@ -395,6 +413,7 @@ class ParameterServer:
     def set_pull_stream(self, stream) -> None:
         ptr = 0 if stream is None else (stream if isinstance(stream, int) else stream.cuda_stream)
         self._check(ps_set_pull_stream(self.h, ptr), "set_pull_stream")
+        self._track(stream)
 
     def apply_pending(self) -> None:
         self._check(ps_apply_pending(self.h), "apply_pending")
@@ -414,7 +433,10 @@ class ParameterServer:
         codes = {_dtype_code(d) for d in dsts}
         if len(codes) > 1:
             raise ValueError(f"{what}: all replicas of one call must share a dtype")
-        return [self._tensor(d, what) for d in dsts], (codes.pop() if codes else PS_F32)
+        ptrs = [self._tensor(d, what) for d in dsts]
+        for d in dsts:
+            self._uses(d)
+        return ptrs, (codes.pop() if codes else PS_F32)
 
     def pull_many(self, learners: Sequence[int], dsts) -> None:
         ptrs, dt = self._replicas(learners, dsts, "pull_many")

@@ -870,6 +870,41 @@ def test_push_async_waits_for_producer_stream(torch):
     srv.close()
 
 
+def test_binding_freed_gradients_not_reused_before_apply(torch):
+    """The binding marks pushed gradients as used on the server's stream: a
+    caller that frees its gradient tensors right after apply_pending, while
+    the apply still runs on a side stream, does not get their memory back
+    from torch's allocator for a new tensor (whose writes would race the
+    apply). The weights then match the oracle bitwise."""
+    n, k = 1 << 24, 32
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(51)
+    w0 = (torch.rand(n, generator=gen, device="cuda") - 0.5) * 0.1
+    grads = [torch.randn(n, generator=gen, device="cuda") * 1e-3 for _ in range(k)]
+    host = [parity.np_bits(g) for g in grads]
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    srv = ps.ParameterServer(n, 0.01, 0.9, queue_depth=k, stream=side)
+    srv.set_weights(w0)
+    for j, g in enumerate(grads):
+        assert srv.push(j % 8, g)
+    srv.apply_pending()
+    old = {g.data_ptr() for g in grads}
+    del g
+    grads.clear()
+    fresh = [torch.empty(n, device="cuda") for _ in range(4)]
+    for t in fresh:
+        t.fill_(1e30)                     # on the current stream, at once
+    assert not old & {t.data_ptr() for t in fresh}
+    w = parity.np_bits(srv.weights_copy())
+    o = orc.OracleServer(parity.np_bits(w0), 0.01, 0.9, depth=k)
+    for j in range(k):
+        o.push(j % 8, host[j])
+    o.apply_pending()
+    assert parity.bitwise(w, o.w)
+    srv.close()
+
+
 def test_record_lets_producer_reuse_its_buffer(torch):
     """After ps_record, a producer stream that waits for the event may
     overwrite the gradient buffer; the apply already read the old values."""
