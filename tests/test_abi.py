@@ -104,6 +104,7 @@ def test_binding_refuses_mixed_replica_dtypes():
     srv = ps.ParameterServer.__new__(ps.ParameterServer)
     srv.n = 4
     srv.h = 0
+    srv._streams = []
 
     class FakeDev:
         def __init__(self, dtype):
