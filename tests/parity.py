@@ -43,12 +43,16 @@ def pull_rounds(learners: Sequence[int]) -> List[List[int]]:
 
 def gpu_replay(cfg: wl.Config, events, pool, w0, ranges: Sequence[Tuple[int, int]],
                fused: bool = False, pull_skip: bool = True, stream=None, fusion=None,
-               replicas=None):
+               replicas=None, round_robin: bool = False):
     """fused: drive apply+pull through ps_apply_pull; fusion: the replica
     count up to which that call writes replicas from the apply pass;
-    replicas: the replica tensors (default: workloads.Rows)."""
+    replicas: the replica tensors (default: workloads.Rows); round_robin:
+    per-learner queues of `depth` slots served round-robin (as bench.py
+    --queue rr sets them)."""
     import torch
     srv = ps.ParameterServer(cfg.n, cfg.lr, cfg.momentum, queue_depth=cfg.depth)
+    if round_robin:
+        srv.set_queue_mode(ps.PS_QUEUE_ROUND_ROBIN, cfg.depth)
     srv.set_pull_skip(pull_skip)
     if fusion is not None:
         srv.set_pull_fusion(fusion)
@@ -118,12 +122,15 @@ def gpu_replay(cfg: wl.Config, events, pool, w0, ranges: Sequence[Tuple[int, int
     return out
 
 
-def oracle_replay(cfg: wl.Config, events, pool_slices, w0_slices, ranges, pull_skip: bool = True):
+def oracle_replay(cfg: wl.Config, events, pool_slices, w0_slices, ranges, pull_skip: bool = True,
+                  round_robin: bool = False):
     """pool_slices[r][buf] is pool buffer `buf` restricted to range r."""
     per_range = []
     for r, (lo, hi) in enumerate(ranges):
         s = orc.OracleServer(w0_slices[r], cfg.lr, cfg.momentum, depth=cfg.depth,
                              pull_skip=pull_skip)
+        if round_robin:
+            assert s.set_queue_mode(orc.ROUND_ROBIN, cfg.depth) == orc.OK
         snaps = []
 
         def on_pull(learners, srv, snaps=snaps):
@@ -151,7 +158,7 @@ def oracle_replay(cfg: wl.Config, events, pool_slices, w0_slices, ranges, pull_s
                   for k in range(len(per_range[0][1]))],
         "staleness": s0.staleness,
         "ts": s0.ts,
-        "counts": (s0.ts + len(s0.queue), s0.ts, s0.pulls, s0.pulls_skipped),
+        "counts": (s0.ts + s0.pending(), s0.ts, s0.pulls, s0.pulls_skipped),
     }
 
 

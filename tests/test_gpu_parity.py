@@ -143,6 +143,31 @@ def test_vgg16_full_size_bench_layouts(torch, layout):
     assert parity.compare(g, o, ranges) == []
 
 
+def test_vgg16_full_size_round_robin_sampled(torch):
+    """VGG-16 at full size with per-learner queues served round-robin, as
+    bench.py --queue rr runs it (K slots per learner, applies of K gradients
+    in service order): sampled ranges of w, v and every replica, the
+    staleness of every applied gradient and the counters against the
+    oracle in the same mode."""
+    cfg = wl.CONFIGS["vgg16"]
+    say("[full] vgg16 round-robin")
+    ev = wl.schedule(cfg)
+    pool = wl.make_pool(cfg, "cuda")
+    w0 = wl.make_w0(cfg, "cuda")
+    ranges = _full_ranges(cfg)
+    g = parity.gpu_replay(cfg, ev, pool, w0, ranges, round_robin=True)
+    ps_, w0s = parity.host_inputs(cfg, pool, w0, ranges)
+    del pool
+    free(torch)
+    o = parity.oracle_replay(cfg, ev, ps_, w0s, ranges, round_robin=True)
+    assert parity.compare(g, o, ranges) == []
+    # the service order differs from FIFO: the same gradients folded in
+    # another order round differently (every learner pulls after every apply,
+    # so the staleness sequence is the same in both modes)
+    fifo = parity.oracle_replay(cfg, ev, ps_, w0s, ranges[:1])
+    assert not parity.bitwise(fifo["w"][0], o["w"][0])
+
+
 def test_mixed_bf16_quantisation_bound_vs_fp32_gradients(torch):
     """The bf16-gradient run against the oracle fed the original fp32
     gradients x (before rounding to bf16). Each push k changes the gradient
