@@ -213,6 +213,52 @@ def copy_ceiling(torch, ps, lib, n: int = 1 << 28, reps: int = 10):
     return 8 * n / (ms * 1e-3) / 1e9
 
 
+class HipEvents:
+    """Timing events recorded with the HIP runtime the library is bound to.
+
+    The same HIP events torch.cuda.Event wraps, recorded through ctypes: a
+    record costs about a microsecond of host time instead of several, which
+    matters for the launch-bound workloads (Tiny), where the host loop
+    otherwise sets the pace."""
+
+    def __init__(self, lib, count: int):
+        import ctypes
+        self._c = ctypes
+        self._rec = lib.hipEventRecord
+        self._rec.restype = ctypes.c_int
+        self._rec.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        self._elapsed = lib.hipEventElapsedTime
+        self._elapsed.restype = ctypes.c_int
+        self._elapsed.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+        self._destroy = lib.hipEventDestroy
+        self._destroy.restype = ctypes.c_int
+        self._destroy.argtypes = [ctypes.c_void_p]
+        create = lib.hipEventCreate
+        create.restype = ctypes.c_int
+        create.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.ev = []
+        for _ in range(count):
+            e = ctypes.c_void_p()
+            if create(ctypes.byref(e)) != 0:
+                raise RuntimeError("hipEventCreate failed")
+            self.ev.append(e.value)
+
+    def record(self, i: int, stream_ptr: int) -> None:
+        if self._rec(self.ev[i], stream_ptr) != 0:
+            raise RuntimeError("hipEventRecord failed")
+
+    def ms(self, i: int, j: int) -> float:
+        out = self._c.c_float()
+        if self._elapsed(self._c.byref(out), self.ev[i], self.ev[j]) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return out.value
+
+    def close(self) -> None:
+        for e in self.ev:
+            self._destroy(e)
+        self.ev = []
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -309,28 +355,34 @@ def main():
     push = lib.ps_push_dtype
     it = 0
 
-    def step(ev=None):
+    sptr = stream.cuda_stream
+    pptr = pstream.cuda_stream if pstream is not None else sptr
+
+    # events of step s: 4s = before the apply, 4s+1 = after it (both on the
+    # library's stream), 4s+2 / 4s+3 = around the pull on the stream it runs
+    # on (with ordered pulls the same point as 4s+1, so 4s+1 serves as both)
+    def step(s_=None):
         nonlocal it
         pushes_b, r, ids, dptr = calls[it % len(calls)]
         it += 1
         for l, g in pushes_b:
             if push(h, l, g, gdt) != 0:
                 raise RuntimeError(ps.ps_last_error())
-        if ev is not None:
-            ev[0].record(stream)
+        if s_ is not None:
+            evs.record(4 * s_, sptr)
         if args.mode == "fused":
             rc = lib.ps_apply_pull(h, r, ids, dptr, pdt)
-            if ev is not None:
-                ev[1].record(stream)
+            if s_ is not None:
+                evs.record(4 * s_ + 1, sptr)
         else:
             rc = lib.ps_apply_sync(h) if args.apply == "sync" else lib.ps_apply_pending(h)
-            ps_ = pstream if pstream is not None else stream
-            if ev is not None:
-                ev[1].record(stream)
-                ev[2].record(ps_)
+            if s_ is not None:
+                evs.record(4 * s_ + 1, sptr)
+                if pstream is not None:
+                    evs.record(4 * s_ + 2, pptr)
             rc = rc or lib.ps_pull_many(h, r, ids, dptr, pdt)
-            if ev is not None:
-                ev[3].record(ps_)
+            if s_ is not None:
+                evs.record(4 * s_ + 3, pptr)
         if rc != 0:
             raise RuntimeError(ps.ps_last_error())
         return r
@@ -339,12 +391,12 @@ def main():
         step()
     torch.cuda.synchronize()
 
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    evs = HipEvents(lib, 4 * args.steps)
     rs = []
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s_ in range(args.steps):
-        rs.append(step(evs[s_]))
+        rs.append(step(s_))
     torch.cuda.synchronize()
     t1 = time.perf_counter()
 
@@ -352,10 +404,13 @@ def main():
     pushes = K * args.steps
     step_bytes = sum(algorithmic_bytes(cfg, args.mode, r)[0] for r in rs)
     launch_bytes = sum(algorithmic_bytes(cfg, args.mode, r)[1] for r in rs) / args.steps
-    k_each = sorted(e[0].elapsed_time(e[1]) for e in evs)
+    k_each = sorted(evs.ms(4 * s_, 4 * s_ + 1) for s_ in range(args.steps))
     k_ms = sum(k_each) / args.steps
-    p_each = sorted(e[2].elapsed_time(e[3]) for e in evs) if args.mode != "fused" else [0.0]
+    p0 = 2 if pstream is not None else 1
+    p_each = (sorted(evs.ms(4 * s_ + p0, 4 * s_ + 3) for s_ in range(args.steps))
+              if args.mode != "fused" else [0.0])
     p_ms = sum(p_each) / len(p_each)
+    evs.close()
     gbps = step_bytes / elapsed / 1e9
     achieved = launch_bytes / (k_ms * 1e-3) / 1e9
     label = (f"{args.config}-{args.mode}" + ("-sync" if args.apply == "sync" else "")
