@@ -909,6 +909,8 @@ def test_binding_freed_gradients_not_reused_before_apply(torch):
     host = [parity.np_bits(g) for g in grads]
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        torch.cuda._sleep(50_000_000)     # ~20 ms: the apply is still queued when the host allocates
     srv = ps.ParameterServer(n, 0.01, 0.9, queue_depth=k, stream=side)
     srv.set_weights(w0)
     for j, g in enumerate(grads):
