@@ -489,14 +489,17 @@ hipError_t go_apply(const ApplyArgs &a, int level, const Geometry &geo, hipStrea
     // bf16 gradients move 16 bytes per lane as 8 values when every buffer is
     // 16-byte aligned; otherwise (and for fp32) a lane's chunk is 4 values.
     const bool e8 = GDT == PS_BF16 && level == 2;
-    // fp32 gradients: with many gradients per apply each lane keeps >= 16
-    // loads of 16 bytes in flight; one block per CU then saturates HBM, and
-    // fewer resident waves keep fewer DRAM pages and translations live at
-    // once across the K+2 streams, which measured faster and steadier. The
-    // kernel uses no LDS: the reservation only limits residency. bf16
-    // gradients (half the bytes per value) measured best at full residency.
+    // fp32 gradients with momentum: with many gradients per apply each lane
+    // keeps >= 16 loads of 16 bytes in flight; one block per CU then
+    // saturates HBM, and fewer resident waves keep fewer DRAM pages and
+    // translations live at once across the K+2 streams, which measured
+    // faster and steadier (VGG-16 shape, K = 32: 3.24 vs 3.55 ms). The kernel
+    // uses no LDS: the reservation only limits residency. Without momentum
+    // the same cap measured slower (K = 16 / 32 / 64: 2.01 / 3.60 / 6.66 ms
+    // capped vs 1.72 / 3.28 / 6.20 ms at full residency), and bf16 gradients
+    // (half the bytes per value) measured best at full residency too.
     const unsigned lds =
-        (GDT == PS_F32 && a.k >= geo.occupancy_cap_min_k) ? geo.occupancy_cap_lds : 0;
+        (GDT == PS_F32 && MOM && a.k >= geo.occupancy_cap_min_k) ? geo.occupancy_cap_lds : 0;
     if constexpr (GDT == PS_BF16) {
         if (e8) {
             hipLaunchKernelGGL((apply_vec<MOM, GDT, PDT, 8>), dim3(grid_for(a.n / 8, geo)),

@@ -268,6 +268,7 @@ def test_edge_sizes(torch, n):
 @pytest.mark.parametrize("k", list(range(1, 18)) + [23, 31, 32, 33, 40, 47, 48, 63, 64])
 def test_edge_queue_depths(torch, k):
     _run_edge(torch, 10007, k, 0.9, ps.PS_F32, ps.PS_F32, seed=k)
+    _run_edge(torch, 10007, k, 0.0, ps.PS_F32, ps.PS_F32, seed=k + 100)
     _run_edge(torch, 10007, k, 0.0, ps.PS_BF16, ps.PS_BF16, seed=k, fusion=2)
 
 
