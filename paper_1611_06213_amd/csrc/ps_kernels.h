@@ -34,19 +34,27 @@ struct PullArgs {
 
 // Launch geometry: blocks are 256 threads; max_blocks caps the grid (the
 // kernels then stride over the remaining chunks). 0 = one chunk per lane.
-// Applies of at least occupancy_cap_min_k gradients reserve
-// occupancy_cap_lds bytes of LDS per block (0 = none), chosen at server
-// creation so that one block fits per compute unit.
+// fp32-gradient kernels reserve LDS so that only a few blocks fit per
+// compute unit: occupancy_cap_lds leaves room for one, occupancy_cap2_lds
+// for two (0 = no reservation; both chosen at server creation for the
+// current device). Asynchronous applies take two blocks per CU from
+// occupancy_cap2_min_k gradients on, one from occupancy_cap_min_k_momentum
+// on when they carry momentum; synchronous steps take one from
+// occupancy_cap_min_k on.
 struct Geometry {
     int max_blocks = 0;
     int fronts_log2 = -1;   // -1: chosen per apply (fronts_log2_for, ps_layout.h)
     unsigned occupancy_cap_lds = 0;
+    unsigned occupancy_cap2_lds = 0;
     int occupancy_cap_min_k = 16;
+    int occupancy_cap2_min_k = 8;
+    int occupancy_cap_min_k_momentum = 24;
 };
 
-// LDS bytes that leave room for exactly one block per compute unit on the
-// current device, or 0 if the device does not allow such a reservation.
-unsigned one_block_per_cu_lds();
+// LDS bytes that leave room for exactly `blocks` (1 or 2) blocks per compute
+// unit on the current device, or 0 if the device does not allow such a
+// reservation.
+unsigned blocks_per_cu_lds(int blocks);
 
 
 // grad_dtype: PS_F32 | PS_BF16. pull_dtype: -1 (no replicas), PS_F32, PS_BF16.

@@ -489,17 +489,23 @@ hipError_t go_apply(const ApplyArgs &a, int level, const Geometry &geo, hipStrea
     // bf16 gradients move 16 bytes per lane as 8 values when every buffer is
     // 16-byte aligned; otherwise (and for fp32) a lane's chunk is 4 values.
     const bool e8 = GDT == PS_BF16 && level == 2;
-    // fp32 gradients with momentum: with many gradients per apply each lane
-    // keeps >= 16 loads of 16 bytes in flight; one block per CU then
-    // saturates HBM, and fewer resident waves keep fewer DRAM pages and
-    // translations live at once across the K+2 streams, which measured
-    // faster and steadier (VGG-16 shape, K = 32: 3.24 vs 3.55 ms). The kernel
-    // uses no LDS: the reservation only limits residency. Without momentum
-    // the same cap measured slower (K = 16 / 32 / 64: 2.01 / 3.60 / 6.66 ms
-    // capped vs 1.72 / 3.28 / 6.20 ms at full residency), and bf16 gradients
-    // (half the bytes per value) measured best at full residency too.
-    const unsigned lds =
-        (GDT == PS_F32 && MOM && a.k >= geo.occupancy_cap_min_k) ? geo.occupancy_cap_lds : 0;
+    // fp32 gradients: with 8 or more gradients per apply each lane keeps
+    // many 16-byte loads in flight; a few blocks per CU then saturate HBM,
+    // and fewer resident waves keep fewer DRAM pages and translations live
+    // at once across the K+2 streams, which measured faster and steadier.
+    // The kernel uses no LDS: the reservation only limits residency.
+    // Measured at the VGG-16 size: two blocks per CU from K = 8, one from
+    // K = 24 with momentum (K = 32: one block 3.24 ms, two 3.36, full
+    // residency 3.55; K = 12: two blocks 1.41 ms, one 1.70, full 1.51-1.52;
+    // without momentum K = 32: two blocks 3.06 ms, one 3.60, full
+    // 3.19-3.28; K = 8: two blocks 0.88 ms, full 0.92-0.95). Below K = 8
+    // full residency was best. bf16 gradients (half the bytes per value)
+    // measured best at full residency.
+    unsigned lds = 0;
+    if constexpr (GDT == PS_F32) {
+        if (a.k >= geo.occupancy_cap2_min_k) lds = geo.occupancy_cap2_lds;
+        if (MOM && a.k >= geo.occupancy_cap_min_k_momentum) lds = geo.occupancy_cap_lds;
+    }
     if constexpr (GDT == PS_BF16) {
         if (e8) {
             hipLaunchKernelGGL((apply_vec<MOM, GDT, PDT, 8>), dim3(grid_for(a.n / 8, geo)),
@@ -621,15 +627,17 @@ hipError_t launch_pull(const PullArgs &a, int pull_dtype, int level, const Geome
     return hipGetLastError();
 }
 
-unsigned one_block_per_cu_lds() {
+unsigned blocks_per_cu_lds(int blocks) {
     int dev = 0, per_cu = 0, per_block = 0;
+    if (blocks < 1) return 0;
     if (hipGetDevice(&dev) != hipSuccess) return 0;
     if (hipDeviceGetAttribute(&per_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) !=
             hipSuccess ||
         hipDeviceGetAttribute(&per_block, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) !=
             hipSuccess)
         return 0;
-    const unsigned want = static_cast<unsigned>(per_cu) / 2 + 1024;   // two blocks cannot fit
+    // `blocks` reservations fit, one more does not
+    const unsigned want = static_cast<unsigned>(per_cu) / static_cast<unsigned>(blocks + 1) + 1024;
     return want <= static_cast<unsigned>(per_block) ? want : 0;
 }
 

@@ -286,7 +286,8 @@ ps_server *ps_create(size_t n_params, float lr, float momentum) {
         delete ps;
         return nullptr;
     }
-    ps->geo.occupancy_cap_lds = gadei::one_block_per_cu_lds();
+    ps->geo.occupancy_cap_lds = gadei::blocks_per_cu_lds(1);
+    ps->geo.occupancy_cap2_lds = gadei::blocks_per_cu_lds(2);
     return ps;
 }
 
