@@ -55,6 +55,9 @@ namespace {
 
 constexpr int kBlock = PS_BLOCK;      // threads per block (waves of 64 lanes)
 constexpr int kGroup = PS_GROUP;      // gradients whose loads are issued together
+// apply_chunk and sync_chunk take full groups of kGroup, then one of 8, then
+// a predicated group of at most 7: that covers every K only for kGroup <= 16.
+static_assert(kGroup >= 1 && kGroup <= 16, "gradient group size must be 1..16");
 // w and v are read once and written once per launch and are not touched
 // again until the next apply, after tens of GB of other traffic: stream them
 // with the non-temporal hint too.
