@@ -297,6 +297,7 @@ def main():
     from paper_1611_06213_amd import ps
     from paper_1611_06213_amd import workloads as wl
     from paper_1611_06213_amd.accounting import learner_ps_bytes_per_push
+    from paper_1611_06213_amd.accounting import pull_bytes as pull_bytes_of
 
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
@@ -438,7 +439,7 @@ def main():
     kern = ("ps_apply_pull (apply + pull kernels)" if args.mode == "fused"
             else "sync_vec (synchronous step)" if args.apply == "sync"
             else "apply_vec (fused K-gradient apply)")
-    pull_bytes = sum(r * n * (2 if pdt == wl.BF16 else 4) + 4 * n for r in rs) / args.steps
+    pull_bytes = sum(pull_bytes_of(n, r, 2 if pdt == wl.BF16 else 4) for r in rs) / args.steps
     out = {
         "metric": METRIC,
         "value": round(pushes / elapsed, 2),

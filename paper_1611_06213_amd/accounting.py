@@ -31,5 +31,8 @@ def apply_bytes(n: int, k: int, grad_bytes: int, momentum: bool) -> int:
 
 def pull_bytes(n: int, r: int, replica_bytes: int, separate: bool = True) -> int:
     """HBM bytes of writing r replicas: r writes, plus one read of w when the
-    pull is its own kernel (a fused pull reuses the apply's registers)."""
+    pull is its own kernel (a fused pull reuses the apply's registers). No
+    replica, no kernel: 0."""
+    if r <= 0:
+        return 0
     return r * n * replica_bytes + (4 * n if separate else 0)

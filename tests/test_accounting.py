@@ -59,5 +59,6 @@ def test_byte_formulas():
     assert acc.apply_bytes(n, 32, 4, True) == 19_923_486_336
     assert acc.pull_bytes(n, 16, 4) == 9_408_312_992
     assert acc.pull_bytes(n, 16, 4, separate=False) == 16 * 4 * n
+    assert acc.pull_bytes(n, 0, 4) == 0            # no replica: no pull kernel, no read of w
     assert acc.apply_bytes(200_000_000, 32, 2, True) == 16_000_000_000
     assert acc.learner_ps_bytes_per_push(n) == 8 * n
