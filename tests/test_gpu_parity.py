@@ -334,6 +334,25 @@ def test_pull_paths_every_element(torch, n, r):
     srv.close()
 
 
+@pytest.mark.parametrize("n", [5, 4096 * 256 + 3, 10_000_019])
+def test_single_replica_pull_every_element(torch, n):
+    """One replica per call takes the streaming copy (pull_vec) for both
+    replica dtypes: every element equals w (fp32) or RNE(w) (bf16), tail
+    included, against the oracle's copy."""
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(n % 997)
+    w0 = (torch.rand(n, generator=gen, device="cuda") - 0.5) * 0.1
+    srv = ps.ParameterServer(n, 0.01, 0.0, queue_depth=1)
+    srv.set_weights(w0)
+    w_host = parity.np_bits(w0)
+    for tdt, want in ((torch.float32, w_host), (torch.bfloat16, orc.f32_to_bf16(w_host))):
+        dst = torch.full((n,), float("nan"), dtype=tdt, device="cuda")
+        srv.pull_many([0], [dst])
+        srv.sync()
+        assert parity.bitwise(parity.np_bits(dst), want), (n, tdt)
+    srv.close()
+
+
 def test_lr_zero_and_zero_gradient(torch):
     n = 5000
     w0 = torch.linspace(-0.05, 0.05, n, device="cuda")
