@@ -360,7 +360,12 @@ class ParameterServer:
         self._track(stream)
 
     def set_weights(self, w0) -> None:
+        """Copy w0 (fp32, n values, on the device) into w on the server's
+        stream; v restarts at zero."""
+        if _dtype_code(w0) != PS_F32:
+            raise TypeError(f"set_weights: need float32 weights, got {w0.dtype}")
         self._check(ps_set_weights(self.h, self._tensor(w0, "set_weights")), "set_weights")
+        self._uses(w0)
 
     def set_fronts(self, fronts_log2: int) -> None:
         self._check(ps_set_fronts(self.h, fronts_log2), "set_fronts")

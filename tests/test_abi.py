@@ -124,3 +124,29 @@ def test_binding_refuses_mixed_replica_dtypes():
         srv._replicas([0, 1], [FakeDev(torch.float32), FakeDev(torch.bfloat16)], "pull_many")
     ptrs, dt = srv._replicas([0, 1], [FakeDev(torch.bfloat16)] * 2, "pull_many")
     assert dt == ps.PS_BF16 and ptrs == [4096, 4096]
+
+
+def test_binding_refuses_non_fp32_weights():
+    """ps_set_weights copies n fp32 values: a bf16 tensor of n elements holds
+    half as many bytes, so the binding must refuse it before the call."""
+    import torch
+    srv = ps.ParameterServer.__new__(ps.ParameterServer)
+    srv.n = 4
+    srv.h = 0
+    srv._streams = []
+
+    class FakeDev:
+        dtype = torch.bfloat16
+        is_cuda = True
+
+        def is_contiguous(self):
+            return True
+
+        def numel(self):
+            return 4
+
+        def data_ptr(self):
+            return 4096
+
+    with pytest.raises(TypeError, match="float32"):
+        srv.set_weights(FakeDev())
