@@ -353,6 +353,115 @@ def test_single_replica_pull_every_element(torch, n):
     srv.close()
 
 
+def _f32_rounding_probes(n_random, seed, nan=True):
+    """fp32 bit patterns that probe rounding to bf16: ties that stay and ties
+    that carry, just below and above one half, carries into the exponent and
+    to infinity, subnormals, signed zeros, infinities and (with nan) NaNs of
+    both kinds and signs; then random patterns over the whole 32-bit range."""
+    hand = [0x00000000, 0x80000000, 0x00000001, 0x80000001, 0x00007FFF, 0x00008000,
+            0x00008001, 0x00018000, 0x0000FFFF, 0x007F8000, 0x007FFFFF, 0x80FF8000,
+            0x00800000, 0x3F808000, 0x3F818000, 0x3F807FFF, 0x3F808001, 0xBF818000,
+            0x3FFF8000, 0x7F7F7FFF, 0x7F7F8000, 0x7F7EFFFF, 0x7F7FFFFF, 0xFF7FFFFF,
+            0x7F800000, 0xFF800000]
+    nans = [0x7F800001, 0x7F80FFFF, 0x7FBFFFFF, 0x7FC00000, 0x7FFFFFFF, 0xFFC00001,
+            0xFF800001, 0xFFFFFFFF]
+    bits = np.array(hand + (nans if nan else []), dtype=np.uint32)
+    rnd = np.random.default_rng(seed).integers(0, 1 << 32, size=n_random, dtype=np.uint64)
+    rnd = rnd.astype(np.uint32)
+    if not nan:
+        rnd = rnd[(rnd & 0x7FFFFFFF) <= 0x7F800000]
+    return np.concatenate([bits, rnd])
+
+
+def _device_f32(torch, bits):
+    return torch.from_numpy(bits.view(np.int32).copy()).to("cuda").view(torch.float32)
+
+
+@pytest.mark.parametrize("r,offset", [(1, 0), (3, 0), (3, 4), (3, 1), (1, 1)],
+                         ids=["vec", "slices-8", "slices-4", "scalar", "vec-scalar"])
+def test_bf16_replica_rounding_special_values(torch, r, offset):
+    """Every pull kernel rounds to bf16 as the oracle does: one replica (the
+    streaming copy), several (the sliced fan-out, 8 values per lane, or 4 for
+    8-byte-aligned replicas) and replicas at an odd element offset (scalar),
+    over ties, carries, subnormals, infinities, NaN payloads and random bit
+    patterns. fp32 replicas carry w's bits unchanged, NaN payloads included."""
+    bits = _f32_rounding_probes(70_000, seed=10 * r + offset)
+    n = bits.size
+    say(f"[bf16 specials] r={r} offset={offset} n={n}")
+    srv = ps.ParameterServer(n, 0.01, 0.0, queue_depth=1)
+    srv.set_weights(_device_f32(torch, bits))
+    want = orc.f32_to_bf16(bits.view(np.float32))
+    bufs = [torch.full((n + 8,), float("nan"), dtype=torch.bfloat16, device="cuda")
+            for _ in range(r)]
+    dsts = [b[offset:offset + n] for b in bufs]
+    srv.pull_many(list(range(r)), dsts)
+    f = torch.full((n + 8,), 7.0, device="cuda")
+    srv.pull_many([r], [f[offset:offset + n]])
+    srv.sync()
+    for j in range(r):
+        assert parity.bitwise(parity.np_bits(dsts[j]), want), (r, offset, j)
+    assert parity.bitwise(parity.np_bits(f[offset:offset + n]), bits.view(np.float32))
+    srv.close()
+
+
+@pytest.mark.parametrize("gdt", [ps.PS_F32, ps.PS_BF16], ids=["f32-grad", "bf16-grad"])
+@pytest.mark.parametrize("offset", [0, 4, 1])
+def test_bf16_replicas_from_the_apply_special_values(torch, gdt, offset):
+    """Replicas written by the apply pass itself (fusion) round as the oracle
+    does, for every apply kernel (8 or 4 values per lane, scalar). w holds the
+    probe patterns without NaN (NaN arithmetic is not bit-specified); zero
+    gradients leave every finite w and infinity in place up to the sign of
+    zero, the same on both sides."""
+    bits = _f32_rounding_probes(50_000, seed=100 + offset + gdt, nan=False)
+    n = bits.size
+    say(f"[bf16 specials fused] gdt={gdt} offset={offset} n={n}")
+    gtd = torch.bfloat16 if gdt == ps.PS_BF16 else torch.float32
+    g = torch.zeros(n, dtype=gtd, device="cuda")
+    srv = ps.ParameterServer(n, 0.01, 0.0, queue_depth=1)
+    srv.set_pull_fusion(2)
+    srv.set_weights(_device_f32(torch, bits))
+    bufs = [torch.full((n + 8,), float("nan"), dtype=torch.bfloat16, device="cuda")
+            for _ in range(2)]
+    dsts = [b[offset:offset + n] for b in bufs]
+    assert srv.push(0, g)
+    srv.apply_pull([0, 1], dsts)
+    srv.sync()
+    o = orc.OracleServer(bits.view(np.float32).copy(), 0.01, 0.0, depth=1)
+    o.push(0, parity.np_bits(g))
+    o.apply_pending()
+    assert parity.bitwise(parity.np_bits(srv.weights_copy()), o.w)
+    for j in range(2):
+        o.pull(j, j, orc.BF16)
+        assert parity.bitwise(parity.np_bits(dsts[j]), o.replicas[j]), (gdt, offset, j)
+    srv.close()
+
+
+def test_bf16_rounding_exhaustive(torch):
+    """All 2^32 fp32 bit patterns, in 16 chunks of 2^28, pulled into two bf16
+    replicas (the sliced fan-out, 8 values per lane) and one more (the
+    streaming copy): every replica equals the oracle's rounding, bit for
+    bit."""
+    chunk = 1 << 28
+    srv = ps.ParameterServer(chunk, 0.01, 0.0, queue_depth=1)
+    reps = [torch.empty(chunk, dtype=torch.bfloat16, device="cuda") for _ in range(3)]
+    base = np.arange(chunk, dtype=np.uint32)
+    for c in range(16):
+        say(f"[bf16 exhaustive] chunk {c}")
+        bits = base + np.uint32(c << 28)
+        srv.set_weights(_device_f32(torch, bits))
+        for t in reps:
+            t.fill_(float("nan"))
+        srv.pull_many([0, 1], reps[:2])
+        srv.pull_many([2], reps[2:])
+        srv.sync()
+        want = orc.f32_to_bf16(bits.view(np.float32))
+        for j, t in enumerate(reps):
+            assert parity.bitwise(parity.np_bits(t), want), (c, j)
+    del reps
+    srv.close()
+    free(torch)
+
+
 def test_lr_zero_and_zero_gradient(torch):
     n = 5000
     w0 = torch.linspace(-0.05, 0.05, n, device="cuda")
