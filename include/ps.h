@@ -127,7 +127,8 @@ void ps_destroy(ps_server *ps);
  * data moves. The buffer is borrowed: the caller must not write or free it
  * until the apply that consumes it has completed on the server's stream.
  * Returns PS_EFULL, with nothing enqueued, when the queue holds its depth of
- * gradients (Sec. 4.1, Theorem 2): apply, then push again. */
+ * gradients (Sec. 4.1, Theorem 2): apply, then push again. PS_EINVAL when
+ * the buffer overlaps the server's w or v. */
 int ps_push(ps_server *ps, int learner_id, const void *grad);
 
 /* ps_push for a gradient of the given dtype (PS_F32 or PS_BF16; a bf16
@@ -165,14 +166,16 @@ int ps_apply_sync(ps_server *ps);
  * dst[n_params] (device, fp32). Asynchronous on the server's stream; the copy
  * sees every apply issued before it. Skipped (no device work) when the same
  * learner last pulled into the same buffer with the same dtype at the current
- * timestamp (Sec. 4.1). dst must not overlap w or a pending gradient. */
+ * timestamp (Sec. 4.1). dst must not overlap a pending gradient; overlapping
+ * w or v is refused with PS_EINVAL. */
 int ps_pull(ps_server *ps, int learner_id, void *dst);
 
 /* Pull for n learners at once: learner_ids[i] into dsts[i], all in dst_dtype
  * (PS_F32, or PS_BF16 = round to nearest even). One fan-out kernel writes
  * every replica that is not skipped, reading w from HBM once (it walks w in
  * tiles that stay cached while the replicas of a tile are written).
- * 0 <= n <= PS_MAX_REPLICAS; the buffers that are written must be distinct. */
+ * 0 <= n <= PS_MAX_REPLICAS; the buffers that are written must be distinct,
+ * and none may overlap w or v (PS_EINVAL, nothing written). */
 int ps_pull_many(ps_server *ps, int n, const int *learner_ids, void *const *dsts, int dst_dtype);
 
 /* ps_apply_pending followed by ps_pull_many, in one call; the result is
@@ -243,7 +246,8 @@ int ps_set_pull_skip(ps_server *ps, int enabled);
 
 /* Reset the server to start from src[n_params] (device, fp32): w := src,
  * v := +0, timestamp := 0, every learner holds timestamp 0, pull history and
- * statistics cleared. PS_ESTATE if gradients are pending. Asynchronous. */
+ * statistics cleared. PS_ESTATE if gradients are pending; PS_EINVAL if src
+ * overlaps w or v. Asynchronous. */
 int ps_set_weights(ps_server *ps, const float *src);
 
 /* Device pointers to w[n_params] and v[n_params] (NULL without momentum).

@@ -78,6 +78,28 @@ int level_of(const void *p, int dtype) {
     return 0;
 }
 
+// Whether [p, p + bytes) shares a byte with w or v.
+bool overlaps_state(const ps_server *ps, const void *p, size_t bytes) {
+    const uintptr_t a = reinterpret_cast<uintptr_t>(p), b = a + bytes;
+    for (const float *x : {static_cast<const float *>(ps->w), static_cast<const float *>(ps->v)}) {
+        if (x == nullptr) continue;
+        const uintptr_t lo = reinterpret_cast<uintptr_t>(x), hi = lo + ps->n * sizeof(float);
+        if (a < hi && lo < b) return true;
+    }
+    return false;
+}
+
+size_t elem_bytes(int dtype) { return dtype == PS_BF16 ? 2 : 4; }
+
+// Replica buffers must not overlap w or v (a bf16 replica written over w
+// would corrupt it). Called after plan_pulls has validated the arguments.
+int check_dsts(const ps_server *ps, int n, void *const *dsts, int dtype) {
+    for (int i = 0; i < n; ++i)
+        if (overlaps_state(ps, dsts[i], ps->n * elem_bytes(dtype)))
+            return fail(PS_EINVAL, "destination %d overlaps the server's w or v", i);
+    return PS_OK;
+}
+
 int check(const ps_server *ps) {
     if (ps == nullptr) return fail(PS_EINVAL, "null server handle");
     return PS_OK;
@@ -350,6 +372,8 @@ int ps_free_rows(ps_server *ps, void *first_row) {
 int ps_push_async(ps_server *ps, int learner_id, const void *grad, int dtype, void *ready_event) {
     if (int rc = check(ps)) return rc;
     PS_LOCK(ps);
+    if (grad != nullptr && overlaps_state(ps, grad, ps->n * elem_bytes(dtype)))
+        return fail(PS_EINVAL, "gradient buffer overlaps the server's w or v");
     return ps->proto.push(learner_id, dtype, grad, ready_event);
 }
 
@@ -415,6 +439,7 @@ int ps_pull_many(ps_server *ps, int n, const int *learner_ids, void *const *dsts
     std::vector<int> write;
     if (int rc = ps->proto.plan_pulls(n, learner_ids, dsts, dst_dtype, ps->proto.ts, write))
         return rc;
+    if (int rc = check_dsts(ps, n, dsts, dst_dtype)) return rc;
     if (!write.empty()) {
         if (int rc = use_device(ps)) return rc;
         if (int rc = launch_pulls(ps, dsts, dst_dtype, write, false)) return rc;
@@ -441,6 +466,7 @@ int ps_apply_pull(ps_server *ps, int n, const int *learner_ids, void *const *dst
     const uint64_t ts_after = ps->proto.ts + b.items.size();
     if (int rc = ps->proto.plan_pulls(n, learner_ids, dsts, dst_dtype, ts_after, write))
         return rc;
+    if (int rc = check_dsts(ps, n, dsts, dst_dtype)) return rc;
     if (int rc = use_device(ps)) return rc;
     if (static_cast<int>(write.size()) <= ps->fuse_max_r) {
         if (int rc = launch_batch(ps, b.items, dst_dtype, dsts, write)) return rc;
@@ -612,6 +638,8 @@ int ps_set_weights(ps_server *ps, const float *src) {
     if (int rc = check(ps)) return rc;
     PS_LOCK(ps);
     if (src == nullptr) return fail(PS_EINVAL, "null source");
+    if (overlaps_state(ps, src, ps->n * sizeof(float)))
+        return fail(PS_EINVAL, "source overlaps the server's w or v");
     if (ps->proto.pending() != 0) return fail(PS_ESTATE, "gradients pending");
     if (int rc = use_device(ps)) return rc;
     if (int rc = drain_pulls(ps)) return rc;

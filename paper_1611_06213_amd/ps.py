@@ -488,6 +488,8 @@ class ParameterServer:
         free_rows(rows) or close(); the server does not keep them alive."""
         import torch
         dtype = torch.float32 if dtype is None else dtype
+        if dtype not in (torch.float32, torch.bfloat16):
+            raise TypeError(f"alloc_rows: rows hold float32 or bfloat16, not {dtype}")
         code = PS_BF16 if dtype == torch.bfloat16 else PS_F32
         rc, ptrs = ps_alloc_rows(self.h, count, code)
         self._check(rc, "alloc_rows")

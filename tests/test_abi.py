@@ -150,3 +150,16 @@ def test_binding_refuses_non_fp32_weights():
 
     with pytest.raises(TypeError, match="float32"):
         srv.set_weights(FakeDev())
+
+
+def test_binding_refuses_other_row_dtypes():
+    """Server rows hold fp32 or bf16; any other dtype is refused before the
+    library is called (a float16 request must not come back as fp32 rows)."""
+    import torch
+    srv = ps.ParameterServer.__new__(ps.ParameterServer)
+    srv.n = 4
+    srv.h = 0
+    srv._streams = []
+    for dt in (torch.float16, torch.float64, torch.int32):
+        with pytest.raises(TypeError, match="float32 or bfloat16"):
+            srv.alloc_rows(2, dt)

@@ -1404,6 +1404,52 @@ def test_learner_threads_push_while_server_applies(torch):
     free(torch)
 
 
+def test_buffers_overlapping_w_or_v_are_refused(torch):
+    """A gradient, a replica or a set_weights source that shares bytes with
+    the server's w or v is refused with PS_EINVAL before any state changes
+    or device work: w, v, the queue and the other replicas stay as they
+    were."""
+    n = 4099
+    srv = ps.ParameterServer(n, 0.01, 0.9, queue_depth=4)
+    w0 = (torch.arange(n, device="cuda", dtype=torch.float32) - 2000.0) * 1e-3
+    srv.set_weights(w0)
+    g = torch.full((n,), 0.5, device="cuda")
+    assert srv.push(0, g)
+    srv.apply_pending()
+    w_before = parity.np_bits(srv.weights_copy())
+    v_before = parity.np_bits(srv.velocity_copy())
+    h = srv.h
+    wp, vp = ps.ps_weights(h), ps.ps_velocity(h)
+    assert wp and vp
+    ts = srv.timestamp
+    # gradients: w itself, a bf16 view ending inside w, v shifted by 4 bytes
+    assert ps.ps_push_dtype(h, 1, wp, ps.PS_F32) == ps.PS_EINVAL
+    assert ps.ps_push_dtype(h, 1, wp - 2 * n + 2, ps.PS_BF16) == ps.PS_EINVAL
+    assert ps.ps_push_dtype(h, 1, vp + 4, ps.PS_F32) == ps.PS_EINVAL
+    assert "overlaps" in ps.ps_last_error()
+    assert srv.pending == 0
+    # replicas: one good buffer and one overlapping w or v, in either order
+    good = torch.full((n,), 7.0, device="cuda")
+    for bad, dt in ((wp, ps.PS_F32), (wp + 4 * n - 2, ps.PS_BF16), (vp, ps.PS_F32)):
+        for ptrs in ([good.data_ptr(), bad], [bad, good.data_ptr()]):
+            assert ps.ps_pull_many(h, [0, 1], ptrs, dt) == ps.PS_EINVAL
+            assert ps.load_library().ps_apply_pull(h, 2, ps._ints([0, 1]), ps._ptrs(ptrs), dt) \
+                == ps.PS_EINVAL
+    assert ps.ps_set_weights(h, wp) == ps.PS_EINVAL
+    assert ps.ps_set_weights(h, vp - 8) == ps.PS_EINVAL
+    srv.sync()
+    assert srv.timestamp == ts and srv.pending == 0
+    assert bool((good == 7.0).all())
+    assert parity.bitwise(parity.np_bits(srv.weights_copy()), w_before)
+    assert parity.bitwise(parity.np_bits(srv.velocity_copy()), v_before)
+    # a buffer that ends where w starts, or starts where w ends, does not
+    # overlap it (a push only records the pointer; both are dropped unapplied)
+    assert ps.ps_push_dtype(h, 3, wp - 4 * n, ps.PS_F32) == ps.PS_OK
+    assert ps.ps_push_dtype(h, 3, wp + 4 * n, ps.PS_F32) == ps.PS_OK
+    assert ps.ps_drop_learner(h, 3) == 2 and srv.pending == 0
+    srv.close()
+
+
 def test_alloc_rows_argument_errors(torch):
     """ps_alloc_rows / ps_free_rows / ps_set_fronts refuse bad arguments with
     PS_EINVAL and change nothing."""
