@@ -294,6 +294,22 @@ def test_bf16_rne_against_torch():
     assert np.array_equal(got, ref)
 
 
+def test_bf16_rne_every_kept_half_against_torch():
+    """Every one of the 65,536 kept halves (sign, exponent, top mantissa bits)
+    with each discarded half at a rounding boundary -- zero, just above zero,
+    just below one half, exactly one half, just above it, all ones -- rounds
+    as torch's cast does (NaN inputs excluded: their rule is pinned apart)."""
+    torch = pytest.importorskip("torch")
+    hi = np.arange(65536, dtype=np.uint32) << 16
+    lows = np.array([0x0000, 0x0001, 0x7FFF, 0x8000, 0x8001, 0xFFFF], np.uint32)
+    u = (hi[:, None] | lows[None, :]).ravel()
+    u = u[(u & 0x7FFFFFFF) <= 0x7F800000]
+    x = u.view(np.float32)
+    ref = torch.from_numpy(x.copy()).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    got = orc.f32_to_bf16(x)
+    assert got.size > 390000 and np.array_equal(got, ref)
+
+
 def test_bf16_rne_ties_by_hand():
     """Hand-derived ties-to-even cases (tests/golden/bf16_rne.txt)."""
     import os
