@@ -178,6 +178,60 @@ def test_momentum_closed_form_general():
 
 # ------------------------------------------------ exact-rational brute force
 
+def test_single_step_equals_numpy_float32():
+    """K = 1 without momentum is the library expression w - float32(lr) * g
+    in numpy's float32 arithmetic (numpy rounds each operation and never
+    fuses), bitwise, over weights and gradients of many magnitudes and both
+    signs, subnormal products included."""
+    rng = np.random.default_rng(21)
+    n = 200_000
+    w = (rng.standard_normal(n) * 10.0 ** rng.integers(-6, 3, n)).astype(np.float32)
+    g = (rng.standard_normal(n) * 10.0 ** rng.integers(-30, 4, n)).astype(np.float32)
+    for lr in (0.01, 0.001, 0.37, 2.0 ** -7):
+        want = w - np.float32(lr) * g
+        got = w.copy()
+        orc.step(got, g, lr)
+        assert np.array_equal(bits(got), bits(want)), lr
+
+
+def test_momentum_matches_torch_sgd():
+    """The heavy-ball convention (reading R2: v = m*v + g, w = w - lr*v,
+    no dampening, not Nesterov, v starting at zero) is the one of
+    torch.optim.SGD(momentum=m, dampening=0) on the CPU: one step at a time
+    from the same state, v is bitwise equal and w differs at most by what a
+    fused w update (one rounding instead of two) can change: one ulp of
+    lr*v plus one ulp of the new w. Over 8 steps of random gradients. A
+    dampened, Nesterov or reordered update fails by far more."""
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(22)
+    n = 50_000
+    lr, m = 0.01, 0.9
+    w = rng.uniform(-0.05, 0.05, n).astype(np.float32)
+    v = np.zeros(n, np.float32)
+    p = torch.nn.Parameter(torch.from_numpy(w.copy()))
+    opt = torch.optim.SGD([p], lr=lr, momentum=m, dampening=0.0, nesterov=False,
+                          foreach=False)
+    exact = 0
+    for t in range(8):
+        g = rand_f32(rng, n, 1e-2)
+        with torch.no_grad():
+            p.copy_(torch.from_numpy(w))
+            if t > 0:
+                opt.state[p]["momentum_buffer"].copy_(torch.from_numpy(v))
+        p.grad = torch.from_numpy(g.copy())
+        opt.step()
+        orc.step(w, g, lr, v=v, momentum=m)
+        tv = opt.state[p]["momentum_buffer"].numpy()
+        tw = p.detach().numpy()
+        assert np.array_equal(bits(v), bits(tv)), t
+        prod = (np.float32(lr) * v).astype(np.float32)
+        bound = np.spacing(np.abs(prod)) + np.spacing(np.abs(w))
+        diff = np.abs(w.astype(np.float64) - tw.astype(np.float64))
+        assert np.all(diff <= bound), (t, float((diff / bound).max()))
+        exact += int((bits(w) == bits(tw)).sum())
+    assert exact >= 0.5 * 8 * n
+
+
 @pytest.mark.parametrize("m", [None, 0.9])
 def test_brute_force_every_permutation(m):
     """N <= 8, 5 pushes, every arrival order: the oracle equals an exact-
