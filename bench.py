@@ -136,6 +136,9 @@ def cpu_baseline(cfg, pool, w0, pulls_per_step: int, seconds: float, distinct: i
         if t1 - t0 >= seconds:
             break
     oracle_rate = steps * cfg.depth / (t1 - t0)
+    from paper_1611_06213_amd import accounting as acc
+    step_bytes = (acc.apply_bytes(cfg.n, cfg.depth, 2 if cfg.grad_dtype == 1 else 4, cfg.momentum != 0)
+                  + acc.pull_bytes(cfg.n, pulls_per_step, 2 if cfg.pull_dtype == 1 else 4))
     oracle_sample = (f"{steps} whole steps ({cfg.depth} pushes + apply + {pulls_per_step} pulls) "
                      f"over the full {cfg.n:,}-parameter vector, 1 thread, pushes cycling over "
                      f"{distinct} host copies of pool buffers; {t1 - t0:.1f} s of CPU work on "
@@ -144,6 +147,8 @@ def cpu_baseline(cfg, pool, w0, pulls_per_step: int, seconds: float, distinct: i
     del host_g
     return {
         "value": round(oracle_rate, 4), "unit": "pushes/s", "cores": 1, "kind": "oracle",
+        # the same algorithmic bytes per step as the GPU line, over the oracle's time
+        "gbps_algorithmic": round(steps * step_bytes / (t1 - t0) / 1e9, 3),
         "sample": oracle_sample,
         "paper_style_ps": paper,
     }

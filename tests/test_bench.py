@@ -24,3 +24,18 @@ def test_more_than_one_gpu_is_refused():
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2 and "one GPU" in r.stderr
+
+
+def test_cpu_baseline_reports_rate_and_bytes():
+    """The oracle leg on a small workload: pushes/s, the algorithmic GB/s of
+    the same steps (bytes per step x steps / time), one core, and the
+    paper-style server beside it."""
+    from paper_1611_06213_amd import accounting as acc
+    from paper_1611_06213_amd import workloads as wl
+    cfg = wl.CONFIGS["alexnet"].scaled(50_000, pool=8)
+    pool = [wl.make_grad(cfg, j, "cpu") for j in range(cfg.pool)]
+    r = bench.cpu_baseline(cfg, pool, wl.make_w0(cfg, "cpu"), 4, 0.2)
+    assert r["kind"] == "oracle" and r["cores"] == 1 and r["unit"] == "pushes/s"
+    step = acc.apply_bytes(cfg.n, cfg.depth, 4, True) + acc.pull_bytes(cfg.n, 4, 4)
+    assert abs(r["gbps_algorithmic"] / (r["value"] / cfg.depth * step / 1e9) - 1) < 0.01
+    assert r["paper_style_ps"]["value"] > 0
