@@ -492,6 +492,15 @@ def main():
         "cpu_baseline": cpu,
         "timestamp_after": ts,
     }
+    state_mb = n * (8 if cfg.momentum != 0 else 4) / 1e6
+    if state_mb <= 256:
+        # small workloads: the weights stay in the memory-side cache between
+        # steps, and tiny steps are paced by launches, not by bandwidth
+        out["roofline"]["note"] = (
+            f"w{' and v' if cfg.momentum != 0 else ''} ({state_mb:.0f} MB) fit the 256 MB "
+            "memory-side cache, so part of the traffic is served from it: GB/s is effective, "
+            "not HBM-only" + ("; steps this small are launch-latency bound"
+                              if step_bytes / args.steps < 64e6 else ""))
     print(json.dumps(out), flush=True)
 
 
