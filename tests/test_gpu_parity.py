@@ -462,6 +462,55 @@ def test_bf16_rounding_exhaustive(torch):
     free(torch)
 
 
+def test_two_servers_on_their_own_streams(torch):
+    """Two handles in one process, each on its own stream (different sizes,
+    momentum, gradient and replica dtypes), with their calls interleaved:
+    each matches its own oracle bitwise, so nothing is shared between
+    handles."""
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(77)
+    specs = [(70_001, 0.01, 0.9, torch.float32, ps.PS_F32), (123_457, 0.005, 0.0, torch.bfloat16, ps.PS_BF16)]
+    servers, oracles, grads, reps = [], [], [], []
+    for n, lr, m, gdt, pdt in specs:
+        w0 = (torch.rand(n, generator=gen, device="cuda") - 0.5) * 0.1
+        grads.append([(torch.randn(n, generator=gen, device="cuda") * 1e-2).to(gdt) for _ in range(5)])
+        reps.append([torch.full((n,), float("nan"), device="cuda",
+                                dtype=torch.bfloat16 if pdt == ps.PS_BF16 else torch.float32)
+                     for _ in range(2)])
+        torch.cuda.synchronize()
+        srv = ps.ParameterServer(n, lr, m, queue_depth=4, stream=torch.cuda.Stream())
+        srv.set_weights(w0)
+        servers.append(srv)
+        oracles.append(orc.OracleServer(parity.np_bits(w0), lr, m, depth=4))
+    host = [[parity.np_bits(g) for g in gs] for gs in grads]
+    for step in range(6):
+        for j, (srv, o) in enumerate(zip(servers, oracles)):
+            for q in range(3 - j):
+                b = (step + q) % 5
+                assert srv.push(q, grads[j][b])
+                o.push(q, host[j][b])
+        for j, (srv, o) in enumerate(zip(servers, oracles)):
+            pdt = specs[j][4]
+            if (step + j) % 2:
+                srv.apply_pull([0, 1], reps[j])
+                o.apply_pending()
+            else:
+                srv.apply_pending()
+                srv.pull_many([0, 1], reps[j])
+                o.apply_pending()
+            for l in range(2):
+                o.pull(l, l, pdt)
+    for j, (srv, o) in enumerate(zip(servers, oracles)):
+        srv.sync()
+        assert parity.bitwise(parity.np_bits(srv.weights_copy()), o.w), j
+        if specs[j][2]:
+            assert parity.bitwise(parity.np_bits(srv.velocity_copy()), o.v), j
+        for l in range(2):
+            assert parity.bitwise(parity.np_bits(reps[j][l]), o.replicas[l]), (j, l)
+        assert srv.timestamp == o.ts
+        srv.close()
+
+
 def test_lr_zero_and_zero_gradient(torch):
     n = 5000
     w0 = torch.linspace(-0.05, 0.05, n, device="cuda")
