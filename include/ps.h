@@ -235,9 +235,10 @@ int ps_set_queue_mode(ps_server *ps, int mode, int slots_per_learner);
 
 /* How the apply kernels sweep the weights: 2^fronts_log2 evenly spaced
  * fronts (0..3), or -1 (default) to choose per apply from the buffers'
- * offsets within 2 MiB -- four fronts when most of the gradient, w and v
- * buffers share one offset (as separately allocated, 2 MiB-aligned buffers
- * do), one front otherwise (ps_alloc_rows buffers). Results are identical
+ * offsets within 2 MiB -- four fronts when at least 8 buffers take part and
+ * more than half of the gradient, w and v buffers share one 4 KiB offset (as
+ * separately allocated, 2 MiB-aligned buffers do), one front otherwise
+ * (ps_alloc_rows buffers). Results are identical
  * either way; only the order in which the grid visits coordinates changes. */
 int ps_set_fronts(ps_server *ps, int fronts_log2);
 
@@ -295,12 +296,14 @@ int ps_load(ps_server *ps, const char *path);
 /* Server-owned device buffers for gradients or replicas: the paper's queue
  * slots, which the server holds and learners fill (Sec. 4.1). Allocates
  * `count` (1..PS_MAX_ROWS) buffers of n_params values of `dtype` in one
- * device allocation and writes their addresses to rows[0..count). A row
- * of 2 MiB or more starts on a 2 MiB boundary plus (i + 2) * 4 KiB (mod
- * 2 MiB); w and v sit at phases 0 and 4 KiB. Smaller rows are packed on
- * 4 KiB boundaries. An apply then streams its gradients, w and v from
- * distinct offsets within 2 MiB, which the DRAM serves fastest. Buffers
- * allocated one by one (2 MiB-aligned, all at one phase) are served slower;
+ * device allocation and writes their addresses to rows[0..count). Rows of
+ * 2 MiB or more are 1.75 MiB apart beyond their 2 MiB-rounded size: row i
+ * starts at ((i + 2) * 1.75 MiB) mod 2 MiB past a 2 MiB boundary, and v
+ * sits 1.75 MiB past w's 2 MiB-rounded end (w on a 2 MiB boundary).
+ * Smaller rows are packed on 4 KiB boundaries. An apply then streams its
+ * gradients, w and v from spread-out addresses, which the DRAM serves
+ * fastest of the layouts measured. Buffers allocated one by one
+ * (2 MiB-aligned, all at one phase) are served slower;
  * for them the apply kernels switch to a schedule that recovers part of the
  * difference. Contents are uninitialised. The buffers belong to the server
  * until ps_free_rows(ps, rows[0]) or ps_destroy. PS_ENOMEM if the device

@@ -13,28 +13,34 @@ size_t velocity_offset(size_t w_bytes) { return round_up(w_bytes, kRowAlign) + k
 
 RowLayout row_layout(size_t row_bytes, int count) {
     RowLayout r;
-    r.head = 2 * kRowStagger;
-    // rows under 2 MiB are packed on 4 KiB boundaries (their phases differ
-    // anyway, and rounding each up to 2 MiB would waste memory)
-    r.stride = row_bytes < kRowAlign ? round_up(row_bytes, kRowStagger)
-                                     : round_up(row_bytes, kRowAlign) + kRowStagger;
+    if (row_bytes < kRowAlign) {
+        // packed on 4 KiB boundaries (their phases differ anyway, and rounding
+        // each up to 2 MiB would waste memory)
+        r.head = 2 * kPhase;
+        r.stride = round_up(row_bytes, kPhase);
+    } else {
+        r.head = 2 * kRowStagger;
+        r.stride = round_up(row_bytes, kRowAlign) + kRowStagger;
+    }
     r.span = r.head + (static_cast<size_t>(count) - 1) * r.stride + row_bytes;
     return r;
 }
 
 int fronts_log2_for(const void *const *ptrs, int count) {
     constexpr int kMaxStreams = 66;   // PS_MAX_QUEUE_DEPTH gradients + w + v
-    uintptr_t seen[kMaxStreams];
-    int distinct = 0, streams = 0;
+    uintptr_t ph[kMaxStreams];
+    int streams = 0;
     for (int i = 0; i < count && streams < kMaxStreams; ++i) {
         if (ptrs[i] == nullptr) continue;
-        ++streams;
-        const uintptr_t ph = (reinterpret_cast<uintptr_t>(ptrs[i]) % kRowAlign) / kRowStagger;
-        bool dup = false;
-        for (int j = 0; j < distinct; ++j) dup = dup || seen[j] == ph;
-        if (!dup) seen[distinct++] = ph;
+        ph[streams++] = (reinterpret_cast<uintptr_t>(ptrs[i]) % kRowAlign) / kPhase;
     }
-    return (streams >= 8 && 2 * distinct < streams) ? 2 : 0;
+    int most = 0;   // the largest number of streams sharing one phase
+    for (int i = 0; i < streams; ++i) {
+        int same = 0;
+        for (int j = 0; j < streams; ++j) same += ph[j] == ph[i];
+        most = same > most ? same : most;
+    }
+    return (streams >= 8 && 2 * most > streams) ? 2 : 0;
 }
 
 }  // namespace gadei

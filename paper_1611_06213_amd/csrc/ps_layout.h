@@ -2,11 +2,15 @@
 // buffers it did not place. Host-only; ps_server.cpp uses it, and it builds
 // on its own for host tests.
 //
-// DRAM serves many concurrent streams fastest when they start at different
-// offsets within 2 MiB. The server's own buffers (w, v and the rows of
-// ps_alloc_rows) start on 2 MiB boundaries plus distinct multiples of 4 KiB.
-// Buffers allocated one by one all start at one such offset; for them the
-// kernels sweep several fronts instead of one (fronts_log2_for).
+// DRAM serves many concurrent streams fastest when they do not start at one
+// offset within 2 MiB (their "phase"), and the distance between them matters
+// beyond that: the apply reads 32 or more rows in lockstep, and how their
+// addresses spread over HBM channels and banks depends on higher address bits
+// too. The server's own large buffers (w, v and the rows of ps_alloc_rows)
+// therefore start 1.75 MiB apart beyond their 2 MiB-rounded sizes, so
+// consecutive rows step through the eight 256 KiB phases downwards. Buffers
+// allocated one by one all start at one phase; for them the kernels sweep
+// several fronts instead of one (fronts_log2_for).
 #pragma once
 
 #include <stddef.h>
@@ -15,20 +19,31 @@
 namespace gadei {
 
 constexpr size_t kRowAlign = size_t(2) << 20;
-constexpr size_t kRowStagger = 4096;
+// Phase granularity: rows under 2 MiB are packed on it, and the front choice
+// compares buffer phases at it.
+constexpr size_t kPhase = 4096;
+// Step between large rows (and from w to v) beyond their 2 MiB-rounded size.
+// Measured on the VGG-16 (fp32) and Mixed (bf16) applies from 32 rows, over
+// steps of 4 KiB and 64 KiB .. 2 MiB: 64-256 KiB were worst (up to 20%
+// slower than 4 KiB), steps near 1 MiB were bad for the bf16 rows, and
+// 1.75 MiB was among the best for both. Whole bench steps against 4 KiB:
+// VGG-16 7,111-7,119 vs 6,953-6,961 pushes/s, Mixed +2.8%, AlexNet +0.9%.
+constexpr size_t kRowStagger = size_t(7) << 18;
 
 size_t round_up(size_t x, size_t a);
 char *align_up(void *p, size_t a);
 
-// Offset of v from w (w at a 2 MiB boundary): one stagger past w's
+// Offset of v from w (w at a 2 MiB boundary): one kRowStagger past w's
 // 2 MiB-rounded end.
 size_t velocity_offset(size_t w_bytes);
 
 // A set of `count` rows of row_bytes each, from a 2 MiB-aligned base: row i
-// at head + i * stride. Rows of 2 MiB or more step by their 2 MiB-rounded
-// size plus 4 KiB, so row i sits at offset (i + 2) * 4 KiB within 2 MiB (w
-// and v take the first two offsets); smaller rows are packed on 4 KiB
-// boundaries. `span` = bytes from the base to the end of the last row.
+// at head + i * stride. Rows of 2 MiB or more start two kRowStagger in and
+// step by their 2 MiB-rounded size plus kRowStagger, so row i sits at phase
+// ((i + 2) * kRowStagger) mod 2 MiB (w, v and the rows of one set cycle
+// through the eight 256 KiB phases); smaller rows are packed on kPhase
+// boundaries after a head of 2 * kPhase. `span` = bytes from the base to the
+// end of the last row.
 struct RowLayout {
     size_t head;
     size_t stride;
@@ -37,11 +52,11 @@ struct RowLayout {
 RowLayout row_layout(size_t row_bytes, int count);
 
 // Fronts (log2) an apply over these streams (gradients, w, v; null entries
-// are skipped) should sweep: 2 (four fronts) when at least 8 streams and
-// fewer than half of them start at distinct 4 KiB offsets within 2 MiB,
-// else 0 (one front). Measured on 34 streams of 553 MB: same-offset buffers
+// are skipped) should sweep: 2 (four fronts) when there are at least 8
+// streams and more than half of them share one phase (compared at kPhase),
+// else 0 (one front). Measured on 34 streams of 553 MB: same-phase buffers
 // 3.97-4.27 ms with one front, 3.42-3.54 ms with four; staggered buffers
-// 3.09-3.31 ms with one front and no better with four.
+// no better with four.
 int fronts_log2_for(const void *const *ptrs, int count);
 
 }  // namespace gadei

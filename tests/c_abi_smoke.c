@@ -135,7 +135,9 @@ int main(void)
     void *rows[8];
     CHECK(ps_alloc_rows(ps, 8, PS_F32, rows) == PS_OK, "ps_alloc_rows");
     for (int j = 0; j < 8; ++j) {
-        CHECK(((uintptr_t)rows[j] % ((uintptr_t)2 << 20)) == (uintptr_t)(j + 2) * 4096,
+        /* rows of 2 MiB or more sit at phase ((j + 2) * 1.75 MiB) mod 2 MiB */
+        CHECK(((uintptr_t)rows[j] % ((uintptr_t)2 << 20)) ==
+                  ((uintptr_t)(j + 2) * ((uintptr_t)7 << 18)) % ((uintptr_t)2 << 20),
               "row %d phase", j);
         HIPCHECK(hipMemcpy(rows[j], grad, n * sizeof(float), hipMemcpyDeviceToDevice));
         CHECK(ps_push(ps, j, rows[j]) == PS_OK, "push row %d", j);

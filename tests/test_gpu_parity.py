@@ -1279,22 +1279,23 @@ def _oracle_apply(torch, w0, grads, lr, m, k, pulls_bf16=False):
 
 
 def test_alloc_rows_layout_and_parity(torch):
-    """Server-owned rows: distinct 4 KiB phases within 2 MiB (w at 0, v at
-    4 KiB, row i at (i + 2) * 4 KiB), no overlap, usable as fp32 and bf16
+    """Server-owned rows: w at phase 0 within 2 MiB, v at 1.75 MiB, row i at
+    ((i + 2) * 1.75 MiB) mod 2 MiB, no overlap, usable as fp32 and bf16
     gradients and replicas with results bitwise equal to the oracle; freeing
     refuses rows a pending gradient lies in."""
     n, k, lr, m = 3 * (1 << 20) + 5, 32, 0.01, 0.9
     say(f"[case] alloc_rows n={n} K={k}")
     two_mib = 2 << 20
     srv = ps.ParameterServer(n, lr, m, queue_depth=k)
-    assert ps.ps_weights(srv.h) % two_mib == 0 and ps.ps_velocity(srv.h) % two_mib == 4096
+    stagger = 7 << 18
+    assert ps.ps_weights(srv.h) % two_mib == 0 and ps.ps_velocity(srv.h) % two_mib == stagger
     gen = torch.Generator(device="cuda")
     gen.manual_seed(31)
     w0 = (torch.rand(n, generator=gen, device="cuda") - 0.5) * 0.1
     srv.set_weights(w0)
     rows = srv.alloc_rows(k + 3)
     addrs = [r.data_ptr() for r in rows]
-    assert [a % two_mib for a in addrs] == [((i + 2) * 4096) % two_mib for i in range(k + 3)]
+    assert [a % two_mib for a in addrs] == [((i + 2) * stagger) % two_mib for i in range(k + 3)]
     assert all(b - a >= 4 * n for a, b in zip(addrs, addrs[1:]))
     for r in rows[:k]:
         r.copy_(torch.randn(n, generator=gen, device="cuda") * 1e-3)
@@ -1304,7 +1305,7 @@ def test_alloc_rows_layout_and_parity(torch):
         srv.free_rows(rows)                       # pending gradients live there
     assert e.value.code == ps.PS_ESTATE
     reps16 = srv.alloc_rows(2, torch.bfloat16)
-    assert [t.data_ptr() % two_mib for t in reps16] == [8192, 12288]
+    assert [t.data_ptr() % two_mib for t in reps16] == [(2 * stagger) % two_mib, (3 * stagger) % two_mib]
     srv.apply_pull([0, 1, 2], rows[k:k + 3])
     srv.pull_many([3, 4], reps16)
     torch.cuda.synchronize()

@@ -179,38 +179,52 @@ def test_scripts_reach_every_outcome(driver):
 MIB2 = 2 << 20
 
 
+STAGGER = 7 << 18   # 1.75 MiB: the step between large server rows
+
+
 def test_row_layout_phases(driver):
-    """Server rows start at distinct 4 KiB offsets within 2 MiB, after the
-    offsets of w (0) and v (4 KiB), never overlap, and fit the span."""
-    for row_bytes, count in ((4 * 138_357_544, 64), (2 * 200_000_000, 32), (4, 3),
-                             (4096, 7), (MIB2, 5), (MIB2 + 1, 600)):
+    """Rows of 2 MiB or more start 2 * 1.75 MiB in and step by their 2 MiB-
+    rounded size plus 1.75 MiB, so consecutive rows step down through the
+    eight 256 KiB phases within 2 MiB; v sits 1.75 MiB past w's 2 MiB-rounded
+    end. Rows never overlap and fit the span."""
+    for row_bytes, count in ((4 * 138_357_544, 64), (2 * 200_000_000, 32), (MIB2, 5),
+                             (MIB2 + 1, 600)):
         out = run_driver(driver, [f"rows {row_bytes} {count}"])[0].split()
         head, stride, span, v_off = map(int, out[1:])
-        assert v_off % MIB2 == 4096 and v_off >= row_bytes
+        assert v_off % MIB2 == STAGGER and v_off >= row_bytes
+        assert head == 2 * STAGGER and stride % MIB2 == STAGGER and stride >= row_bytes
         starts = [head + i * stride for i in range(count)]
         assert all(b - a >= row_bytes for a, b in zip(starts, starts[1:]))
         assert starts[-1] + row_bytes == span
         phases = [x % MIB2 for x in starts]
-        assert phases[:510] == [(i + 2) * 4096 for i in range(min(count, 510))]
-        assert 0 not in phases[:510] and 4096 not in phases[:510]
+        assert phases == [((i + 2) * STAGGER) % MIB2 for i in range(count)]
+        assert len(set(phases[:8])) == min(count, 8) and all(p % (256 << 10) == 0 for p in phases)
 
 
 def test_front_choice(driver):
-    """Four fronts (log2 = 2) for many streams at one offset within 2 MiB
-    (separately allocated buffers), one front for staggered buffers, for few
-    streams, and when half or more of the offsets are distinct."""
+    """Four fronts (log2 = 2) when at least 8 streams and more than half of
+    them share one phase within 2 MiB (separately allocated buffers); one
+    front for staggered buffers (4 KiB apart, or the server's rows and w, v
+    spread over eight 256 KiB phases), for few streams, and when no phase
+    holds more than half of them."""
     base = 0x7f0000000000
     aligned = [base + i * 265 * MIB2 for i in range(34)]
     staggered = [base + i * (265 * MIB2 + 4096) for i in range(34)]
+    rows = [base + 2 * STAGGER + i * (265 * MIB2 + STAGGER) for i in range(32)]
+    server = rows + [base, base + 264 * MIB2 + STAGGER]          # 32 rows, w, v
+    eight = [base + (i % 8) * (256 << 10) + i * 265 * MIB2 for i in range(34)]
     lines = ["fronts " + " ".join(map(str, aligned)),
              "fronts " + " ".join(map(str, staggered)),
              "fronts " + " ".join(map(str, aligned[:7])),
              "fronts " + " ".join(map(str, aligned[:8])),
              "fronts " + " ".join(map(str, aligned[:17] + staggered[17:])),
              "fronts " + " ".join(map(str, aligned[:19] + staggered[19:])),
-             "fronts " + " ".join(map(str, aligned[:16] + [0] * 16))]
+             "fronts " + " ".join(map(str, aligned[:16] + [0] * 16)),
+             "fronts " + " ".join(map(str, server)),
+             "fronts " + " ".join(map(str, eight))]
     assert run_driver(driver, lines) == ["fronts 2", "fronts 0", "fronts 0", "fronts 2",
-                                         "fronts 0", "fronts 2", "fronts 2"]
+                                         "fronts 0", "fronts 2", "fronts 2", "fronts 0",
+                                         "fronts 0"]
 
 
 def test_small_rows_are_packed(driver):
