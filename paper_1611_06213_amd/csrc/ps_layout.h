@@ -28,6 +28,8 @@ constexpr size_t kPhase = 4096;
 // slower than 4 KiB), steps near 1 MiB were bad for the bf16 rows, and
 // 1.75 MiB was among the best for both. Whole bench steps against 4 KiB:
 // VGG-16 7,111-7,119 vs 6,953-6,961 pushes/s, Mixed +2.8%, AlexNet +0.9%.
+// The gain is at the default depth: for applies of 16 or fewer gradients
+// with momentum, 4 KiB steps measured 1.5-3.7 points of peak faster.
 constexpr size_t kRowStagger = size_t(7) << 18;
 
 size_t round_up(size_t x, size_t a);
