@@ -39,3 +39,21 @@ def test_cpu_baseline_reports_rate_and_bytes():
     step = acc.apply_bytes(cfg.n, cfg.depth, 4, True) + acc.pull_bytes(cfg.n, 4, 4)
     assert abs(r["gbps_algorithmic"] / (r["value"] / cfg.depth * step / 1e9) - 1) < 0.01
     assert r["paper_style_ps"]["value"] > 0
+
+
+def test_algorithmic_bytes_per_step_and_launch():
+    """The bytes bench.py divides by: a VGG-16 step moves the apply's
+    19,923,486,336 bytes plus the 16-replica pull's 9,408,312,992 (29.33 GB,
+    the figure the roofline is quoted on); the dominant launch is the apply.
+    ps_apply_pull with one replica writes it from the apply pass (no second
+    read of w); above one replica the pull is its own kernel again."""
+    from paper_1611_06213_amd import workloads as wl
+    cfg = wl.CONFIGS["vgg16"]
+    n = cfg.n
+    assert bench.algorithmic_bytes(cfg, "separate", 16) == (29_331_799_328, 19_923_486_336)
+    assert bench.algorithmic_bytes(cfg, "fused", 16) == (29_331_799_328, 29_331_799_328)
+    one = 19_923_486_336 + 4 * n
+    assert bench.algorithmic_bytes(cfg, "fused", 1) == (one, one)
+    assert bench.algorithmic_bytes(cfg, "separate", 0) == (19_923_486_336, 19_923_486_336)
+    mixed = wl.CONFIGS["mixed"]
+    assert bench.algorithmic_bytes(mixed, "separate", 32)[0] == 29_600_000_000
