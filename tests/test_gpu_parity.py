@@ -1110,6 +1110,34 @@ def test_binding_freed_gradients_not_reused_before_apply(torch):
     srv.close()
 
 
+def test_binding_freed_weights_source_not_reused_before_copy(torch):
+    """set_weights copies on the server's stream: a caller that frees the
+    source tensor at once, while the copy is still queued behind other work
+    on a side stream, does not get its memory back from torch's allocator for
+    a new tensor (whose writes would race the copy). w then equals the source
+    bitwise."""
+    n = 1 << 24
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(52)
+    src = (torch.rand(n, generator=gen, device="cuda") - 0.5) * 0.1
+    want = parity.np_bits(src)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    srv = ps.ParameterServer(n, 0.01, 0.9, stream=side)
+    with torch.cuda.stream(side):
+        torch.cuda._sleep(50_000_000)     # ~20 ms: the copy is still queued when the host allocates
+    srv.set_weights(src)
+    old = src.data_ptr()
+    del src
+    fresh = [torch.empty(n, device="cuda") for _ in range(4)]
+    for t in fresh:
+        t.fill_(1e30)                     # on the current stream, at once
+    assert old not in {t.data_ptr() for t in fresh}
+    assert parity.bitwise(parity.np_bits(srv.weights_copy()), want)
+    assert not parity.np_bits(srv.velocity_copy()).view(np.uint32).any()
+    srv.close()
+
+
 def test_record_lets_producer_reuse_its_buffer(torch):
     """After ps_record, a producer stream that waits for the event may
     overwrite the gradient buffer; the apply already read the old values."""
