@@ -31,6 +31,11 @@ gradients this way. A synchronous step takes one gradient from every
 non-empty queue, summed in increasing learner order (Eq. "ssgd" sums over
 l = 1..lambda).
 
+Dead learners (Sec. 4.3): drop_learner discards a dead learner's queued
+gradients (its buffers may have died with it); retire_learner keeps them
+queued, to be applied exactly once in their turn, as the paper's stateless
+server does with gradients already in its shared slots.
+
 Readings where the paper is silent (each also listed in the design notes):
   * one global FIFO in push-call order stands in for the per-learner queues;
   * a batch of K pending gradients is applied as K sequential steps, each over
@@ -208,6 +213,7 @@ class OracleServer:
         self.slots = 0
         self.per_learner: Dict[int, List[Tuple[int, np.ndarray, int]]] = {}
         self.last_served = -1
+        self.retired = set()
 
     def set_queue_mode(self, mode: int, slots: int = 1) -> int:
         if mode not in (FIFO, ROUND_ROBIN) or not 1 <= slots <= MAX_DEPTH:
@@ -225,6 +231,8 @@ class OracleServer:
     def push(self, learner: int, grad: np.ndarray) -> int:
         if learner < 0:
             return EINVAL
+        if learner in self.retired:
+            return ESTATE
         entry = (learner, grad, self.learner_ts.get(learner, 0))
         if self.mode == ROUND_ROBIN:
             q = self.per_learner.setdefault(learner, [])
@@ -290,7 +298,10 @@ class OracleServer:
         return OK
 
     def pull(self, learner: int, dst_key, dtype: int = F32) -> bool:
-        """Refresh replica `dst_key` for `learner`. Returns False if skipped."""
+        """Refresh replica `dst_key` for `learner`. Returns False if skipped.
+        A retired learner pulls no more (ValueError)."""
+        if learner in self.retired:
+            raise ValueError(f"learner {learner} has retired")
         self.pulls += 1
         key = (dst_key, dtype, self.ts)
         if self.pull_skip and self.last_pull.get(learner) == key:
@@ -300,6 +311,20 @@ class OracleServer:
         self.last_pull[learner] = key
         self.learner_ts[learner] = self.ts
         return True
+
+    def retire_learner(self, learner: int) -> int:
+        """A learner died (Sec. 4.3) while its gradients sat in the server's
+        own slots. The server is stateless -- it processes the gradients in
+        its queues without regard to who produced them -- so those gradients
+        stay queued and are applied exactly once in their turn (Theorem 2);
+        the dead learner pushes and pulls no more. Returns how many of its
+        gradients are still queued."""
+        if learner < 0:
+            return EINVAL
+        self.retired.add(learner)
+        if self.mode == ROUND_ROBIN:
+            return len(self.per_learner.get(learner, []))
+        return sum(1 for e in self.queue if e[0] == learner)
 
     def drop_learner(self, learner: int) -> int:
         """A learner died (Sec. 4.3): its queued gradients are discarded, the

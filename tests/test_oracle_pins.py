@@ -669,6 +669,94 @@ def test_round_robin_sync_one_per_learner_in_id_order():
 
 # ------------------------------------------------ dead learners (Sec. 4.3)
 
+def test_golden_retire_script():
+    """tests/golden/retire_rr.txt, worked by hand from Sec. 4.3, Theorem 2
+    and Sec. 4.1: a dead learner's gradient left in the server's slot is
+    applied once in its turn, with the staleness of the timestamp it was
+    pushed with; the dead learner's pushes and pulls are refused."""
+    depth, ops, expect, mode = golden_script.load("retire_rr.txt", with_mode=True)
+    s = orc.OracleServer(np.zeros(2, np.float32), 2.0 ** -4, 0.0, depth=depth)
+    assert s.set_queue_mode(orc.ROUND_ROBIN, mode[1]) == orc.OK
+    g = np.full(2, 0.5, np.float32)
+    rejected = 0
+    for op, l, outcome in ops:
+        if op == "push":
+            rc = s.push(l, g)
+            assert rc == {"ok": orc.OK, "full": orc.EFULL, "refused": orc.ESTATE}[outcome]
+            rejected += rc == orc.EFULL
+        elif op == "apply":
+            assert s.apply_pending() == orc.OK
+        elif op == "retire":
+            assert s.retire_learner(l) == int(outcome)
+        elif op == "drop":
+            assert s.drop_learner(l) == int(outcome)
+        elif outcome == "refused":
+            with pytest.raises(ValueError):
+                s.pull(l, ("dst", l), orc.F32)
+        else:
+            assert s.pull(l, ("dst", l), orc.F32) == (outcome == "pulled")
+    assert s.applied_order == expect["order"]
+    assert s.staleness == expect["staleness"]
+    assert s.ts == expect["ts"][0]
+    assert (s.pulls, s.pulls_skipped, rejected) == (expect["pulls"], expect["skipped"], expect["rejected"])
+    assert np.all(s.w == -6 / 32)            # six steps of lr * g = 1/32 each
+
+
+def test_retire_learner_applies_queued_exactly_once():
+    """Theorem 2 across a death: over random interleavings (both queue
+    modes) in which learners retire, every accepted gradient -- a retired
+    learner's queued ones included -- is applied exactly once; a retired
+    learner's later pushes are refused.
+    The weights equal a run in which the learner simply stopped pushing at
+    that point (the server is stateless, Sec. 4.3), and differ from the drop
+    reading whenever a retired learner had gradients queued."""
+    rng = np.random.default_rng(41)
+    queued_at_death = 0
+    for mode, slots, depth in ((orc.FIFO, 1, 5), (orc.ROUND_ROBIN, 3, 4), (orc.ROUND_ROBIN, 1, 2)):
+        w0 = rng.uniform(-0.05, 0.05, 16).astype(np.float32)
+        a = orc.OracleServer(w0, 0.01, 0.9, depth=depth)   # retires learners
+        b = orc.OracleServer(w0, 0.01, 0.9, depth=depth)   # never told
+        c = orc.OracleServer(w0, 0.01, 0.9, depth=depth)   # drops them instead
+        for s in (a, b, c):
+            s.set_queue_mode(mode, slots)
+        accepted, dead, queued_here = [], set(), 0
+        for step in range(400):
+            r = rng.random()
+            if r < 0.75:
+                l = int(rng.integers(5))
+                g = rng.normal(0, 0.01, 16).astype(np.float32)
+                rc = a.push(l, g)
+                if l in dead:
+                    assert rc == orc.ESTATE
+                    continue
+                assert b.push(l, g) == rc and c.push(l, g) == rc
+                if rc == orc.OK:
+                    accepted.append(l)
+            elif r < 0.97:
+                for s in (a, b, c):
+                    s.apply_pending()
+            elif len(dead) < 3:
+                l = int(rng.integers(5))
+                if l not in dead:
+                    n = a.retire_learner(l)
+                    queued_here += n
+                    assert c.drop_learner(l) == n
+                    dead.add(l)
+        while a.pending():
+            a.apply_pending()
+            b.apply_pending()
+        assert b.pending() == 0
+        assert np.array_equal(bits(a.w), bits(b.w)) and np.array_equal(bits(a.v), bits(b.v))
+        assert a.applied_order == b.applied_order and a.staleness == b.staleness
+        assert len(a.applied_order) == len(accepted) and a.ts == len(accepted)
+        for l in range(5):
+            assert a.applied_order.count(l) == accepted.count(l)
+        if queued_here:
+            assert not np.array_equal(bits(a.w), bits(c.w))
+        queued_at_death += queued_here
+    assert queued_at_death > 0
+
+
 def test_drop_learner_isolates_failure():
     """Dropping a dead learner's queued gradients leaves the others' in order
     and the result equals a run in which it never pushed them (the server
