@@ -10,11 +10,23 @@ are resident in HBM before timing starts. By default they and the replicas
 are the server's own rows (ps_alloc_rows: the queue slots learners fill);
 --layout torch puts every buffer in its own torch allocation instead.
 
+Timing. After W warm-up steps, `runs` (default 5) timed runs of exactly K
+steps each, w and v reset to w0 and 0 before every run (ps_set_weights);
+each run is one ps_run call (the library's native executor walks the
+prepared schedule of pushes, applies and pulls), bracketed by device
+synchronisation, and `value` is the median run's pushes/s. One more run
+drives the same calls one by one from Python (`python_driven_pushes_per_s`),
+and a last one records HIP events around every kernel on the stream it runs
+on, for the per-kernel durations behind `roofline` (events between kernels
+cost a few microseconds each, which only the launch-bound workloads notice,
+so they stay out of the runs that give `value`).
+
 Prints one JSON line (rank 0, N = 1). Extra keys: the dominant kernel's
-roofline (algorithmic bytes per launch / mean launch time from HIP events on
-the library's stream), HBM traffic from recorded rocprofv3 counters when the
-kernel source still matches them, a device-copy ceiling, and the oracle timed
-on the host's cores on a bounded sample.
+roofline (algorithmic bytes per launch / mean launch time), HBM traffic from
+recorded rocprofv3 counters when the code they were taken on is unchanged,
+reference rates of other implementations on this machine (torch's sum, the HIP
+runtime's device copy, the library's own one-replica copy), and the oracle
+timed on the host's cores on a bounded sample.
 """
 from __future__ import annotations
 
@@ -30,7 +42,11 @@ sys.path.insert(0, ROOT)
 
 PEAK_GBPS = 8000.0          # MI355X HBM3E, published
 METRIC = "gradient pushes applied/sec + achieved HBM GB/s (% of peak), 1 MI355X"
-KERNEL_SRC = os.path.join(ROOT, "paper_1611_06213_amd", "csrc", "ps_kernels.hip")
+CSRC = os.path.join(ROOT, "paper_1611_06213_amd", "csrc")
+# the kernels and the host code that decides their launch shapes and the
+# buffers' placement: recorded counters stay valid only while all are unchanged
+KERNEL_SRC = [os.path.join(CSRC, f) for f in ("ps_kernels.hip", "ps_kernels.h", "ps_server.cpp",
+                                              "ps_layout.cpp", "ps_layout.h")]
 COUNTERS = os.path.join(ROOT, "profiles", "traffic_apply_vec_vgg16.txt")
 
 
@@ -73,15 +89,21 @@ def batches(cfg, wl):
     return out
 
 
-def kernel_source_digest(path: str = KERNEL_SRC) -> str:
-    """sha256 of the kernel source with comments and blank space removed, so
+def kernel_source_digest(paths=KERNEL_SRC) -> str:
+    """sha256 over the kernel source and the host files that shape its
+    launches and buffer placement, with comments and blank space removed, so
     that a comment-only edit keeps recorded counters valid and any code
     change invalidates them."""
     import re
-    text = open(path).read()
-    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
-    text = re.sub(r"//[^\n]*", " ", text)
-    return hashlib.sha256(" ".join(text.split()).encode()).hexdigest()
+    if isinstance(paths, str):
+        paths = [paths]
+    h = hashlib.sha256()
+    for path in paths:
+        text = open(path).read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode() + b"\0")
+    return h.hexdigest()
 
 
 def recorded_traffic(kernel_label: str):
@@ -196,9 +218,43 @@ def cpu_model() -> str:
     return "unknown CPU"
 
 
+def reference_rates(torch, ps, lib, n: int = 1 << 28, reps: int = 10):
+    """GB/s of plain device streams over 1 GiB on this machine, for context: a
+    read by torch's sum reduction, a copy by the HIP runtime
+    (hipMemcpyAsync device to device), and the library's own one-replica pull
+    (a 1-read/1-write copy)."""
+    import ctypes
+    stream = torch.cuda.current_stream()
+    x = torch.empty(n, dtype=torch.float32, device="cuda").normal_()
+    y = torch.empty_like(x)
+    hip = ps._hip()
+
+    def hip_copy():
+        if hip(ctypes.c_void_p(y.data_ptr()), ctypes.c_void_p(x.data_ptr()),
+               ctypes.c_size_t(4 * n), 3, ctypes.c_void_p(stream.cuda_stream)) != 0:
+            raise RuntimeError("hipMemcpyAsync failed")
+
+    def rate(fn, byt):
+        fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return byt / (e0.elapsed_time(e1) / reps * 1e-3) / 1e9
+
+    out = {"torch_sum_read_gbps": round(rate(lambda: x.sum(), 4 * n), 1),
+           "hip_memcpy_d2d_gbps": round(rate(hip_copy, 8 * n), 1),
+           "library_copy_gbps": round(copy_ceiling(torch, ps, lib, n, reps), 1),
+           "bytes": 4 * n}
+    del x, y
+    return out
+
+
 def copy_ceiling(torch, ps, lib, n: int = 1 << 28, reps: int = 10):
     """The library's pull kernel with a single fp32 replica is a plain
-    1-read/1-write device copy: its GB/s is the copy ceiling of this machine."""
+    1-read/1-write device copy."""
     h = ps.ps_create(n, 0.0, 0.0)
     stream = torch.cuda.current_stream()
     ps.ps_set_stream(h, stream.cuda_stream)
@@ -269,6 +325,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--runs", type=int, default=5,
+                    help="timed runs of --steps steps each, w and v reset before each; "
+                         "value is the median run")
     ap.add_argument("--config", default="vgg16")
     ap.add_argument("--mode", choices=["fused", "separate", "hogwild"], default="separate",
                     help="separate: ps_apply_pending + ps_pull_many (one kernel each, timed "
@@ -354,8 +413,9 @@ def main():
     gptr = [pool[j].data_ptr() for j in range(cfg.pool)]
     calls = []
     for pushes_b, pulls_b in plan:
+        dl = [replicas[l].data_ptr() for l in pulls_b]
         calls.append(([(l, gptr[b]) for l, b in pushes_b], len(pulls_b), ps._ints(pulls_b or [0]),
-                      ps._ptrs([replicas[l].data_ptr() for l in pulls_b] or [0])))
+                      ps._ptrs(dl or [0]), list(pulls_b), dl))
     pdt = cfg.pull_dtype
     gdt = cfg.grad_dtype
     push = lib.ps_push_dtype
@@ -364,12 +424,26 @@ def main():
     sptr = stream.cuda_stream
     pptr = pstream.cuda_stream if pstream is not None else sptr
 
+    def script(steps: int):
+        """The calls of `steps` steps from the start of the plan, for ps_run."""
+        sc = ps.OpScript()
+        for i in range(steps):
+            pushes_b, r, _, _, ids, dl = calls[i % len(calls)]
+            for l, g in pushes_b:
+                sc.push(l, g, gdt)
+            if args.mode == "fused":
+                sc.apply_pull(ids, dl, pdt)
+            else:
+                sc.apply_sync() if args.apply == "sync" else sc.apply()
+                sc.pull(ids, dl, pdt)
+        return sc.build()
+
     # events of step s: 4s = before the apply, 4s+1 = after it (both on the
     # library's stream), 4s+2 / 4s+3 = around the pull on the stream it runs
     # on (with ordered pulls the same point as 4s+1, so 4s+1 serves as both)
     def step(s_=None):
         nonlocal it
-        pushes_b, r, ids, dptr = calls[it % len(calls)]
+        pushes_b, r, ids, dptr, _, _ = calls[it % len(calls)]
         it += 1
         for l, g in pushes_b:
             if push(h, l, g, gdt) != 0:
@@ -393,20 +467,49 @@ def main():
             raise RuntimeError(ps.ps_last_error())
         return r
 
+    def reset():
+        """w := w0, v := 0, timestamp and learner history cleared; the plan
+        restarts at its first step."""
+        nonlocal it
+        if ps.ps_set_weights(h, w0.data_ptr()) != 0:
+            raise RuntimeError(ps.ps_last_error())
+        it = 0
+        torch.cuda.synchronize()
+
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
 
-    evs = HipEvents(lib, 4 * args.steps)
-    rs = []
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for s_ in range(args.steps):
-        rs.append(step(s_))
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
+    # value: median of `runs` runs of exactly K steps, each one native call
+    timed = script(args.steps)
+    rs = [calls[i % len(calls)][1] for i in range(args.steps)]
+    run_s = []
+    for _ in range(args.runs):
+        reset()
+        t0 = time.perf_counter()
+        rc, done = ps.ps_run(h, timed)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        if rc != 0 or done != len(timed):
+            raise RuntimeError(f"ps_run stopped at call {done}: {ps.ps_last_error()}")
+        run_s.append(t1 - t0)
+    elapsed = sorted(run_s)[len(run_s) // 2]
 
-    elapsed = t1 - t0
+    # the same steps driven call by call from Python
+    reset()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    py_elapsed = time.perf_counter() - t0
+
+    # per-kernel durations: events around every kernel, on its stream
+    reset()
+    evs = HipEvents(lib, 4 * args.steps)
+    for s_ in range(args.steps):
+        step(s_)
+    torch.cuda.synchronize()
+
     pushes = K * args.steps
     step_bytes = sum(algorithmic_bytes(cfg, args.mode, r)[0] for r in rs)
     launch_bytes = sum(algorithmic_bytes(cfg, args.mode, r)[1] for r in rs) / args.steps
@@ -433,7 +536,7 @@ def main():
         del a, b
 
     ts = ps.ps_timestamp(h)
-    ceiling = copy_ceiling(torch, ps, lib)
+    refs = reference_rates(torch, ps, lib)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -453,6 +556,13 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(elapsed / args.steps * 1e3, 4),
+        "timing": {
+            "runs": args.runs,
+            "pushes_per_s_each_run": [round(pushes / t, 2) for t in run_s],
+            "value_is": "median run; each run one ps_run call over the prepared steps, after "
+                        "ps_set_weights(w0) reset w, v and the timestamp",
+            "python_driven_pushes_per_s": round(pushes / py_elapsed, 2),
+        },
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -488,7 +598,13 @@ def main():
             "traffic": traffic,
             "algorithmic_bytes_per_launch": round(launch_bytes),
         },
-        "copy_gbps": round(ceiling, 1),
+        "reference_rates": refs,
+        "apply_vs_reference": {
+            "of_8tbps_peak": round(achieved / PEAK_GBPS, 4),
+            "of_torch_sum_read": round(achieved / refs["torch_sum_read_gbps"], 4),
+            "of_hip_memcpy_d2d": round(achieved / refs["hip_memcpy_d2d_gbps"], 4),
+            "of_library_copy": round(achieved / refs["library_copy_gbps"], 4),
+        },
         "cpu_baseline": cpu,
         "timestamp_after": ts,
     }

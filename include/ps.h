@@ -182,7 +182,11 @@ int ps_pull_many(ps_server *ps, int n, const int *learner_ids, void *const *dsts
  * identical to the two calls in sequence. Up to the fusion limit (see
  * ps_set_pull_fusion) the replicas are written from the same pass that
  * updates w, so w is not read again; above it the apply kernel is followed
- * by the tiled fan-out, which serves many replicas faster than one pass. */
+ * by the tiled fan-out, which serves many replicas faster than one pass.
+ * With lock-free pulls on (ps_set_pull_stream) and replicas to write, the
+ * call first makes the server's stream wait for the lock-free pulls already
+ * enqueued, so none of them can overwrite a replica this call marks
+ * current. */
 int ps_apply_pull(ps_server *ps, int n, const int *learner_ids, void *const *dsts, int dst_dtype);
 
 /* Largest replica count ps_apply_pull writes from the apply pass itself
@@ -279,17 +283,30 @@ int ps_last_applied(const ps_server *ps, int *learner_ids, int cap);
  * (>= 0) or a negative status. */
 int ps_drop_learner(ps_server *ps, int learner_id);
 
+/* A learner died (Sec. 4.3) while its gradients sat in the server's own
+ * slots (ps_alloc_rows rows, which outlive the learner): the server is
+ * stateless, so those gradients stay queued and are applied exactly once,
+ * in their turn (Theorem 2, Sec. 4.2), like everyone else's. Later pushes
+ * and pulls under learner_id are refused with PS_ESTATE, until
+ * ps_set_weights or ps_load starts a new run. Returns how many of its
+ * gradients are still queued (>= 0), or a negative status: PS_ESTATE, with
+ * nothing changed, when one of them lies outside the server's rows (a
+ * borrowed buffer may be gone with the learner: use ps_drop_learner). */
+int ps_retire_learner(ps_server *ps, int learner_id);
+
 /* Checkpoint (Sec. 4.3: the server checkpoints its parameters so that a
  * restart resumes from the last checkpoint). ps_save writes w, v, the
- * timestamp, the round-robin position and every learner's timestamp to
- * `path` (waits for the server's stream and lock-free pulls first); ps_load restores them into
- * a server created with the same n_params, lr and momentum, after checking
- * the whole file (format version, sizes, a checksum over header and data)
- * -- on any failure the server is unchanged. Pull history and statistics start afresh after a load (learners
- * pull again after a restart). Both need an empty queue (PS_ESTATE
- * otherwise); file errors give PS_EIO, mismatched servers PS_EINVAL.
- * Continuing from a loaded checkpoint gives the bits of the uninterrupted
- * run. */
+ * timestamp, the queue configuration (mode, depth, slots per learner), the
+ * round-robin position and every learner's timestamp to `path` (waits for
+ * the server's stream and lock-free pulls first); ps_load restores them
+ * into a server created with the same n_params, lr and momentum and set to
+ * the same queue configuration, after checking the whole file (format
+ * version, sizes, a checksum over header and data) -- on any failure the
+ * server is unchanged. Pull history and statistics start afresh after a
+ * load (learners pull again after a restart). Both need an empty queue
+ * (PS_ESTATE otherwise); file errors give PS_EIO, mismatched servers
+ * (sizes, lr, momentum or queue configuration) PS_EINVAL. Continuing from a
+ * loaded checkpoint gives the bits of the uninterrupted run. */
 int ps_save(ps_server *ps, const char *path);
 int ps_load(ps_server *ps, const char *path);
 
@@ -314,6 +331,57 @@ int ps_alloc_rows(ps_server *ps, int count, int dtype, void **rows);
  * waiting for the server's streams. PS_ESTATE (nothing freed) if a pending
  * gradient lies in them; PS_EINVAL if first_row is not such a row. */
 int ps_free_rows(ps_server *ps, void *first_row);
+
+/* Learners in their own processes (Sec. 4.1, 4.3: each learner and the
+ * server has its own address space and all of them map one shared region
+ * holding the gradient slots and the weights). On one GPU the shared region
+ * is the server's rows, shared through HIP IPC.
+ *
+ * ps_export_rows: a handle (PS_IPC_HANDLE_BYTES opaque bytes written to
+ * `handle`) for the device allocation holding the rows of one
+ * ps_alloc_rows call, named by its first row, and the offset of that row in
+ * the allocation. Another process on the same device passes both to
+ * ps_import_rows. The rows stay the server's: they are freed by
+ * ps_free_rows or ps_destroy, after which importers must not touch them.
+ * PS_EINVAL if first_row is not the first row of a row set. */
+#define PS_IPC_HANDLE_BYTES 64
+int ps_export_rows(ps_server *ps, void *first_row, void *handle, size_t *offset);
+
+/* Learner side, in another process, with the server's device current: map
+ * the exported allocation and write the address of its first row (rows
+ * follow at the stride the server's ps_alloc_rows reported). The learner
+ * writes gradients into its slots and reads replicas there; every write must
+ * have completed on the device before the server is told to push it.
+ * ps_release_rows waits for this process's device work, then unmaps. */
+int ps_import_rows(const void *handle, size_t offset, void **first_row);
+int ps_release_rows(void *first_row);
+
+/* One call of the hot path, for ps_run. */
+enum {
+    PS_OP_PUSH = 0,        /* ps_push_dtype(learner_id, grad, dtype)                 */
+    PS_OP_APPLY = 1,       /* ps_apply_pending                                        */
+    PS_OP_APPLY_SYNC = 2,  /* ps_apply_sync                                           */
+    PS_OP_PULL = 3,        /* ps_pull_many(count, learner_ids, dsts, dtype)           */
+    PS_OP_APPLY_PULL = 4   /* ps_apply_pull(count, learner_ids, dsts, dtype)          */
+};
+typedef struct ps_op {
+    int kind;                  /* PS_OP_*                                              */
+    int learner_id;            /* PS_OP_PUSH                                           */
+    int dtype;                 /* gradient dtype (push) or replica dtype (pulls)       */
+    int count;                 /* replicas (pulls)                                     */
+    const void *grad;          /* device gradient (push)                               */
+    const int *learner_ids;    /* count ids (pulls)                                    */
+    void *const *dsts;         /* count device replica buffers (pulls)                 */
+} ps_op;
+
+/* Run a script of hot-path calls in order, each exactly as the call it
+ * names (same validation, results and errors), under one acquisition of
+ * the handle's lock -- the server loop of Sec. 4.1 driven from a prepared
+ * schedule without a host-language round trip per call. Stops at the first
+ * call that does not return PS_OK (a full queue included) and returns its
+ * status; *done (may be NULL) receives the number of calls completed.
+ * PS_EINVAL for an unknown kind or ops == NULL with count > 0. */
+int ps_run(ps_server *ps, const ps_op *ops, int count, int *done);
 
 /* Block until all work enqueued by the server has completed. */
 int ps_sync(ps_server *ps);

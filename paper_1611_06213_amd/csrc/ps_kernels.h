@@ -34,34 +34,31 @@ struct PullArgs {
 
 // Launch geometry: blocks are 256 threads; max_blocks caps the grid (the
 // kernels then stride over the remaining chunks). 0 = one chunk per lane.
-// fp32-gradient kernels reserve LDS so that only a few blocks fit per
-// compute unit: occupancy_cap_lds leaves room for one, occupancy_cap2_lds
-// for two (0 = no reservation; both chosen at server creation for the
-// current device). Asynchronous applies take two blocks per CU from
-// occupancy_cap2_min_k gradients on, one from occupancy_cap_min_k_momentum
-// on when they carry momentum; synchronous steps take one from
-// occupancy_cap_min_k on.
+// fp32-gradient kernels may reserve LDS (they use none) so that only a few
+// blocks fit per compute unit: lds_for_blocks[b] leaves room for exactly b
+// blocks (b = 1..4; 0 = no such reservation on this device; chosen at server
+// creation). An asynchronous apply is told how many blocks to allow
+// (apply_shape_f32, ps_layout.h); synchronous steps take one block per CU
+// from sync_one_block_min_k gradients on.
 struct Geometry {
     int max_blocks = 0;
     int fronts_log2 = -1;   // -1: chosen per apply (fronts_log2_for, ps_layout.h)
-    unsigned occupancy_cap_lds = 0;
-    unsigned occupancy_cap2_lds = 0;
-    int occupancy_cap_min_k = 16;
-    int occupancy_cap2_min_k = 8;
-    int occupancy_cap_min_k_momentum = 24;
+    unsigned lds_for_blocks[5] = {0, 0, 0, 0, 0};
+    int sync_one_block_min_k = 16;
 };
 
-// LDS bytes that leave room for exactly `blocks` (1 or 2) blocks per compute
+// LDS bytes that leave room for exactly `blocks` (1..4) blocks per compute
 // unit on the current device, or 0 if the device does not allow such a
 // reservation.
 unsigned blocks_per_cu_lds(int blocks);
 
-
 // grad_dtype: PS_F32 | PS_BF16. pull_dtype: -1 (no replicas), PS_F32, PS_BF16.
 // level: 2 = every buffer 16-byte aligned; 1 = fp32 buffers 16-byte and bf16
 // buffers 8-byte aligned; 0 = anything else (scalar kernels).
+// blocks_per_cu: 1..4 resident blocks per compute unit for fp32 gradients
+// (0 = as many as fit; ignored for bf16 gradients and the scalar kernels).
 hipError_t launch_apply(const ApplyArgs &a, int grad_dtype, int pull_dtype, int level,
-                        const Geometry &geo, hipStream_t s);
+                        int blocks_per_cu, const Geometry &geo, hipStream_t s);
 hipError_t launch_pull(const PullArgs &a, int pull_dtype, int level, const Geometry &geo,
                        hipStream_t s);
 // Synchronous step over a.k gradients of one dtype (no replicas).

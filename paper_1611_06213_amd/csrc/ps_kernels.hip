@@ -62,6 +62,18 @@ static_assert(kGroup >= 1 && kGroup <= 16, "gradient group size must be 1..16");
 // again until the next apply, after tens of GB of other traffic: stream them
 // with the non-temporal hint too.
 constexpr bool kNtWV = PS_NT_WV != 0;
+// The same choice for the 8-coordinate chunks of bf16-gradient applies, for
+// loads and stores separately.
+#ifndef PS_NT_WV_LD8
+#define PS_NT_WV_LD8 PS_NT_WV
+#endif
+#ifndef PS_NT_WV_ST8
+#define PS_NT_WV_ST8 PS_NT_WV
+#endif
+template <int E>
+constexpr bool nt_wv_ld() { return E == 8 ? PS_NT_WV_LD8 != 0 : kNtWV; }
+template <int E>
+constexpr bool nt_wv_st() { return E == 8 ? PS_NT_WV_ST8 != 0 : kNtWV; }
 
 // A launch's work-items (blocks * threads) must stay below 2^32.
 constexpr uint64_t kMaxBlocks = 0xffffffffull / kBlock;
@@ -219,8 +231,8 @@ __device__ __forceinline__ void apply_group(const ApplyArgs &a, int k0, uint64_t
 template <bool MOM, int GDT, int PDT, int E>
 __device__ __forceinline__ void apply_chunk(const ApplyArgs &a, uint64_t i) {
     float w[E], v[E];
-    ld_f32<E, kNtWV>(w, a.w + i);
-    if constexpr (MOM) ld_f32<E, kNtWV>(v, a.v + i);
+    ld_f32<E, nt_wv_ld<E>()>(w, a.w + i);
+    if constexpr (MOM) ld_f32<E, nt_wv_ld<E>()>(v, a.v + i);
     const float lr = a.lr;
     const float m = a.m;
     const int k = a.k;
@@ -241,8 +253,8 @@ __device__ __forceinline__ void apply_chunk(const ApplyArgs &a, uint64_t i) {
         for (int j = 0; j < 8; ++j)
             if (k0 + j < k) step<MOM, E>(w, v, g[j], lr, m);
     }
-    st_f32<E, kNtWV>(a.w + i, w);
-    if constexpr (MOM) st_f32<E, kNtWV>(a.v + i, v);
+    st_f32<E, nt_wv_st<E>()>(a.w + i, w);
+    if constexpr (MOM) st_f32<E, nt_wv_st<E>()>(a.v + i, v);
     if constexpr (PDT >= 0) {
         for (int r = 0; r < a.r; ++r) st_dst<PDT, E>(a.dst[r], i, w);
     }
@@ -266,8 +278,8 @@ __device__ __forceinline__ void sum_group(const ApplyArgs &a, int k0, uint64_t i
 template <bool MOM, int GDT, int E>
 __device__ __forceinline__ void sync_chunk(const ApplyArgs &a, uint64_t i) {
     float w[E], v[E], s[E];
-    ld_f32<E, kNtWV>(w, a.w + i);
-    if constexpr (MOM) ld_f32<E, kNtWV>(v, a.v + i);
+    ld_f32<E, nt_wv_ld<E>()>(w, a.w + i);
+    if constexpr (MOM) ld_f32<E, nt_wv_ld<E>()>(v, a.v + i);
 #pragma unroll
     for (int e = 0; e < E; ++e) s[e] = 0.0f;
     const int k = a.k;
@@ -295,8 +307,8 @@ __device__ __forceinline__ void sync_chunk(const ApplyArgs &a, uint64_t i) {
 #pragma unroll
     for (int e = 0; e < E; ++e) avg[e] = s[e] / kf;
     step<MOM, E>(w, v, avg, a.lr, a.m);
-    st_f32<E, kNtWV>(a.w + i, w);
-    if constexpr (MOM) st_f32<E, kNtWV>(a.v + i, v);
+    st_f32<E, nt_wv_st<E>()>(a.w + i, w);
+    if constexpr (MOM) st_f32<E, nt_wv_st<E>()>(a.v + i, v);
 }
 
 // Blocks are dispatched in index order. With F = 2^f fronts, block b works
@@ -488,7 +500,7 @@ unsigned grid_for(uint64_t items, const Geometry &geo) {
 }
 
 template <bool MOM, int GDT, int PDT>
-hipError_t go_apply(const ApplyArgs &a, int level, const Geometry &geo, hipStream_t s) {
+hipError_t go_apply(const ApplyArgs &a, int level, int bpc, const Geometry &geo, hipStream_t s) {
     if (level == 0) {
         hipLaunchKernelGGL((apply_scalar<MOM, GDT, PDT>), dim3(grid_for(a.n, geo)), dim3(kBlock),
                            0, s, a);
@@ -497,22 +509,12 @@ hipError_t go_apply(const ApplyArgs &a, int level, const Geometry &geo, hipStrea
     // bf16 gradients move 16 bytes per lane as 8 values when every buffer is
     // 16-byte aligned; otherwise (and for fp32) a lane's chunk is 4 values.
     const bool e8 = GDT == PS_BF16 && level == 2;
-    // fp32 gradients: with 8 or more gradients per apply each lane keeps
-    // many 16-byte loads in flight; a few blocks per CU then saturate HBM,
-    // and fewer resident waves keep fewer DRAM pages and translations live
-    // at once across the K+2 streams, which measured faster and steadier.
-    // The kernel uses no LDS: the reservation only limits residency.
-    // Measured at the VGG-16 size: two blocks per CU from K = 8, one from
-    // K = 24 with momentum (K = 32: one block 3.24 ms, two 3.36, full
-    // residency 3.55; K = 12: two blocks 1.41 ms, one 1.70, full 1.51-1.52;
-    // without momentum K = 32: two blocks 3.06 ms, one 3.60, full
-    // 3.19-3.28; K = 8: two blocks 0.88 ms, full 0.92-0.95). Below K = 8
-    // full residency was best. bf16 gradients (half the bytes per value)
-    // measured best at full residency.
+    // fp32 gradients: the caller's residency (apply_shape_f32), reserved via
+    // dynamic LDS that the kernel does not use. bf16 gradients (half the
+    // bytes per value) measured best at full residency.
     unsigned lds = 0;
     if constexpr (GDT == PS_F32) {
-        if (a.k >= geo.occupancy_cap2_min_k) lds = geo.occupancy_cap2_lds;
-        if (MOM && a.k >= geo.occupancy_cap_min_k_momentum) lds = geo.occupancy_cap_lds;
+        if (bpc >= 1 && bpc <= 4) lds = geo.lds_for_blocks[bpc];
     }
     if constexpr (GDT == PS_BF16) {
         if (e8) {
@@ -533,8 +535,10 @@ hipError_t go_sync(const ApplyArgs &a, int level, const Geometry &geo, hipStream
                            a);
         return hipGetLastError();
     }
+    // one block per CU from sync_one_block_min_k fp32 gradients on (VGG-16
+    // size, 16 learners: 1.58-1.61 ms vs 1.62 with two blocks, 1.74 full)
     const unsigned lds =
-        (GDT == PS_F32 && a.k >= geo.occupancy_cap_min_k) ? geo.occupancy_cap_lds : 0;
+        (GDT == PS_F32 && a.k >= geo.sync_one_block_min_k) ? geo.lds_for_blocks[1] : 0;
     if constexpr (GDT == PS_BF16) {
         if (level == 2) {
             hipLaunchKernelGGL((sync_vec<MOM, GDT, 8>), dim3(grid_for(a.n / 8, geo)),
@@ -548,26 +552,28 @@ hipError_t go_sync(const ApplyArgs &a, int level, const Geometry &geo, hipStream
 }
 
 template <bool MOM, int GDT>
-hipError_t go_apply_p(const ApplyArgs &a, int pdt, int level, const Geometry &geo, hipStream_t s) {
-    if (pdt == PS_F32) return go_apply<MOM, GDT, PS_F32>(a, level, geo, s);
-    if (pdt == PS_BF16) return go_apply<MOM, GDT, PS_BF16>(a, level, geo, s);
-    return go_apply<MOM, GDT, -1>(a, level, geo, s);
+hipError_t go_apply_p(const ApplyArgs &a, int pdt, int level, int bpc, const Geometry &geo,
+                      hipStream_t s) {
+    if (pdt == PS_F32) return go_apply<MOM, GDT, PS_F32>(a, level, bpc, geo, s);
+    if (pdt == PS_BF16) return go_apply<MOM, GDT, PS_BF16>(a, level, bpc, geo, s);
+    return go_apply<MOM, GDT, -1>(a, level, bpc, geo, s);
 }
 
 template <bool MOM>
-hipError_t go_apply_g(const ApplyArgs &a, int gdt, int pdt, int level, const Geometry &geo,
-                      hipStream_t s) {
-    if (gdt == PS_BF16) return go_apply_p<MOM, PS_BF16>(a, pdt, level, geo, s);
-    return go_apply_p<MOM, PS_F32>(a, pdt, level, geo, s);
+hipError_t go_apply_g(const ApplyArgs &a, int gdt, int pdt, int level, int bpc,
+                      const Geometry &geo, hipStream_t s) {
+    if (gdt == PS_BF16) return go_apply_p<MOM, PS_BF16>(a, pdt, level, bpc, geo, s);
+    return go_apply_p<MOM, PS_F32>(a, pdt, level, bpc, geo, s);
 }
 
 }  // namespace
 
 hipError_t launch_apply(const ApplyArgs &a, int grad_dtype, int pull_dtype, int level,
-                        const Geometry &geo, hipStream_t s) {
+                        int blocks_per_cu, const Geometry &geo, hipStream_t s) {
     if (a.r == 0) pull_dtype = -1;
-    if (a.v != nullptr) return go_apply_g<true>(a, grad_dtype, pull_dtype, level, geo, s);
-    return go_apply_g<false>(a, grad_dtype, pull_dtype, level, geo, s);
+    if (a.v != nullptr)
+        return go_apply_g<true>(a, grad_dtype, pull_dtype, level, blocks_per_cu, geo, s);
+    return go_apply_g<false>(a, grad_dtype, pull_dtype, level, blocks_per_cu, geo, s);
 }
 
 template <int PDT, int E>

@@ -43,4 +43,22 @@ int fronts_log2_for(const void *const *ptrs, int count) {
     return (streams >= 8 && 2 * most > streams) ? 2 : 0;
 }
 
+ApplyShape apply_shape_f32(int k, bool momentum) {
+    if (momentum) {
+        if (k <= 1) return {0, 0};
+        if (k == 2) return {4, 0};
+        if (k <= 5) return {3, 0};
+        if (k == 16) return {1, 0};
+        if (k <= 23) return {2, 0};
+        return {1, 0};
+    }
+    if (k <= 2) return {0, 0};
+    if (k == 3) return {4, 0};
+    if (k <= 7) return {3, 0};
+    if (k <= 11) return {2, 0};
+    if (k <= 23) return {3, 1};
+    if (k <= 31) return {2, 1};
+    return {2, 0};
+}
+
 }  // namespace gadei

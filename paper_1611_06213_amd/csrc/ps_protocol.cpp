@@ -45,6 +45,7 @@ int Protocol::push(int learner, int dtype, const void *grad, void *ready) {
     if (int rc = check_learner(learner)) return rc;
     if (grad == nullptr) return fail(PS_EINVAL, "null gradient");
     if (dtype != PS_F32 && dtype != PS_BF16) return fail(PS_EINVAL, "bad gradient dtype %d", dtype);
+    if (retired(learner)) return fail(PS_ESTATE, "learner %d has retired", learner);
     const uint64_t lts =
         static_cast<size_t>(learner) < learner_ts.size() ? learner_ts[learner] : 0;
     const PushDesc d{learner, dtype, grad, lts, ready};
@@ -191,6 +192,7 @@ int Protocol::plan_pulls(int n, const int *ids, void *const *dsts, int dtype, ui
     for (int i = 0; i < n; ++i) {
         if (int rc = check_learner(ids[i])) return rc;
         if (dsts[i] == nullptr) return fail(PS_EINVAL, "null destination %d", i);
+        if (retired(ids[i])) return fail(PS_ESTATE, "learner %d has retired", ids[i]);
         const int l = ids[i];
         bool current = false;
         if (pull_skip) {
@@ -259,6 +261,25 @@ int Protocol::drop_learner(int learner) {
     return dropped;
 }
 
+int Protocol::retire_learner(int learner) {
+    if (int rc = check_learner(learner)) return rc;
+    retired_.insert(learner);
+    return static_cast<int>(queued_of(learner).size());
+}
+
+bool Protocol::retired(int learner) const { return retired_.count(learner) != 0; }
+
+std::vector<PushDesc> Protocol::queued_of(int learner) const {
+    std::vector<PushDesc> out;
+    if (mode == PS_QUEUE_FIFO) {
+        for (const PushDesc &d : fifo_)
+            if (d.learner == learner) out.push_back(d);
+    } else if (learner >= 0 && static_cast<size_t>(learner) < rr_.size()) {
+        out.assign(rr_[learner].begin(), rr_[learner].end());
+    }
+    return out;
+}
+
 int Protocol::set_depth(int new_depth) {
     if (new_depth < 1 || new_depth > PS_MAX_QUEUE_DEPTH)
         return fail(PS_EINVAL, "queue depth %d outside [1, %d]", new_depth, PS_MAX_QUEUE_DEPTH);
@@ -283,6 +304,7 @@ int Protocol::set_mode(int new_mode, int slots_per_learner) {
 }
 
 void Protocol::reset() {
+    retired_.clear();
     ts = 0;
     learner_ts.clear();
     last_pull.clear();
@@ -292,6 +314,7 @@ void Protocol::reset() {
 }
 
 void Protocol::restore(uint64_t new_ts, int new_last_served, const std::vector<uint64_t> &lts) {
+    retired_.clear();
     ts = new_ts;
     last_served = new_last_served;
     learner_ts = lts;

@@ -114,6 +114,14 @@ struct Protocol {
 
     // Discard a dead learner's queued gradients (Sec. 4.3); returns the count.
     int drop_learner(int learner);
+    // A dead learner whose queued gradients stay queued and are applied in
+    // their turn (the stateless server of Sec. 4.3; Theorem 2): later pushes
+    // and pulls under its id are refused with PS_ESTATE until reset() or
+    // restore(). Returns how many of its gradients are still queued.
+    int retire_learner(int learner);
+    bool retired(int learner) const;
+    // The queued gradients of one learner, oldest first.
+    std::vector<PushDesc> queued_of(int learner) const;
     int set_depth(int new_depth);
     int set_mode(int new_mode, int slots_per_learner);
     // New weights: timestamp 0, every learner at 0, history and stats cleared.
@@ -126,6 +134,7 @@ struct Protocol {
     std::vector<std::deque<PushDesc>> rr_;   // round robin: queue of each learner id
     std::set<int> waiting_;                  // ... ids whose queue is not empty
     size_t rr_count_ = 0;
+    std::set<int> retired_;                  // learners retired (retire_learner)
 
     void grow(int id);
     void consume(const Batch &b);

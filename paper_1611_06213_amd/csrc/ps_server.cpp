@@ -13,6 +13,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <map>
 #include <mutex>
 #include <new>
 #include <vector>
@@ -51,6 +52,9 @@ struct ps_server {
     hipStream_t stream = nullptr;
     hipStream_t pull_stream = nullptr;   // lock-free pulls when pull_lock_free
     bool pull_lock_free = false;
+    // recorded on pull_stream so that ps_apply_pull's replica writes follow
+    // earlier lock-free pulls into the same buffers
+    hipEvent_t pulls_done = nullptr;
     int fuse_max_r = 1;   // ps_apply_pull writes up to this many replicas in the apply pass
     gadei::Geometry geo;
     gadei::Protocol proto;
@@ -139,16 +143,20 @@ int drain_pulls(ps_server *ps) {
     return PS_OK;
 }
 
-// Fronts for an apply over a.g[0..k), w and v: the server's setting, or
-// chosen from the buffers' offsets (fronts_log2_for).
-int fronts_for(const ps_server *ps, const gadei::ApplyArgs &a) {
+// Fronts for an apply over a.g[0..k) of dtype gdt, w and v: the server's
+// setting, or chosen from the buffers' offsets (fronts_log2_for), and for
+// fp32 gradients at distinct offsets from the gradient count
+// (apply_shape_f32).
+int fronts_for(const ps_server *ps, const gadei::ApplyArgs &a, int gdt) {
     if (ps->geo.fronts_log2 >= 0) return ps->geo.fronts_log2;
     const void *p[PS_MAX_QUEUE_DEPTH + 2];
     int c = 0;
     for (int j = 0; j < a.k; ++j) p[c++] = a.g[j];
     p[c++] = a.w;
     p[c++] = a.v;   // null without momentum: not a stream
-    return gadei::fronts_log2_for(p, c);
+    const int f = gadei::fronts_log2_for(p, c);
+    if (f == 0 && gdt == PS_F32) return gadei::apply_shape_f32(a.k, a.v != nullptr).fronts_log2;
+    return f;
 }
 
 // Launch a batch as runs of equal gradient dtype, in order. The last run
@@ -176,7 +184,9 @@ int launch_batch(ps_server *ps, const std::vector<PushDesc> &items, int pull_dty
         }
         a.k = static_cast<int>(end - start);
         a.r = 0;
-        a.fronts_log2 = fronts_for(ps, a);
+        a.fronts_log2 = fronts_for(ps, a, gdt);
+        const int bpc =
+            gdt == PS_F32 ? gadei::apply_shape_f32(a.k, a.v != nullptr).blocks_per_cu : 0;
         int pdt = -1;
         if (end == q && pull_dtype >= 0 && !write.empty()) {
             pdt = pull_dtype;
@@ -186,10 +196,22 @@ int launch_batch(ps_server *ps, const std::vector<PushDesc> &items, int pull_dty
                 level = std::min(level, level_of(a.dst[j], pull_dtype));
             }
         }
-        hipError_t e = gadei::launch_apply(a, gdt, pdt, level, ps->geo, ps->stream);
+        hipError_t e = gadei::launch_apply(a, gdt, pdt, level, bpc, ps->geo, ps->stream);
         if (e != hipSuccess) return fail_hip(e, "apply kernel launch");
         start = end;
     }
+    return PS_OK;
+}
+
+// Make the server's stream wait (on the device) for every lock-free pull
+// enqueued so far. ps_apply_pull marks its replicas current; without this an
+// earlier lock-free pull into the same buffer, still running on the pull
+// stream, could land after the newer weights.
+int order_after_pulls(ps_server *ps) {
+    if (!ps->pull_lock_free) return PS_OK;
+    hipError_t e = hipEventRecord(ps->pulls_done, ps->pull_stream);
+    if (e == hipSuccess) e = hipStreamWaitEvent(ps->stream, ps->pulls_done, 0);
+    if (e != hipSuccess) return fail_hip(e, "ordering after lock-free pulls");
     return PS_OK;
 }
 
@@ -232,11 +254,16 @@ struct CkptHeader {
     uint64_t ts;
     int64_t last_served;
     uint64_t n_learner_ts;
+    int32_t queue_mode;   // the queue configuration the run was made with:
+    int32_t depth;        // a restart under another one would serve the
+    int32_t slots;        // gradients in another order
+    int32_t reserved;
     uint64_t checksum;
 };
 
 constexpr char kMagic[8] = {'G', 'A', 'D', 'E', 'I', 'P', 'S', '1'};
-constexpr uint32_t kVersion = 2;   // 2: the checksum covers the header too
+// 2: the checksum covers the header too; 3: the queue configuration is kept
+constexpr uint32_t kVersion = 3;
 constexpr size_t kChunk = size_t(16) << 20;   // floats per device<->host copy
 
 struct Fnv {
@@ -266,11 +293,50 @@ int save_array(FILE *f, const float *dev, size_t n, std::vector<float> &buf, Fnv
     return PS_OK;
 }
 
+// Row sets this process mapped with ps_import_rows: first row -> the base
+// hipIpcOpenMemHandle returned.
+std::mutex g_import_mu;
+std::map<void *, void *> g_imports;
+
 }  // namespace
 
 extern "C" {
 
 const char *ps_last_error(void) { return gadei::last_error(); }
+
+int ps_import_rows(const void *handle, size_t offset, void **first_row) {
+    if (handle == nullptr || first_row == nullptr) return fail(PS_EINVAL, "null argument");
+    hipIpcMemHandle_t h;
+    std::memcpy(&h, handle, sizeof h);
+    void *base = nullptr;
+    hipError_t e = hipIpcOpenMemHandle(&base, h, hipIpcMemLazyEnablePeerAccess);
+    if (e != hipSuccess) return fail_hip(e, "hipIpcOpenMemHandle");
+    void *first = static_cast<char *>(base) + offset;
+    try {
+        std::lock_guard<std::mutex> lock(g_import_mu);
+        g_imports[first] = base;
+    } catch (...) {
+        (void)hipIpcCloseMemHandle(base);
+        return fail(PS_ENOMEM, "host allocation failed");
+    }
+    *first_row = first;
+    return PS_OK;
+}
+
+int ps_release_rows(void *first_row) {
+    void *base = nullptr;
+    {
+        std::lock_guard<std::mutex> lock(g_import_mu);
+        auto it = g_imports.find(first_row);
+        if (it == g_imports.end()) return fail(PS_EINVAL, "not a row set imported here");
+        base = it->second;
+        g_imports.erase(it);
+    }
+    hipError_t e = hipDeviceSynchronize();
+    if (e == hipSuccess) e = hipIpcCloseMemHandle(base);
+    if (e != hipSuccess) return fail_hip(e, "hipIpcCloseMemHandle");
+    return PS_OK;
+}
 
 ps_server *ps_create(size_t n_params, float lr, float momentum) {
     if (n_params == 0 || n_params > (size_t(1) << 48)) {
@@ -308,8 +374,7 @@ ps_server *ps_create(size_t n_params, float lr, float momentum) {
         delete ps;
         return nullptr;
     }
-    ps->geo.occupancy_cap_lds = gadei::blocks_per_cu_lds(1);
-    ps->geo.occupancy_cap2_lds = gadei::blocks_per_cu_lds(2);
+    for (int b = 1; b <= 4; ++b) ps->geo.lds_for_blocks[b] = gadei::blocks_per_cu_lds(b);
     return ps;
 }
 
@@ -322,6 +387,7 @@ void ps_destroy(ps_server *ps) {
             if (ps->pull_lock_free) (void)hipStreamSynchronize(ps->pull_stream);
             for (const RowSet &r : ps->row_sets) (void)hipFree(r.base);
             (void)hipFree(ps->wv_base);
+            if (ps->pulls_done) (void)hipEventDestroy(ps->pulls_done);
         }
     }
     delete ps;
@@ -426,7 +492,7 @@ int ps_apply_sync(ps_server *ps) {
         a.g[j] = b.items[j].grad;
         level = std::min(level, level_of(a.g[j], gdt));
     }
-    a.fronts_log2 = fronts_for(ps, a);
+    a.fronts_log2 = fronts_for(ps, a, -1);   // the phase rule only (no apply_shape_f32)
     hipError_t e = gadei::launch_sync(a, gdt, level, ps->geo, ps->stream);
     if (e != hipSuccess) return fail_hip(e, "synchronous step launch");
     ps->proto.commit_sync(b);
@@ -468,6 +534,8 @@ int ps_apply_pull(ps_server *ps, int n, const int *learner_ids, void *const *dst
         return rc;
     if (int rc = check_dsts(ps, n, dsts, dst_dtype)) return rc;
     if (int rc = use_device(ps)) return rc;
+    if (!write.empty())
+        if (int rc = order_after_pulls(ps)) return rc;
     if (static_cast<int>(write.size()) <= ps->fuse_max_r) {
         if (int rc = launch_batch(ps, b.items, dst_dtype, dsts, write)) return rc;
     } else {
@@ -487,6 +555,45 @@ int ps_drop_learner(ps_server *ps, int learner_id) {
     if (int rc = check(ps)) return rc;
     PS_LOCK(ps);
     return ps->proto.drop_learner(learner_id);
+}
+
+int ps_retire_learner(ps_server *ps, int learner_id) {
+    if (int rc = check(ps)) return rc;
+    PS_LOCK(ps);
+    if (int rc = gadei::check_learner(learner_id)) return rc;
+    // its gradients stay queued, so they must live in memory the server
+    // owns: a borrowed buffer may have gone with the learner
+    for (const PushDesc &d : ps->proto.queued_of(learner_id)) {
+        const char *g = static_cast<const char *>(d.grad);
+        const size_t bytes = ps->n * elem_bytes(d.dtype);
+        const bool owned = std::any_of(ps->row_sets.begin(), ps->row_sets.end(), [&](const RowSet &r) {
+            return g >= r.first && g <= r.end && bytes <= static_cast<size_t>(r.end - g);
+        });
+        if (!owned)
+            return fail(PS_ESTATE,
+                        "learner %d has a queued gradient outside the server's rows; drop it "
+                        "(ps_drop_learner) instead",
+                        learner_id);
+    }
+    return ps->proto.retire_learner(learner_id);
+}
+
+static_assert(sizeof(hipIpcMemHandle_t) == PS_IPC_HANDLE_BYTES, "IPC handle size");
+
+int ps_export_rows(ps_server *ps, void *first_row, void *handle, size_t *offset) {
+    if (int rc = check(ps)) return rc;
+    PS_LOCK(ps);
+    if (handle == nullptr || offset == nullptr) return fail(PS_EINVAL, "null output");
+    auto it = std::find_if(ps->row_sets.begin(), ps->row_sets.end(),
+                           [&](const RowSet &r) { return r.first == first_row; });
+    if (it == ps->row_sets.end()) return fail(PS_EINVAL, "not the first row of a row set");
+    if (int rc = use_device(ps)) return rc;
+    hipIpcMemHandle_t h;
+    hipError_t e = hipIpcGetMemHandle(&h, it->base);
+    if (e != hipSuccess) return fail_hip(e, "hipIpcGetMemHandle");
+    std::memcpy(handle, &h, sizeof h);
+    *offset = static_cast<size_t>(it->first - static_cast<char *>(it->base));
+    return PS_OK;
 }
 
 int ps_save(ps_server *ps, const char *path) {
@@ -512,6 +619,9 @@ int ps_save(ps_server *ps, const char *path) {
     h.ts = pr.ts;
     h.last_served = pr.last_served;
     h.n_learner_ts = pr.learner_ts.size();
+    h.queue_mode = pr.mode;
+    h.depth = pr.depth;
+    h.slots = pr.mode == PS_QUEUE_ROUND_ROBIN ? pr.slots : 0;
     Fnv fnv;
     int rc = write_all(f, &h, sizeof h, &fnv);   // checksum still zero here
     std::vector<float> buf;
@@ -552,6 +662,13 @@ int ps_load(ps_server *ps, const char *path) {
     else if (std::memcmp(&h.lr, &ps->lr, sizeof(float)) != 0 ||
              std::memcmp(&h.m, &ps->m, sizeof(float)) != 0)
         rc = fail(PS_EINVAL, "checkpoint lr/momentum differ from the server's");
+    else if (h.queue_mode != ps->proto.mode || h.depth != ps->proto.depth ||
+             h.slots != (ps->proto.mode == PS_QUEUE_ROUND_ROBIN ? ps->proto.slots : 0))
+        rc = fail(PS_EINVAL,
+                  "checkpoint queue configuration (mode %d, depth %d, slots %d) differs from "
+                  "the server's (mode %d, depth %d, slots %d)",
+                  h.queue_mode, h.depth, h.slots, ps->proto.mode, ps->proto.depth,
+                  ps->proto.mode == PS_QUEUE_ROUND_ROBIN ? ps->proto.slots : 0);
     else if (h.n_learner_ts > static_cast<uint64_t>(PS_MAX_LEARNERS) || h.last_served < -1 ||
              h.last_served >= PS_MAX_LEARNERS)
         rc = fail(PS_EIO, "corrupt checkpoint (learner table)");
@@ -689,6 +806,28 @@ int ps_last_applied(const ps_server *ps, int *learner_ids, int cap) {
     return count;
 }
 
+int ps_run(ps_server *ps, const ps_op *ops, int count, int *done) {
+    if (done) *done = 0;
+    if (int rc = check(ps)) return rc;
+    if (count < 0 || (count > 0 && ops == nullptr)) return fail(PS_EINVAL, "bad op script");
+    PS_LOCK(ps);
+    for (int i = 0; i < count; ++i) {
+        const ps_op &o = ops[i];
+        int rc;
+        switch (o.kind) {
+            case PS_OP_PUSH: rc = ps_push_dtype(ps, o.learner_id, o.grad, o.dtype); break;
+            case PS_OP_APPLY: rc = ps_apply_pending(ps); break;
+            case PS_OP_APPLY_SYNC: rc = ps_apply_sync(ps); break;
+            case PS_OP_PULL: rc = ps_pull_many(ps, o.count, o.learner_ids, o.dsts, o.dtype); break;
+            case PS_OP_APPLY_PULL: rc = ps_apply_pull(ps, o.count, o.learner_ids, o.dsts, o.dtype); break;
+            default: rc = fail(PS_EINVAL, "op %d: unknown kind %d", i, o.kind);
+        }
+        if (rc != PS_OK) return rc;
+        if (done) *done = i + 1;
+    }
+    return PS_OK;
+}
+
 int ps_sync(ps_server *ps) {
     if (int rc = check(ps)) return rc;
     hipStream_t s, ps_s;
@@ -726,6 +865,13 @@ int ps_set_pull_stream(ps_server *ps, void *hip_stream) {
     PS_LOCK(ps);
     if (int rc = use_device(ps)) return rc;
     if (int rc = drain_pulls(ps)) return rc;
+    if (hip_stream != nullptr && ps->pulls_done == nullptr) {
+        hipError_t e = hipEventCreateWithFlags(&ps->pulls_done, hipEventDisableTiming);
+        if (e != hipSuccess) {
+            ps->pulls_done = nullptr;
+            return fail_hip(e, "hipEventCreateWithFlags");
+        }
+    }
     ps->pull_lock_free = hip_stream != nullptr;
     ps->pull_stream = static_cast<hipStream_t>(hip_stream);
     return PS_OK;

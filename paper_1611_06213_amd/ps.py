@@ -9,6 +9,8 @@ from __future__ import annotations
 
 import ctypes
 import os
+import threading
+from collections import deque
 from typing import Optional, Sequence
 
 PS_OK = 0
@@ -30,6 +32,7 @@ PS_MAX_REPLICAS = 64
 PS_MAX_LEARNERS = 65536
 PS_STALENESS_BINS = 64
 PS_MAX_ROWS = 4096
+PS_IPC_HANDLE_BYTES = 64
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libgadeips.so")
@@ -44,6 +47,21 @@ class ps_stats(ctypes.Structure):
         ("pulls_skipped", _u64),
         ("staleness_max", _u64), ("staleness_sum", _u64),
         ("staleness_hist", _u64 * PS_STALENESS_BINS),
+    ]
+
+
+PS_OP_PUSH = 0
+PS_OP_APPLY = 1
+PS_OP_APPLY_SYNC = 2
+PS_OP_PULL = 3
+PS_OP_APPLY_PULL = 4
+
+
+class ps_op(ctypes.Structure):
+    _fields_ = [
+        ("kind", ctypes.c_int), ("learner_id", ctypes.c_int), ("dtype", ctypes.c_int),
+        ("count", ctypes.c_int), ("grad", ctypes.c_void_p),
+        ("learner_ids", ctypes.POINTER(ctypes.c_int)), ("dsts", ctypes.POINTER(ctypes.c_void_p)),
     ]
 
 
@@ -79,9 +97,15 @@ _SIGS = {
     "ps_pending": (ctypes.c_int, [_VP]),
     "ps_last_staleness": (ctypes.c_int, [_VP, ctypes.POINTER(ctypes.c_int64), ctypes.c_int]),
     "ps_drop_learner": (ctypes.c_int, [_VP, ctypes.c_int]),
+    "ps_retire_learner": (ctypes.c_int, [_VP, ctypes.c_int]),
+    "ps_export_rows": (ctypes.c_int, [_VP, _VP, _VP, ctypes.POINTER(ctypes.c_size_t)]),
+    "ps_import_rows": (ctypes.c_int, [_VP, ctypes.c_size_t, ctypes.POINTER(_VP)]),
+    "ps_release_rows": (ctypes.c_int, [_VP]),
     "ps_save": (ctypes.c_int, [_VP, ctypes.c_char_p]),
     "ps_load": (ctypes.c_int, [_VP, ctypes.c_char_p]),
     "ps_sync": (ctypes.c_int, [_VP]),
+    "ps_run": (ctypes.c_int, [_VP, ctypes.POINTER(ps_op), ctypes.c_int,
+                              ctypes.POINTER(ctypes.c_int)]),
     "ps_get_stats": (ctypes.c_int, [_VP, ctypes.POINTER(ps_stats)]),
     "ps_alloc_rows": (ctypes.c_int, [_VP, ctypes.c_int, ctypes.c_int, ctypes.POINTER(_VP)]),
     "ps_free_rows": (ctypes.c_int, [_VP, _VP]),
@@ -256,6 +280,31 @@ def ps_drop_learner(h: int, learner_id: int) -> int:
     return load_library().ps_drop_learner(h, learner_id)
 
 
+def ps_retire_learner(h: int, learner_id: int) -> int:
+    return load_library().ps_retire_learner(h, learner_id)
+
+
+def ps_export_rows(h: int, first_row: int):
+    """(status, handle bytes, offset of the first row in the allocation)."""
+    buf = ctypes.create_string_buffer(PS_IPC_HANDLE_BYTES)
+    off = ctypes.c_size_t()
+    rc = load_library().ps_export_rows(h, first_row, buf, ctypes.byref(off))
+    return rc, (buf.raw if rc == PS_OK else b""), off.value
+
+
+def ps_import_rows(handle: bytes, offset: int):
+    """(status, address of the first row mapped into this process)."""
+    if len(handle) != PS_IPC_HANDLE_BYTES:
+        return PS_EINVAL, 0
+    out = _VP()
+    rc = load_library().ps_import_rows(handle, offset, ctypes.byref(out))
+    return rc, (out.value or 0)
+
+
+def ps_release_rows(first_row: int) -> int:
+    return load_library().ps_release_rows(first_row)
+
+
 def ps_save(h: int, path: str) -> int:
     return load_library().ps_save(h, os.fsencode(path))
 
@@ -266,6 +315,54 @@ def ps_load(h: int, path: str) -> int:
 
 def ps_sync(h: int) -> int:
     return load_library().ps_sync(h)
+
+
+class OpScript:
+    """A prepared ps_run script: a ctypes ps_op array plus the id and
+    pointer arrays its pull ops point into (kept alive here)."""
+
+    def __init__(self):
+        self._ops = []
+        self._keep = []
+        self.array = None
+
+    def push(self, learner_id: int, grad_ptr: int, dtype: int = PS_F32):
+        self._ops.append(ps_op(PS_OP_PUSH, learner_id, dtype, 0, grad_ptr, None, None))
+
+    def apply(self):
+        self._ops.append(ps_op(PS_OP_APPLY, 0, 0, 0, None, None, None))
+
+    def apply_sync(self):
+        self._ops.append(ps_op(PS_OP_APPLY_SYNC, 0, 0, 0, None, None, None))
+
+    def _pulls(self, kind, learner_ids, dst_ptrs, dtype):
+        ids, dp = _ints(learner_ids), _ptrs(dst_ptrs)
+        self._keep += [ids, dp]
+        self._ops.append(ps_op(kind, 0, dtype, len(learner_ids), None,
+                               ctypes.cast(ids, ctypes.POINTER(ctypes.c_int)),
+                               ctypes.cast(dp, ctypes.POINTER(_VP))))
+
+    def pull(self, learner_ids, dst_ptrs, dtype: int = PS_F32):
+        self._pulls(PS_OP_PULL, learner_ids, dst_ptrs, dtype)
+
+    def apply_pull(self, learner_ids, dst_ptrs, dtype: int = PS_F32):
+        self._pulls(PS_OP_APPLY_PULL, learner_ids, dst_ptrs, dtype)
+
+    def __len__(self):
+        return len(self._ops)
+
+    def build(self):
+        self.array = (ps_op * max(1, len(self._ops)))(*self._ops)
+        return self
+
+
+def ps_run(h: int, script: "OpScript"):
+    """(status, calls completed)."""
+    if script.array is None:
+        script.build()
+    done = ctypes.c_int()
+    rc = load_library().ps_run(h, script.array, len(script), ctypes.byref(done))
+    return rc, done.value
 
 
 def ps_set_fronts(h: int, fronts_log2: int) -> int:
@@ -305,16 +402,21 @@ class ParameterServer:
 
     Pushed gradients are borrowed: the tensor is kept referenced until the
     apply that consumes it has been enqueued, and the caller must not write it
-    before that apply has run on the server's stream. Gradients and replicas
-    are marked as used on the torch streams given to set_stream and
+    before that apply has run on the server's stream. An apply may leave
+    gradients queued (round-robin mode takes at most `depth`, a synchronous
+    step one per waiting learner); those stay referenced. Gradients and
+    replicas are marked as used on the torch streams given to set_stream and
     set_pull_stream (Tensor.record_stream), so a tensor the caller frees is not
-    reused by torch's allocator before the server's kernels on it have run."""
+    reused by torch's allocator before the server's kernels on it have run.
+    One lock covers each library call together with this bookkeeping, so
+    learner threads may push while another thread applies."""
 
     def __init__(self, n_params: int, lr: float, momentum: float = 0.0,
                  queue_depth: Optional[int] = None, stream=None):
         self.h = ps_create(n_params, lr, momentum)
         self.n = n_params
-        self._pending = []
+        self._lock = threading.RLock()
+        self._pending = {}   # learner id -> deque of pushed tensors, oldest first
         self._streams = []   # torch streams the device work may run on (set_stream, set_pull_stream)
         if queue_depth is not None:
             self._check(ps_set_queue_depth(self.h, queue_depth), "set_queue_depth")
@@ -332,10 +434,11 @@ class ParameterServer:
         return t.data_ptr()
 
     def close(self):
-        if self.h:
-            ps_destroy(self.h)
-            self.h = 0
-            self._pending = []
+        with self._lock:
+            if self.h:
+                ps_destroy(self.h)
+                self.h = 0
+                self._pending = {}
 
     def __del__(self):
         try:
@@ -387,25 +490,42 @@ class ParameterServer:
 
     def push(self, learner: int, grad) -> bool:
         """Enqueue; False when the queue is full (nothing enqueued)."""
-        rc = ps_push_dtype(self.h, learner, self._tensor(grad, "push"), _dtype_code(grad))
-        if rc == PS_EFULL:
-            return False
-        self._check(rc, "push")
-        self._uses(grad)
-        self._pending.append(grad)
+        ptr, code = self._tensor(grad, "push"), _dtype_code(grad)
+        with self._lock:
+            rc = ps_push_dtype(self.h, learner, ptr, code)
+            if rc == PS_EFULL:
+                return False
+            self._check(rc, "push")
+            self._uses(grad)
+            self._pending.setdefault(learner, deque()).append(grad)
         return True
 
     def push_async(self, learner: int, grad, ready_event) -> bool:
         """Push a gradient still being written on another stream; the apply
         waits for `ready_event` (a recorded torch.cuda.Event) on the device."""
-        rc = ps_push_async(self.h, learner, self._tensor(grad, "push_async"), _dtype_code(grad),
-                           ready_event.cuda_event)
-        if rc == PS_EFULL:
-            return False
-        self._check(rc, "push_async")
-        self._uses(grad)
-        self._pending.append((grad, ready_event))
+        ptr, code = self._tensor(grad, "push_async"), _dtype_code(grad)
+        with self._lock:
+            rc = ps_push_async(self.h, learner, ptr, code, ready_event.cuda_event)
+            if rc == PS_EFULL:
+                return False
+            self._check(rc, "push_async")
+            self._uses(grad)
+            self._pending.setdefault(learner, deque()).append((grad, ready_event))
         return True
+
+    def _release_applied(self) -> None:
+        """Drop the references of the gradients the last apply consumed: per
+        learner the oldest ones (every queue mode keeps each learner's pushes
+        in order), as many as ps_last_applied names. Caller holds the lock."""
+        ids = ps_last_applied(self.h)
+        if isinstance(ids, int):
+            self._check(ids, "last_applied")
+        for l in ids:
+            q = self._pending.get(l)
+            if q:
+                q.popleft()
+                if not q:
+                    del self._pending[l]
 
     def record(self, event) -> None:
         """Record a torch.cuda.Event on the server's stream."""
@@ -421,12 +541,14 @@ class ParameterServer:
         self._track(stream)
 
     def apply_pending(self) -> None:
-        self._check(ps_apply_pending(self.h), "apply_pending")
-        self._pending = []
+        with self._lock:
+            self._check(ps_apply_pending(self.h), "apply_pending")
+            self._release_applied()
 
     def apply_sync(self) -> None:
-        self._check(ps_apply_sync(self.h), "apply_sync")
-        self._pending = []
+        with self._lock:
+            self._check(ps_apply_sync(self.h), "apply_sync")
+            self._release_applied()
 
     def pull(self, learner: int, dst) -> None:
         self.pull_many([learner], [dst])
@@ -449,11 +571,21 @@ class ParameterServer:
 
     def apply_pull(self, learners: Sequence[int], dsts) -> None:
         ptrs, dt = self._replicas(learners, dsts, "apply_pull")
-        self._check(ps_apply_pull(self.h, list(learners), ptrs, dt), "apply_pull")
-        self._pending = []
+        with self._lock:
+            self._check(ps_apply_pull(self.h, list(learners), ptrs, dt), "apply_pull")
+            self._release_applied()
+
+    def retire_learner(self, learner: int) -> int:
+        """A dead learner whose gradients in server rows still apply (the
+        references stay until their apply is enqueued)."""
+        with self._lock:
+            return self._check(ps_retire_learner(self.h, learner), "retire_learner")
 
     def drop_learner(self, learner: int) -> int:
-        n = self._check(ps_drop_learner(self.h, learner), "drop_learner")
+        with self._lock:
+            n = self._check(ps_drop_learner(self.h, learner), "drop_learner")
+            # dropped gradients are never read by a kernel
+            self._pending.pop(learner, None)
         return n
 
     def save(self, path: str) -> None:

@@ -10,7 +10,7 @@
 //   sync                  synchronous step (ps_apply_sync)
 //   pull DT L1 D1 ...     ordered pulls of learners Li into buffers Di (ps_pull_many)
 //   applypull DT L1 D1 .. ps_apply_pull
-//   drop L | depth K | mode M S | skip 0|1 | state
+//   drop L | retire L | depth K | mode M S | skip 0|1 | state
 //   fronts A1 A2 ...      front choice for streams at addresses Ai (0 = none)
 //   rows B C              row layout of C rows of B bytes: head stride span
 #include <cstdio>
@@ -91,6 +91,7 @@ int main() {
             const int n = static_cast<int>(ids.size());
             int rc = p.plan_pulls(n, ids.data(), dsts.data(), dt, p.ts, write);
             if (rc == 0) p.commit_pulls(n, ids.data(), dsts.data(), dt, write, true);
+            else write.clear();
             std::printf("pull %d", rc);
             print_written(write);
         } else if (cmd == "applypull") {
@@ -116,6 +117,7 @@ int main() {
                     p.commit_pulls(n, ids.data(), dsts.data(), dt, write, true);
                 }
             }
+            if (rc != 0) write.clear();
             std::printf("applypull %d", rc);
             print_applied(p);
             print_written(write);
@@ -123,6 +125,10 @@ int main() {
             long l;
             in >> l;
             std::printf("drop %d", p.drop_learner(static_cast<int>(l)));
+        } else if (cmd == "retire") {
+            long l;
+            in >> l;
+            std::printf("retire %d", p.retire_learner(static_cast<int>(l)));
         } else if (cmd == "depth") {
             long k;
             in >> k;

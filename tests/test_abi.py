@@ -42,11 +42,17 @@ def test_header_constants_match_binding():
                  "PS_EIO", "PS_F32", "PS_BF16", "PS_QUEUE_FIFO", "PS_QUEUE_ROUND_ROBIN"):
         m = re.search(rf"\b{name}\s*=\s*(-?\d+)", text)
         assert m and int(m.group(1)) == getattr(ps, name), name
+    for name in ("PS_OP_PUSH", "PS_OP_APPLY", "PS_OP_APPLY_SYNC", "PS_OP_PULL",
+                 "PS_OP_APPLY_PULL"):
+        m = re.search(rf"\b{name}\s*=\s*(-?\d+)", text)
+        assert m and int(m.group(1)) == getattr(ps, name), name
     for name in ("PS_MAX_QUEUE_DEPTH", "PS_MAX_REPLICAS", "PS_MAX_LEARNERS", "PS_STALENESS_BINS",
-                 "PS_MAX_ROWS"):
+                 "PS_MAX_ROWS", "PS_IPC_HANDLE_BYTES"):
         m = re.search(rf"#define {name} (\d+)", text)
         assert m and int(m.group(1)) == getattr(ps, name), name
     assert ctypes.sizeof(ps.ps_stats) == 8 * (10 + ps.PS_STALENESS_BINS)
+    # ps_op: four ints, then three pointers (x86-64)
+    assert ctypes.sizeof(ps.ps_op) == 40 and ps.ps_op.grad.offset == 16
 
 
 def test_validation_without_device(lib):
@@ -57,6 +63,12 @@ def test_validation_without_device(lib):
     assert lib.ps_create(10, float("nan"), 0.0) is None
     assert lib.ps_create(10, 0.1, float("inf")) is None
     assert lib.ps_push(None, 0, None) == ps.PS_EINVAL
+    assert lib.ps_run(None, None, 0, None) == ps.PS_EINVAL
+    assert lib.ps_retire_learner(None, 0) == ps.PS_EINVAL
+    assert lib.ps_export_rows(None, None, None, None) == ps.PS_EINVAL
+    assert lib.ps_import_rows(None, 0, None) == ps.PS_EINVAL
+    assert lib.ps_release_rows(ctypes.c_void_p(4096)) == ps.PS_EINVAL
+    assert ps.ps_import_rows(b"short", 0) == (ps.PS_EINVAL, 0)
     assert lib.ps_apply_pending(None) == ps.PS_EINVAL
     assert lib.ps_pull(None, 0, None) == ps.PS_EINVAL
     assert ps.ps_pull_many(None, [0], [1], ps.PS_F32) == ps.PS_EINVAL

@@ -18,6 +18,17 @@ def test_kernel_digest_ignores_comments_not_code(tmp_path):
     c.write_text("__global__ void k(float *p) { p[0] = 2.0f; }\n")
     da, db, dc = (bench.kernel_source_digest(str(x)) for x in (a, b, c))
     assert da == db != dc
+    # over several files: any code change in any of them counts
+    assert bench.kernel_source_digest([str(a), str(c)]) == bench.kernel_source_digest([str(b), str(c)])
+    assert bench.kernel_source_digest([str(a), str(c)]) != bench.kernel_source_digest([str(a), str(a)])
+
+
+def test_kernel_digest_covers_launch_shaping_host_code():
+    """The counters bench.py reports are keyed to the kernels and to the host
+    code that picks their launch shapes and buffer placement."""
+    names = {os.path.basename(p) for p in bench.KERNEL_SRC}
+    assert names == {"ps_kernels.hip", "ps_kernels.h", "ps_server.cpp", "ps_layout.cpp",
+                     "ps_layout.h"}
 
 
 def test_more_than_one_gpu_is_refused():

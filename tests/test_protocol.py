@@ -59,9 +59,13 @@ def run_oracle(lines):
         return f" ts={o.ts}" + "".join(f" {l}:{s}" for l, s in last)
 
     def pulls(t):
+        """(status, written indices); a call naming a retired learner is
+        refused whole."""
         dt = int(t[1])
         pairs = [(int(t[i]), int(t[i + 1])) for i in range(2, len(t), 2)]
-        return ",".join(str(i) for i, (l, d) in enumerate(pairs) if o.pull(l, d, dt))
+        if any(l in o.retired for l, _ in pairs):
+            return orc.ESTATE, ""
+        return orc.OK, ",".join(str(i) for i, (l, d) in enumerate(pairs) if o.pull(l, d, dt))
 
     for line in lines:
         t = line.split()
@@ -71,6 +75,8 @@ def run_oracle(lines):
             g = (np.array([gid], np.uint16) if dt == orc.BF16
                  else np.array([gid * 1e-3], np.float32))
             out.append(f"push {o.push(l, g)}")
+        elif c == "applypull" and any(int(t[i]) in o.retired for i in range(2, len(t), 2)):
+            out.append(f"applypull {orc.ESTATE}" + applied() + " w=")
         elif c in ("apply", "sync", "applypull"):
             n0 = len(o.staleness)
             rc = o.apply_sync() if c == "sync" else o.apply_pending()
@@ -78,12 +84,15 @@ def run_oracle(lines):
                 last = list(zip(o.applied_order[n0:], o.staleness[n0:]))
             line_out = f"{c} {rc}" + applied()
             if c == "applypull":
-                line_out += " w=" + pulls(t)
+                line_out += " w=" + pulls(t)[1]
             out.append(line_out)
         elif c == "pull":
-            out.append("pull 0 w=" + pulls(t))
+            rc, w = pulls(t)
+            out.append(f"pull {rc} w={w}")
         elif c == "drop":
             out.append(f"drop {o.drop_learner(int(t[1]))}")
+        elif c == "retire":
+            out.append(f"retire {o.retire_learner(int(t[1]))}")
         elif c == "depth":
             out.append(f"depth {o.set_depth(int(t[1]))}")
         elif c == "mode":
@@ -109,8 +118,9 @@ def script(seed, learners, n_cmds=700, bf16_rate=0.1):
     rng = np.random.default_rng(seed)
     lines = []
     gid = 0
-    kinds = ["push", "apply", "sync", "pull", "applypull", "drop", "depth", "mode", "skip", "state"]
-    p = np.array([44, 10, 5, 12, 8, 3, 5, 4, 3, 6], float)
+    kinds = ["push", "apply", "sync", "pull", "applypull", "drop", "depth", "mode", "skip", "state",
+             "retire"]
+    p = np.array([44, 10, 5, 12, 8, 3, 5, 4, 3, 6, 0.6], float)
     for _ in range(n_cmds):
         c = kinds[rng.choice(len(kinds), p=p / p.sum())]
         if c == "push":
@@ -123,8 +133,8 @@ def script(seed, learners, n_cmds=700, bf16_rate=0.1):
             dt = int(rng.integers(2))
             pairs = " ".join(f"{l} {2 * l + int(rng.random() < 0.2)}" for l in ls)
             lines.append(f"{c} {dt} {pairs}")
-        elif c == "drop":
-            lines.append(f"drop {rng.integers(learners)}")
+        elif c in ("drop", "retire"):
+            lines.append(f"{c} {rng.integers(learners)}")
         elif c == "depth":
             lines.append(f"depth {rng.choice([0, 1, 2, 4, 8, 16, 32, 64, 65])}")
         elif c == "mode":
@@ -151,7 +161,9 @@ def test_protocol_matches_oracle(driver, seed, learners):
 def test_scripts_reach_every_outcome(driver):
     """The random scripts exercise what they are meant to: full queues,
     skipped and written pulls, mixed-dtype synchronous steps refused, queue
-    settings refused while gradients wait, round-robin service."""
+    settings refused while gradients wait, round-robin service, dead
+    learners dropped or retired with gradients queued, and a retired
+    learner's pushes and pulls refused."""
     seen = set()
     for learners in (1, 3, 8, 40):
         for seed in range(6):
@@ -172,8 +184,15 @@ def test_scripts_reach_every_outcome(driver):
                         seen.add("skipped pull")
                 if c == "drop" and res != "drop 0":
                     seen.add("dropped")
+                if c == "retire" and res != "retire 0":
+                    seen.add("retired with gradients queued")
+                if c == "push" and res == f"push {orc.ESTATE}":
+                    seen.add("push after retire refused")
+                if c == "pull" and res.startswith(f"pull {orc.ESTATE}"):
+                    seen.add("pull after retire refused")
     assert seen == {"full", "mixed sync", "state refused", "round robin", "skipped pull",
-                    "dropped"}, seen
+                    "dropped", "retired with gradients queued", "push after retire refused",
+                    "pull after retire refused"}, seen
 
 
 MIB2 = 2 << 20
