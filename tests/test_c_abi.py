@@ -10,13 +10,18 @@ from paper_1611_06213_amd import build as lib_build
 
 
 @pytest.mark.gpu
-def test_c_program_drives_the_abi():
+def test_c_program_drives_the_abi(spawner, tmp_path):
+    """Started by the session's launcher (tests/spawner.py), which never
+    touches the GPU; the program's output goes to a file."""
     if not os.path.exists(lib_build.C_SMOKE):
         pytest.fail("tests/c_abi_smoke is not built (run __graft_entry__.build())")
-    r = subprocess.run([lib_build.C_SMOKE], capture_output=True, text=True, timeout=120)
-    assert r.returncode == 0, r.stderr[-2000:]
-    assert "c abi ok" in r.stdout
-    for line in r.stdout.splitlines():
+    out = tmp_path / "c_abi.out"
+    sh = f"exec {lib_build.C_SMOKE} > {out} 2>&1"
+    r = spawner.run([["/bin/sh", "-c", sh]], timeout=120)
+    text = out.read_text()
+    assert r == {"rc": [0], "timed_out": False}, text[-2000:]
+    assert "c abi ok" in text
+    for line in text.splitlines():
         if line.startswith("tiny loop"):
             print(line, flush=True)
 

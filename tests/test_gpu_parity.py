@@ -1172,7 +1172,9 @@ def test_lock_free_pull_sees_before_or_after(torch, dtype):
     """HogWild! mode (Sec. 4.1): a pull on its own stream, concurrent with an
     apply, writes for every coordinate either the weights before the apply
     or after it (bitwise one of the two; which one may vary by coordinate).
-    Nondeterministic by design, so checked by this bound, not by bits."""
+    Nondeterministic by design, so checked by this bound, not by bits; the
+    two candidates are the oracle's weights before and after that apply
+    (and the server's equal them bitwise)."""
     n = 50_000_003
     gen = torch.Generator(device="cuda")
     gen.manual_seed(52)
@@ -1187,6 +1189,19 @@ def test_lock_free_pull_sees_before_or_after(torch, dtype):
         srv.push(j % 8, pool[j])
     srv.apply_pending()
     before = srv.weights_copy()
+    # the weights before and after the raced apply, from the oracle
+    o = orc.OracleServer(parity.np_bits(w0), 0.01, 0.9, depth=32)
+    host = [parity.np_bits(pool[j]) for j in range(32)]
+    for j in range(32):
+        o.push(j % 8, host[j])
+    o.apply_pending()
+    o_before = o.w.copy()
+    for j in range(32):
+        o.push(j % 8, host[31 - j])
+    o.apply_pending()
+    o_after = o.w.copy()
+    del host
+    assert parity.bitwise(parity.np_bits(before), o_before)
     side = torch.cuda.Stream()
     srv.set_pull_stream(side)
     tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
@@ -1198,9 +1213,9 @@ def test_lock_free_pull_sees_before_or_after(torch, dtype):
     srv.pull_many([3], [dst[0]])          # ... and a pull racing it
     srv.sync()
     after = srv.weights_copy()
+    assert parity.bitwise(parity.np_bits(after), o_after)
     d = parity.np_bits(dst[0])
-    a = parity.np_bits(before)
-    b = parity.np_bits(after)
+    a, b = o_before, o_after
     if dtype == "bf16":
         a, b = orc.f32_to_bf16(a), orc.f32_to_bf16(b)
     else:
@@ -1211,7 +1226,7 @@ def test_lock_free_pull_sees_before_or_after(torch, dtype):
     srv.set_pull_stream(None)
     srv.pull_many([3], [dst[0]])
     srv.sync()
-    want = parity.np_bits(after)
+    want = o_after
     got = parity.np_bits(dst[0])
     assert parity.bitwise(got, want if dtype == "f32" else orc.f32_to_bf16(want))
     srv.close()

@@ -1,0 +1,261 @@
+"""GPU tests of protocol rules added around the kernels: a dead learner's
+gradients in the server's rows (retire), checkpoints that carry the queue
+configuration, apply+pull after lock-free pulls, and the binding keeping
+every gradient that is still queued alive."""
+import numpy as np
+import pytest
+
+from oracle import server as orc
+from paper_1611_06213_amd import ps
+from paper_1611_06213_amd import workloads as wl
+from tests import golden_script, parity
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    ps.load_library()
+    return torch
+
+
+def test_golden_retire_through_abi(torch):
+    """tests/golden/retire_rr.txt through the C ABI, every gradient in a
+    server row (the paper's shared slots): service order, staleness,
+    refused push and pull of the retired learner, counters, weights."""
+    depth, ops, expect, mode = golden_script.load("retire_rr.txt", with_mode=True)
+    n = 4
+    srv = ps.ParameterServer(n, 2.0 ** -4, 0.0, queue_depth=depth)
+    srv.set_queue_mode(ps.PS_QUEUE_ROUND_ROBIN, mode[1])
+    srv.set_weights(torch.zeros(n, device="cuda"))
+    rows = srv.alloc_rows(len(ops))
+    for r in rows:
+        r.fill_(0.5)
+    dsts = {l: torch.empty(n, device="cuda") for l in range(3)}
+    order, stale = [], []
+    for i, (op, l, outcome) in enumerate(ops):
+        if op == "push":
+            rc = ps.ps_push(srv.h, l, rows[i].data_ptr())
+            assert rc == {"ok": ps.PS_OK, "full": ps.PS_EFULL, "refused": ps.PS_ESTATE}[outcome]
+        elif op == "apply":
+            srv.apply_pending()
+            order += srv.last_applied()
+            stale += srv.last_staleness()
+        elif op == "retire":
+            assert ps.ps_retire_learner(srv.h, l) == int(outcome)
+        elif op == "drop":
+            assert ps.ps_drop_learner(srv.h, l) == int(outcome)
+        elif outcome == "refused":
+            assert ps.ps_pull(srv.h, l, dsts[l].data_ptr()) == ps.PS_ESTATE
+        else:
+            before = srv.stats().pulls_skipped
+            srv.pull(l, dsts[l])
+            assert (srv.stats().pulls_skipped == before) == (outcome == "pulled")
+    st = srv.stats()
+    assert order == expect["order"] and stale == expect["staleness"]
+    assert srv.timestamp == expect["ts"][0]
+    assert (st.pulls, st.pulls_skipped, st.pushes_rejected) == (
+        expect["pulls"], expect["skipped"], expect["rejected"])
+    assert torch.all(srv.weights_copy() == -6 / 32)
+    # a new run (set_weights) readmits the retired learner
+    srv.set_weights(torch.zeros(n, device="cuda"))
+    assert ps.ps_push(srv.h, 1, rows[0].data_ptr()) == ps.PS_OK
+    srv.apply_pending()
+    del rows
+    srv.close()
+
+
+def test_retire_refuses_borrowed_buffers(torch):
+    """A queued gradient outside the server's rows may have died with its
+    learner: retiring that learner is refused (nothing changes) and dropping
+    is the way; a learner with only row gradients queued retires."""
+    n = 100_003
+    srv = ps.ParameterServer(n, 0.01, 0.9, queue_depth=8)
+    srv.set_weights(torch.zeros(n, device="cuda"))
+    rows = srv.alloc_rows(2)
+    own = torch.ones(n, device="cuda")
+    assert srv.push(0, rows[0]) and srv.push(1, own) and srv.push(0, rows[1])
+    assert ps.ps_retire_learner(srv.h, 1) == ps.PS_ESTATE
+    assert srv.pending == 3 and ps.ps_push(srv.h, 1, own.data_ptr()) == ps.PS_OK   # not retired
+    assert ps.ps_retire_learner(srv.h, 0) == 2
+    assert ps.ps_push(srv.h, 0, rows[0].data_ptr()) == ps.PS_ESTATE
+    assert ps.ps_drop_learner(srv.h, 1) == 2
+    srv.apply_pending()
+    assert srv.last_applied() == [0, 0] and srv.timestamp == 2
+    assert ps.ps_retire_learner(srv.h, -1) == ps.PS_EINVAL
+    del rows
+    srv.close()
+
+
+def test_checkpoint_keeps_queue_configuration(torch, tmp_path):
+    """A checkpoint records the queue mode, depth and slots per learner; a
+    server set up otherwise refuses it (PS_EINVAL, unchanged), since the
+    same gradients would then be served in another order."""
+    n = 10_007
+    a = ps.ParameterServer(n, 0.01, 0.9, queue_depth=4)
+    a.set_queue_mode(ps.PS_QUEUE_ROUND_ROBIN, 2)
+    a.set_weights(torch.full((n,), 0.25, device="cuda"))
+    g = torch.ones(n, device="cuda")
+    a.push(0, g)
+    a.apply_pending()
+    path = str(tmp_path / "q.ckpt")
+    a.save(path)
+    for depth, mode, slots in ((4, ps.PS_QUEUE_FIFO, 1), (8, ps.PS_QUEUE_ROUND_ROBIN, 2),
+                               (4, ps.PS_QUEUE_ROUND_ROBIN, 3)):
+        b = ps.ParameterServer(n, 0.01, 0.9, queue_depth=depth)
+        if mode == ps.PS_QUEUE_ROUND_ROBIN:
+            b.set_queue_mode(mode, slots)
+        b.set_weights(torch.zeros(n, device="cuda"))
+        assert ps.ps_load(b.h, path) == ps.PS_EINVAL and "queue configuration" in ps.ps_last_error()
+        assert torch.all(b.weights_copy() == 0) and b.timestamp == 0
+        b.close()
+    c = ps.ParameterServer(n, 0.01, 0.9, queue_depth=4)
+    c.set_queue_mode(ps.PS_QUEUE_ROUND_ROBIN, 2)
+    c.load(path)
+    assert c.timestamp == 1
+    assert parity.bitwise(parity.np_bits(c.weights_copy()), parity.np_bits(a.weights_copy()))
+    a.close()
+    c.close()
+
+
+def test_apply_pull_after_lock_free_pulls(torch):
+    """Lock-free pulls of 64 replicas (slow) on their own stream, then at
+    once an apply+pull into one of those replicas on the server's stream:
+    the replica ends with the new weights (the apply+pull waits for the
+    earlier lock-free pulls), and a repeat pull is skipped as current and
+    leaves it so. Checked against the oracle."""
+    n = 4_000_037
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(61)
+    w0 = (torch.rand(n, generator=gen, device="cuda") - 0.5) * 0.1
+    g = torch.randn(n, generator=gen, device="cuda") * 1e-2
+    reps = wl.Rows(64, n, torch.float32, "cuda")
+    srv = ps.ParameterServer(n, 0.01, 0.0, queue_depth=4)
+    srv.set_stream(torch.cuda.current_stream())
+    srv.set_weights(w0)
+    side = torch.cuda.Stream()
+    srv.set_pull_stream(side)
+    torch.cuda.synchronize()
+    srv.pull_many(list(range(64)), [reps[l] for l in range(64)])   # lock-free, old weights
+    srv.push(5, g)
+    srv.apply_pull([5], [reps[5]])                                  # ordered, new weights
+    srv.apply_pull([5], [reps[5]])                                  # nothing pending: skipped
+    srv.sync()
+    assert srv.stats().pulls_skipped == 1
+    o = orc.OracleServer(parity.np_bits(w0), 0.01, 0.0, depth=4)
+    o.push(5, parity.np_bits(g))
+    o.apply_pending()
+    assert parity.bitwise(parity.np_bits(reps[5]), o.w)
+    assert parity.bitwise(parity.np_bits(reps[6]), parity.np_bits(w0))
+    srv.set_pull_stream(None)
+    srv.close()
+
+
+def test_binding_keeps_unapplied_gradients_referenced(torch):
+    """Round-robin queues, 4 learners x 2 slots, depth 2: each apply takes
+    two gradients and leaves the rest queued. The caller drops its own
+    references right after the first apply and allocates and fills new
+    tensors; the binding must keep the queued gradients alive (their memory
+    not reused) until their applies are enqueued. Bitwise against the
+    oracle."""
+    n = 1_000_003
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(62)
+    w0 = (torch.rand(n, generator=gen, device="cuda") - 0.5) * 0.1
+    srv = ps.ParameterServer(n, 0.01, 0.9, queue_depth=2)
+    srv.set_queue_mode(ps.PS_QUEUE_ROUND_ROBIN, 2)
+    srv.set_stream(torch.cuda.current_stream())
+    srv.set_weights(w0)
+    grads = [torch.randn(n, generator=gen, device="cuda") * 1e-2 for _ in range(8)]
+    host = [parity.np_bits(t) for t in grads]
+    for j, t in enumerate(grads):
+        assert srv.push(j % 4, t)
+    srv.apply_pending()
+    del grads, t                        # the caller lets go of every gradient
+    junk = [torch.full((n,), 1e6, device="cuda") for _ in range(8)]   # would reuse freed blocks
+    while srv.pending:
+        srv.apply_pending()
+    w = parity.np_bits(srv.weights_copy())
+    o = orc.OracleServer(parity.np_bits(w0), 0.01, 0.9, depth=2)
+    o.set_queue_mode(orc.ROUND_ROBIN, 2)
+    for j, hg in enumerate(host):
+        o.push(j % 4, hg)
+    while o.pending():
+        o.apply_pending()
+    assert parity.bitwise(w, o.w)
+    assert srv._pending == {}
+    del junk
+    srv.close()
+
+
+@pytest.mark.parametrize("fused", [False, True], ids=["separate", "fused"])
+def test_run_script_equals_calls(torch, fused):
+    """ps_run over a prepared schedule (pushes, applies, pulls) gives the
+    bits, staleness and counters of the same calls made one by one; it
+    stops at the first call that fails (a full queue) and reports how many
+    ran."""
+    cfg = wl.CONFIGS["alexnet"].scaled(200_003, pushes=96, pool=16)
+    ev = wl.schedule(cfg)
+    pool = wl.make_pool(cfg, "cuda")
+    w0 = wl.make_w0(cfg, "cuda")
+    out = []
+    for native in (False, True):
+        srv = ps.ParameterServer(cfg.n, cfg.lr, cfg.momentum, queue_depth=cfg.depth)
+        srv.set_stream(torch.cuda.current_stream())
+        srv.set_weights(w0)
+        reps = wl.Rows(cfg.replicas, cfg.n, torch.float32, "cuda")
+        sc = ps.OpScript()
+        i = 0
+        while i < len(ev):
+            e = ev[i]
+            if isinstance(e, wl.Push):
+                if native:
+                    sc.push(e.learner, pool[e.buf].data_ptr())
+                else:
+                    assert ps.ps_push(srv.h, e.learner, pool[e.buf].data_ptr()) == ps.PS_OK
+            elif isinstance(e, wl.Apply):
+                nxt = ev[i + 1] if i + 1 < len(ev) else None
+                if fused and isinstance(nxt, wl.Pull):
+                    ls = parity.pull_rounds(nxt.learners)
+                    dl = [reps[l].data_ptr() for l in ls[0]]
+                    if native:
+                        sc.apply_pull(ls[0], dl)
+                    else:
+                        assert ps.ps_apply_pull(srv.h, ls[0], dl, ps.PS_F32) == ps.PS_OK
+                    for rnd in ls[1:]:
+                        dr = [reps[l].data_ptr() for l in rnd]
+                        sc.pull(rnd, dr) if native else ps.ps_pull_many(srv.h, rnd, dr, ps.PS_F32)
+                    i += 2
+                    continue
+                sc.apply() if native else ps.ps_apply_pending(srv.h)
+            else:
+                for rnd in parity.pull_rounds(e.learners):
+                    dr = [reps[l].data_ptr() for l in rnd]
+                    sc.pull(rnd, dr) if native else ps.ps_pull_many(srv.h, rnd, dr, ps.PS_F32)
+            i += 1
+        if native:
+            assert ps.ps_run(srv.h, sc) == (ps.PS_OK, len(sc))
+        st = srv.stats()
+        out.append((parity.np_bits(srv.weights_copy()), parity.np_bits(srv.velocity_copy()),
+                    [parity.np_bits(reps[l]) for l in range(cfg.replicas)], srv.last_staleness(),
+                    (st.timestamp, st.pushes_applied, st.pulls, st.pulls_skipped, st.staleness_sum)))
+        srv.close()
+        del reps
+    (wa, va, ra, sa, ca), (wb, vb, rb, sb, cb) = out
+    assert parity.bitwise(wa, wb) and parity.bitwise(va, vb) and sa == sb and ca == cb
+    assert all(parity.bitwise(x, y) for x, y in zip(ra, rb))
+    # a script that overfills the queue stops at the refused push
+    srv = ps.ParameterServer(cfg.n, cfg.lr, 0.0, queue_depth=2)
+    sc = ps.OpScript()
+    for j in range(3):
+        sc.push(j, pool[j].data_ptr())
+    sc.apply()
+    assert ps.ps_run(srv.h, sc) == (ps.PS_EFULL, 2)
+    assert srv.pending == 2
+    assert ps.ps_run(srv.h, ps.OpScript()) == (ps.PS_OK, 0)
+    srv.apply_pending()
+    srv.close()
+    del pool
