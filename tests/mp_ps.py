@@ -18,7 +18,9 @@ Usage: python tests/mp_ps.py server CONF.json
        python tests/mp_ps.py learner CONF.json L
 CONF holds: sock, out (a directory), n, lr, momentum, learners, slots,
 depth, pool, pushes (per learner), die ({learner: pushes before dying}),
-dead_mode ("retire" | "drop").
+dead_mode ("retire" | "drop"), and optionally workload ("alexnet": fp32
+gradients, or "mixed": bf16) and queue ("rr": per-learner queues of `slots`,
+or "fifo": one queue of `depth`; the learners still own `slots` rows each).
 
 The server writes out/server.json (every protocol call it made, in order:
 push, apply with the learners served and their staleness, pull, retire or
@@ -47,7 +49,8 @@ def say(*a):
 
 def workload(conf):
     from paper_1611_06213_amd import workloads as wl
-    return wl.CONFIGS["alexnet"].scaled(conf["n"], pushes=sum(conf["pushes"]), pool=conf["pool"])
+    return wl.CONFIGS[conf.get("workload", "alexnet")].scaled(conf["n"], pushes=sum(conf["pushes"]),
+                                                             pool=conf["pool"])
 
 
 def buffer_of(conf, learner, k):
@@ -115,12 +118,15 @@ def server(conf):
     h = ps.ps_create(n, conf["lr"], conf["momentum"])
     check(ps.ps_set_stream(h, stream.cuda_stream), "set_stream")
     check(ps.ps_set_queue_depth(h, D), "set_queue_depth")
-    check(ps.ps_set_queue_mode(h, ps.PS_QUEUE_ROUND_ROBIN, S), "set_queue_mode")
+    if conf.get("queue", "rr") == "rr":
+        check(ps.ps_set_queue_mode(h, ps.PS_QUEUE_ROUND_ROBIN, S), "set_queue_mode")
+    gdt = cfg.grad_dtype
+    fifo = conf.get("queue", "rr") == "fifo"
     w0 = wl.make_w0(cfg, "cuda")
     check(ps.ps_set_weights(h, w0.data_ptr()), "set_weights")
     slots, reps, offer = {}, {}, {}
     for l in range(L):
-        rc, g = ps.ps_alloc_rows(h, S, ps.PS_F32)
+        rc, g = ps.ps_alloc_rows(h, S, gdt)
         check(rc, "alloc_rows")
         rc, r = ps.ps_alloc_rows(h, 1, ps.PS_F32)
         check(rc, "alloc_rows")
@@ -157,7 +163,9 @@ def server(conf):
     def on_message(l, m):
         if "push" in m:
             s = m["push"]
-            check(ps.ps_push(h, l, slots[l][s]), "push")
+            if fifo and check(ps.ps_pending(h), "pending") >= D:
+                apply_and_pull()           # one queue of D: make room first
+            check(ps.ps_push_dtype(h, l, slots[l][s], gdt), "push")
             queued[l].append(s)
             log.append(["push", l, s, m["buf"]])
         elif "done" in m:
@@ -212,7 +220,9 @@ def server(conf):
     t_end = time.monotonic() + conf.get("limit", 120)
     while time.monotonic() < t_end:
         got = drain(0.05)
-        while drain(0):          # everything already there, EOFs included
+        # everything already there or arriving within 2 ms (a learner that
+        # stops right after a push closes its socket just after it), EOFs included
+        while drain(0.002):
             got = True
         pending = check(ps.ps_pending(h), "pending")
         active = live - done
@@ -285,7 +295,8 @@ def learner(conf, l):
     check(rc, "import_rows")
     rc, r0 = ps.ps_import_rows(bytes.fromhex(offer["rep"]), offer["roff"])
     check(rc, "import_rows")
-    slot = ps.rows_as_tensors([g0 + i * offer["stride"] for i in range(S)], n, torch.float32)
+    gtd = torch.bfloat16 if cfg.grad_dtype == wl.BF16 else torch.float32
+    slot = ps.rows_as_tensors([g0 + i * offer["stride"] for i in range(S)], n, gtd)
     replica = ps.rows_as_tensors([r0], n, torch.float32)[0]
     free = collections.deque(range(S))
     die = conf["die"].get(str(l))

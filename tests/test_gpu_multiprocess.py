@@ -63,7 +63,8 @@ def replay(torch, conf, log):
     w0 = parity.np_bits(wl.make_w0(cfg, "cuda"))
     pool = {}
     o = orc.OracleServer(w0, conf["lr"], conf["momentum"], depth=conf["depth"])
-    assert o.set_queue_mode(orc.ROUND_ROBIN, conf["slots"]) == orc.OK
+    if conf.get("queue", "rr") == "rr":
+        assert o.set_queue_mode(orc.ROUND_ROBIN, conf["slots"]) == orc.OK
     deaths = []
     for e in log:
         if e[0] == "push":
@@ -93,10 +94,16 @@ CONF = {"n": 1_000_003, "lr": 0.005, "momentum": 0.9, "learners": 4, "slots": 3,
         "pool": 16, "pushes": [10, 10, 10, 10], "limit": 80}
 
 
-@pytest.mark.parametrize("dead_mode,die", [("retire", {}), ("retire", {"2": 7}), ("drop", {"2": 7})],
-                         ids=["all-finish", "retire", "drop"])
-def test_learner_processes_share_server_rows(torch, spawner, tmp_path, dead_mode, die):
-    conf, out = run_processes(spawner, tmp_path, dict(CONF, die=die, dead_mode=dead_mode))
+@pytest.mark.parametrize("dead_mode,die,extra", [
+    ("retire", {}, {}),
+    ("retire", {"2": 7}, {}),
+    ("drop", {"2": 7}, {}),
+    ("retire", {"1": 6}, {"workload": "mixed", "queue": "fifo", "lr": 0.001, "depth": 6}),
+], ids=["all-finish", "retire", "drop", "bf16-fifo-retire"])
+def test_learner_processes_share_server_rows(torch, spawner, tmp_path, dead_mode, die, extra):
+    """Round-robin queues with fp32 gradients (the first three), and one FIFO
+    queue of 6 with bf16 gradients in bf16 rows."""
+    conf, out = run_processes(spawner, tmp_path, dict(CONF, die=die, dead_mode=dead_mode, **extra))
     log = out["log"]
     o, deaths = replay(torch, conf, log)
     assert o.ts == out["ts"] and o.pending() == 0
