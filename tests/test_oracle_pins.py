@@ -779,3 +779,34 @@ def test_drop_learner_isolates_failure():
         b.apply_pending()
         assert np.array_equal(bits(a.w), bits(b.w)) and a.applied_order == b.applied_order
         assert 2 not in a.applied_order
+
+
+def test_bf16_gradients_shift_w_by_the_propagated_quantisation():
+    """R13 pinned on the oracle: the heavy-ball recurrence is linear in the
+    gradients, so feeding the bf16-rounded gradients instead of the fp32
+    ones moves w by exactly dw = -lr * sum_k e_k (1 - m^(T-k+1)) / (1 - m) in
+    real arithmetic, e_k = widen(bf16(x_k)) - x_k. The oracle's two runs of the
+    Mixed schedule (scaled to 20,011 coordinates, all 400 pushes) differ by
+    dw up to binary32 rounding; a dropped momentum term, a wrong widening or
+    rounding would break it by the size of the effect itself (~1e-4)."""
+    from paper_1611_06213_amd import workloads as wl
+    from tests import parity
+    cfg = wl.CONFIGS["mixed"].scaled(20_011, pool=64)
+    ev = wl.schedule(cfg)
+    w0 = parity.np_bits(wl.make_w0(cfg, "cpu"))
+    bf = [parity.np_bits(wl.make_grad(cfg, b, "cpu")) for b in range(cfg.pool)]
+    f32 = [parity.np_bits(wl.make_grad_f32(cfg, b, "cpu")) for b in range(cfg.pool)]
+    ranges = [(0, cfg.n)]
+    a = parity.oracle_replay(cfg, ev, [bf], [w0], ranges)["w"][0].astype(np.float64)
+    ref = parity.oracle_replay(cfg, ev, [f32], [w0], ranges)["w"][0].astype(np.float64)
+    pushes = [e.buf for e in ev if isinstance(e, wl.Push)]
+    T = len(pushes)
+    lr, m = float(np.float32(cfg.lr)), float(np.float32(cfg.momentum))
+    pred = np.zeros(cfg.n)
+    for k, b in enumerate(pushes):
+        e = orc.bf16_to_f32(bf[b]).astype(np.float64) - f32[b]
+        pred -= lr * (1 - m ** (T - k)) / (1 - m) * e
+    rounding = 8 * T * 2.0 ** -24 * (np.abs(ref).max() + 1e-3)
+    effect = np.abs(a - ref).max()
+    assert effect > 4 * rounding                       # the quantisation is visible ...
+    assert np.abs(a - ref - pred).max() <= rounding     # ... and is exactly the predicted shift
