@@ -339,6 +339,19 @@ class OracleServer:
         self.queue = keep
         return dropped
 
+    def restart(self) -> int:
+        """Resume from a checkpoint (Sec. 4.3: the server restarts from its
+        last checkpoint and the learners are restarted): weights, velocity,
+        timestamp, every learner's timestamp and the round-robin position are
+        what was saved; pull history starts afresh (the restarted learners
+        pull again) and every learner is live again. Like a checkpoint it needs
+        an empty queue."""
+        if self.pending():
+            return ESTATE
+        self.last_pull = {}
+        self.retired = set()
+        return OK
+
     def set_depth(self, depth: int) -> int:
         if not 1 <= depth <= MAX_DEPTH:
             return EINVAL

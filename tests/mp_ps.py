@@ -19,8 +19,15 @@ Usage: python tests/mp_ps.py server CONF.json
 CONF holds: sock, out (a directory), n, lr, momentum, learners, slots,
 depth, pool, pushes (per learner), die ({learner: pushes before dying}),
 dead_mode ("retire" | "drop"), and optionally workload ("alexnet": fp32
-gradients, or "mixed": bf16) and queue ("rr": per-learner queues of `slots`,
-or "fifo": one queue of `depth`; the learners still own `slots` rows each).
+gradients, or "mixed": bf16), queue ("rr": per-learner queues of `slots`,
+or "fifo": one queue of `depth`; the learners still own `slots` rows each),
+push_offset (learner l's k-th push uses pool buffer (5 l + push_offset + k)
+mod pool), and the restart of Sec. 4.3 in two runs: stop_after (after that
+many applies the server stops taking pushes, tells the learners to stop and
+waits until they have detached, applies what is queued, writes the
+checkpoint `checkpoint` and exits -- the watchdog's restart point) and
+resume (a checkpoint the server loads instead of starting from w0; the
+learners are new processes).
 
 The server writes out/server.json (every protocol call it made, in order:
 push, apply with the learners served and their staleness, pull, retire or
@@ -55,7 +62,7 @@ def workload(conf):
 
 def buffer_of(conf, learner, k):
     """Pool buffer of learner's k-th push."""
-    return (5 * learner + k) % conf["pool"]
+    return (5 * learner + conf.get("push_offset", 0) + k) % conf["pool"]
 
 
 class Lines:
@@ -86,6 +93,20 @@ class Lines:
             return None
         line, self.buf = self.buf.split(b"\n", 1)
         return json.loads(line)
+
+    def pop_ready(self):
+        """Whether a complete message is there, reading what the socket
+        holds without blocking."""
+        if b"\n" in self.buf:
+            return True
+        if not self.eof:
+            import select
+            while select.select([self.sock], [], [], 0)[0]:
+                if not self.feed():
+                    break
+                if b"\n" in self.buf:
+                    break
+        return b"\n" in self.buf
 
     def recv(self):
         """Block for the next message; None at EOF."""
@@ -122,8 +143,13 @@ def server(conf):
         check(ps.ps_set_queue_mode(h, ps.PS_QUEUE_ROUND_ROBIN, S), "set_queue_mode")
     gdt = cfg.grad_dtype
     fifo = conf.get("queue", "rr") == "fifo"
-    w0 = wl.make_w0(cfg, "cuda")
-    check(ps.ps_set_weights(h, w0.data_ptr()), "set_weights")
+    log = []
+    if conf.get("resume"):
+        check(ps.ps_load(h, conf["resume"]), "load")
+        log.append(["resume", ps.ps_timestamp(h)])
+    else:
+        w0 = wl.make_w0(cfg, "cuda")
+        check(ps.ps_set_weights(h, w0.data_ptr()), "set_weights")
     slots, reps, offer = {}, {}, {}
     for l in range(L):
         rc, g = ps.ps_alloc_rows(h, S, gdt)
@@ -156,11 +182,14 @@ def server(conf):
     sel = selectors.DefaultSelector()
     for l, ch in conns.items():
         sel.register(ch.sock, selectors.EVENT_READ, l)
-    log = []
     queued = {l: collections.deque() for l in range(L)}   # slots waiting, oldest first
     live, done = set(range(L)), set()
 
+    stopping = False
+
     def on_message(l, m):
+        if "push" in m and stopping:
+            return                         # after the stop decision: lost, as in a crash
         if "push" in m:
             s = m["push"]
             if fifo and check(ps.ps_pending(h), "pending") >= D:
@@ -173,7 +202,7 @@ def server(conf):
 
     def on_eof(l):
         sel.unregister(conns[l].sock)
-        if l in live and l not in done:
+        if l in live and l not in done and not stopping:
             if conf["dead_mode"] == "retire":
                 cnt = check(ps.ps_retire_learner(h, l), "retire_learner")
             else:
@@ -217,8 +246,39 @@ def server(conf):
             except (BrokenPipeError, ConnectionResetError):
                 pass                          # it died; its EOF is read next
 
+    def stop_and_checkpoint():
+        """The watchdog's restart point: no more pushes are taken, the
+        learners are told to stop and detach (they release the shared rows
+        before this process frees them), the queued gradients are applied
+        and the checkpoint is written."""
+        nonlocal stopping
+        stopping = True
+        for l in sorted(live):
+            try:
+                conns[l].send({"stop": 1})
+            except (BrokenPipeError, ConnectionResetError):
+                pass
+        t_stop = time.monotonic() + 60
+        while live:
+            drain(0.5)
+            if time.monotonic() > t_stop:
+                raise RuntimeError("server: learners did not stop")
+        while check(ps.ps_pending(h), "pending"):
+            apply_and_pull()
+        check(ps.ps_save(h, conf["checkpoint"]), "save")
+        log.append(["checkpoint", ps.ps_timestamp(h)])
+        with open(os.path.join(conf["out"], "server.json"), "w") as f:
+            json.dump({"log": log, "ts": ps.ps_timestamp(h)}, f)
+        ps.ps_destroy(h)
+        lsock.close()
+        say(f"server: checkpoint at ts {log[-1][1]}, stopping")
+        return 0
+
+    applies = 0
     t_end = time.monotonic() + conf.get("limit", 120)
     while time.monotonic() < t_end:
+        if conf.get("stop_after") and applies >= conf["stop_after"]:
+            return stop_and_checkpoint()
         got = drain(0.05)
         # everything already there or arriving within 2 ms (a learner that
         # stops right after a push closes its socket just after it), EOFs included
@@ -230,6 +290,7 @@ def server(conf):
             break
         if pending >= D or (pending > 0 and (not got or not active)):
             apply_and_pull()
+            applies += 1
     else:
         raise RuntimeError("server: run did not finish in time")
 
@@ -303,18 +364,34 @@ def learner(conf, l):
     grads = {}
     bye = None
 
+    stop = False
+
     def handle(m):
-        nonlocal bye
+        nonlocal bye, stop
         if m is None:
             raise RuntimeError(f"learner {l}: server went away")
         if "free" in m:
             free.extend(m["free"])
         elif "bye" in m:
             bye = m["bye"]
+        elif "stop" in m:
+            stop = True
+
+    def detach(why):
+        c.close()
+        check(ps.ps_release_rows(g0), "release_rows")
+        check(ps.ps_release_rows(r0), "release_rows")
+        say(f"learner {l}: {why}")
+        return 0
 
     for k in range(conf["pushes"][l]):
-        while not free:
+        while not free and not stop:
             handle(ch.recv())
+        while ch.pop_ready():             # messages already there (a stop among them)
+            handle(ch.pop())
+        if stop:
+            del slot, replica
+            return detach(f"stopped by the server after {k} pushes")
         s = free.popleft()
         j = buffer_of(conf, l, k)
         if j not in grads:
@@ -323,15 +400,14 @@ def learner(conf, l):
         torch.cuda.synchronize()           # the write is complete before the push
         ch.send({"push": s, "buf": j})
         if die is not None and k + 1 == die:
-            c.close()                      # dies here, gradients still queued
-            del slot, replica
-            check(ps.ps_release_rows(g0), "release_rows")
-            check(ps.ps_release_rows(r0), "release_rows")
-            say(f"learner {l}: stopping after {k + 1} pushes")
-            return 0
+            del slot, replica              # dies here, gradients still queued
+            return detach(f"stopping after {k + 1} pushes")
     ch.send({"done": 1})
-    while bye is None:
+    while bye is None and not stop:
         handle(ch.recv())
+    if stop:
+        del slot, replica
+        return detach("stopped by the server after its last push")
     digest = hashlib.sha256(replica.cpu().numpy().tobytes()).hexdigest()
     with open(os.path.join(conf["out"], f"learner{l}.json"), "w") as f:
         json.dump({"ts": bye, "replica_sha256": digest}, f)

@@ -40,6 +40,7 @@ def run_processes(spawner, tmp_path, conf):
     """Start the server and the learners together; returns the server log."""
     sock_dir = f"/tmp/mp_ps_{os.getpid()}_{abs(hash(str(tmp_path))) % 100000}"
     os.makedirs(sock_dir, exist_ok=True)
+    os.makedirs(tmp_path, exist_ok=True)
     conf = dict(conf, sock=os.path.join(sock_dir, "s"), out=str(tmp_path))
     if os.path.exists(conf["sock"]):
         os.unlink(conf["sock"])
@@ -57,14 +58,16 @@ def run_processes(spawner, tmp_path, conf):
         return conf, json.load(f)
 
 
-def replay(torch, conf, log):
-    """The oracle through the server's calls, in the server's order."""
+def replay(torch, conf, log, o=None):
+    """The oracle through the server's calls, in the server's order (from a
+    given oracle state, for the run after a restart)."""
     cfg = mp_ps.workload(conf)
-    w0 = parity.np_bits(wl.make_w0(cfg, "cuda"))
     pool = {}
-    o = orc.OracleServer(w0, conf["lr"], conf["momentum"], depth=conf["depth"])
-    if conf.get("queue", "rr") == "rr":
-        assert o.set_queue_mode(orc.ROUND_ROBIN, conf["slots"]) == orc.OK
+    if o is None:
+        w0 = parity.np_bits(wl.make_w0(cfg, "cuda"))
+        o = orc.OracleServer(w0, conf["lr"], conf["momentum"], depth=conf["depth"])
+        if conf.get("queue", "rr") == "rr":
+            assert o.set_queue_mode(orc.ROUND_ROBIN, conf["slots"]) == orc.OK
     deaths = []
     for e in log:
         if e[0] == "push":
@@ -85,6 +88,10 @@ def replay(torch, conf, log):
         elif e[0] == "drop":
             assert o.drop_learner(e[1]) == e[2]
             deaths.append(e)
+        elif e[0] == "checkpoint":
+            assert o.pending() == 0 and o.ts == e[1]
+        elif e[0] == "resume":
+            assert o.restart() == orc.OK and o.ts == e[1]
         else:
             raise AssertionError(e)
     return o, deaths
@@ -131,3 +138,32 @@ def test_learner_processes_share_server_rows(torch, spawner, tmp_path, dead_mode
             assert got["replica_sha256"] == want
     if not die:
         assert deaths == []
+
+
+def test_restart_from_checkpoint_in_new_processes(torch, spawner, tmp_path):
+    """Sec. 4.3's restart across processes: after 5 applies the server takes
+    no more pushes, tells its learners to stop (they detach), applies what
+    is queued, writes a checkpoint and exits. A new server process loads it
+    and four new learner processes push on. Both runs' logs replayed through
+    one oracle (with its restart between them: pull history starts afresh,
+    learners keep their timestamps) give the final w, v and replicas bit for
+    bit."""
+    ckpt = str(tmp_path / "ps.ckpt")
+    base = dict(CONF, die={}, dead_mode="retire")
+    c1, out1 = run_processes(spawner, tmp_path / "first",
+                             dict(base, stop_after=5, checkpoint=ckpt))
+    assert out1["log"][-1][0] == "checkpoint"
+    c2, out2 = run_processes(spawner, tmp_path / "second",
+                             dict(base, resume=ckpt, push_offset=3, pushes=[6, 6, 6, 6]))
+    assert out2["log"][0] == ["resume", out1["ts"]]
+    o, _ = replay(torch, c1, out1["log"])
+    o, _ = replay(torch, c2, out2["log"], o)
+    assert o.ts == out2["ts"] and o.pending() == 0
+    second = tmp_path / "second"
+    assert parity.bitwise(np.load(second / "w.npy"), o.w)
+    assert parity.bitwise(np.load(second / "v.npy"), o.v)
+    for l in range(4):
+        with open(second / f"learner{l}.json") as f:
+            got = json.load(f)
+        assert got["ts"] == o.ts
+        assert got["replica_sha256"] == hashlib.sha256(o.replicas[("replica", l)].tobytes()).hexdigest()

@@ -810,3 +810,44 @@ def test_bf16_gradients_shift_w_by_the_propagated_quantisation():
     effect = np.abs(a - ref).max()
     assert effect > 4 * rounding                       # the quantisation is visible ...
     assert np.abs(a - ref - pred).max() <= rounding     # ... and is exactly the predicted shift
+
+
+def test_restart_keeps_the_run_and_forgets_pulls():
+    """Sec. 4.3 restart: resuming from a checkpoint (empty queue) continues
+    the uninterrupted run bit for bit -- weights, velocity, timestamps,
+    staleness (learners keep the timestamps they held), round-robin position
+    -- except that pull history starts afresh: a pull that would have been
+    skipped as current is made again, with the same bits, and a retired
+    learner is live again."""
+    rng = np.random.default_rng(43)
+    w0 = rng.uniform(-0.05, 0.05, 32).astype(np.float32)
+    gs = [rand_f32(rng, 32, 0.01) for _ in range(12)]
+    for mode in (orc.FIFO, orc.ROUND_ROBIN):
+        a = orc.OracleServer(w0, 0.01, 0.9, depth=4)
+        b = orc.OracleServer(w0, 0.01, 0.9, depth=4)
+        for s in (a, b):
+            s.set_queue_mode(mode, 2)
+        for s in (a, b):
+            for j in range(6):
+                assert s.push(j % 3, gs[j]) == orc.OK
+                if s.pending() == 2:
+                    s.apply_pending()
+            while s.pending():
+                s.apply_pending()
+            assert s.pull(1, "r1") is True
+        b.retire_learner(2)
+        assert b.push(2, gs[0]) == orc.ESTATE
+        assert b.restart() == orc.OK
+        assert a.pull(1, "r1") is False and b.pull(1, "r1") is True   # history forgotten
+        assert np.array_equal(bits(a.replicas["r1"]), bits(b.replicas["r1"]))
+        for s in (a, b):
+            for j in range(6, 12):
+                assert s.push(j % 3, gs[j]) == orc.OK
+                if s.pending() == 2:
+                    s.apply_pending()
+            while s.pending():
+                s.apply_pending()
+        assert np.array_equal(bits(a.w), bits(b.w)) and np.array_equal(bits(a.v), bits(b.v))
+        assert a.staleness == b.staleness and a.applied_order == b.applied_order and a.ts == b.ts
+        b.push(0, gs[0])
+        assert b.restart() == orc.ESTATE                               # needs an empty queue
