@@ -34,17 +34,22 @@ struct PullArgs {
 
 // Launch geometry: blocks are 256 threads; max_blocks caps the grid (the
 // kernels then stride over the remaining chunks). 0 = one chunk per lane.
-// fp32-gradient kernels may reserve LDS (they use none) so that only a few
-// blocks fit per compute unit: lds_for_blocks[b] leaves room for exactly b
-// blocks (b = 1..4; 0 = no such reservation on this device; chosen at server
-// creation). An asynchronous apply is told how many blocks to allow
-// (apply_shape_f32, ps_layout.h); synchronous steps take one block per CU
-// from sync_one_block_min_k gradients on.
+// The kernels may reserve LDS (they use none) so that only a few blocks fit
+// per compute unit: lds_for_blocks[b] leaves room for exactly b blocks
+// (b = 1..4; 0 = no such reservation on this device; chosen at server
+// creation). Every apply and synchronous step is told its shape
+// (apply_shape, sync_shape; ps_layout.h).
 struct Geometry {
     int max_blocks = 0;
     int fronts_log2 = -1;   // -1: chosen per apply (fronts_log2_for, ps_layout.h)
     unsigned lds_for_blocks[5] = {0, 0, 0, 0, 0};
-    int sync_one_block_min_k = 16;
+};
+
+// How one apply launch runs: resident blocks per compute unit (1..4; 0 = as
+// many as fit) and gradients per load group (4, 8, 12 or 16; others = 16).
+struct Shape {
+    int blocks_per_cu = 0;
+    int group = 16;
 };
 
 // LDS bytes that leave room for exactly `blocks` (1..4) blocks per compute
@@ -55,15 +60,15 @@ unsigned blocks_per_cu_lds(int blocks);
 // grad_dtype: PS_F32 | PS_BF16. pull_dtype: -1 (no replicas), PS_F32, PS_BF16.
 // level: 2 = every buffer 16-byte aligned; 1 = fp32 buffers 16-byte and bf16
 // buffers 8-byte aligned; 0 = anything else (scalar kernels).
-// blocks_per_cu: 1..4 resident blocks per compute unit for fp32 gradients
-// (0 = as many as fit; ignored for bf16 gradients and the scalar kernels).
+// shape: residency and group size of the vector kernels (the scalar kernel
+// for misaligned buffers ignores it).
 hipError_t launch_apply(const ApplyArgs &a, int grad_dtype, int pull_dtype, int level,
-                        int blocks_per_cu, const Geometry &geo, hipStream_t s);
+                        const Shape &shape, const Geometry &geo, hipStream_t s);
 hipError_t launch_pull(const PullArgs &a, int pull_dtype, int level, const Geometry &geo,
                        hipStream_t s);
 // Synchronous step over a.k gradients of one dtype (no replicas).
-hipError_t launch_sync(const ApplyArgs &a, int grad_dtype, int level, const Geometry &geo,
-                       hipStream_t s);
+hipError_t launch_sync(const ApplyArgs &a, int grad_dtype, int level, const Shape &shape,
+                       const Geometry &geo, hipStream_t s);
 hipError_t launch_zero(float *p, uint64_t n, hipStream_t s);
 
 }  // namespace gadei

@@ -54,9 +54,11 @@ namespace {
 #endif
 
 constexpr int kBlock = PS_BLOCK;      // threads per block (waves of 64 lanes)
-constexpr int kGroup = PS_GROUP;      // gradients whose loads are issued together
-// apply_chunk and sync_chunk take full groups of kGroup, then one of 8, then
-// a predicated group of at most 7: that covers every K only for kGroup <= 16.
+// Gradients whose loads are issued together: the synchronous step always
+// takes kGroup; an apply takes the group size its launcher chooses (4, 8,
+// 12 or 16). Full groups, then one of 8, then a predicated group of at most
+// 7 cover every K for group sizes up to 16.
+constexpr int kGroup = PS_GROUP;
 static_assert(kGroup >= 1 && kGroup <= 16, "gradient group size must be 1..16");
 // w and v are read once and written once per launch and are not touched
 // again until the next apply, after tens of GB of other traffic: stream them
@@ -214,8 +216,8 @@ __device__ __forceinline__ void step(float (&w)[E], float (&v)[E], const float (
 
 // Coordinates i .. i+E-1 through all K pending gradients, oldest first.
 // Gradients go in groups whose loads are all issued before the group's
-// updates, so each lane keeps many independent loads in flight: full groups
-// of kGroup, then one of 8 if that many remain (neither carries predicates,
+// updates, so each lane keeps several independent loads in flight: full
+// groups of G, then one of 8 if that many remain (neither carries predicates,
 // so their pointer loads batch and the waits count down one load at a
 // time), then a predicated group for the last 0..7.
 template <bool MOM, int GDT, int E, int G>
@@ -228,8 +230,9 @@ __device__ __forceinline__ void apply_group(const ApplyArgs &a, int k0, uint64_t
     for (int j = 0; j < G; ++j) step<MOM, E>(w, v, g[j], lr, m);
 }
 
-template <bool MOM, int GDT, int PDT, int E>
+template <bool MOM, int GDT, int PDT, int E, int G>
 __device__ __forceinline__ void apply_chunk(const ApplyArgs &a, uint64_t i) {
+    static_assert(G >= 1 && G <= 16, "gradient group size must be 1..16");
     float w[E], v[E];
     ld_f32<E, nt_wv_ld<E>()>(w, a.w + i);
     if constexpr (MOM) ld_f32<E, nt_wv_ld<E>()>(v, a.v + i);
@@ -237,8 +240,8 @@ __device__ __forceinline__ void apply_chunk(const ApplyArgs &a, uint64_t i) {
     const float m = a.m;
     const int k = a.k;
     int k0 = 0;
-    for (; k0 + kGroup <= k; k0 += kGroup) apply_group<MOM, GDT, E, kGroup>(a, k0, i, w, v, lr, m);
-    if constexpr (kGroup > 8) {
+    for (; k0 + G <= k; k0 += G) apply_group<MOM, GDT, E, G>(a, k0, i, w, v, lr, m);
+    if constexpr (G > 8) {
         if (k0 + 8 <= k) {
             apply_group<MOM, GDT, E, 8>(a, k0, i, w, v, lr, m);
             k0 += 8;
@@ -275,8 +278,9 @@ __device__ __forceinline__ void sum_group(const ApplyArgs &a, int k0, uint64_t i
         for (int e = 0; e < E; ++e) s[e] = s[e] + g[j][e];
 }
 
-template <bool MOM, int GDT, int E>
+template <bool MOM, int GDT, int E, int G>
 __device__ __forceinline__ void sync_chunk(const ApplyArgs &a, uint64_t i) {
+    static_assert(G >= 1 && G <= 16, "gradient group size must be 1..16");
     float w[E], v[E], s[E];
     ld_f32<E, nt_wv_ld<E>()>(w, a.w + i);
     if constexpr (MOM) ld_f32<E, nt_wv_ld<E>()>(v, a.v + i);
@@ -284,8 +288,8 @@ __device__ __forceinline__ void sync_chunk(const ApplyArgs &a, uint64_t i) {
     for (int e = 0; e < E; ++e) s[e] = 0.0f;
     const int k = a.k;
     int k0 = 0;
-    for (; k0 + kGroup <= k; k0 += kGroup) sum_group<GDT, E, kGroup>(a, k0, i, s);
-    if constexpr (kGroup > 8) {
+    for (; k0 + G <= k; k0 += G) sum_group<GDT, E, G>(a, k0, i, s);
+    if constexpr (G > 8) {
         if (k0 + 8 <= k) {
             sum_group<GDT, E, 8>(a, k0, i, s);
             k0 += 8;
@@ -322,27 +326,27 @@ __device__ __forceinline__ uint64_t front_block(unsigned b, unsigned nb, int f) 
     return b;
 }
 
-template <bool MOM, int GDT, int E>
+template <bool MOM, int GDT, int E, int G>
 __global__ void __launch_bounds__(kBlock) sync_vec(const ApplyArgs a) {
     const uint64_t chunks = a.n / E;
     const uint64_t tid = static_cast<uint64_t>(blockIdx.x) * kBlock + threadIdx.x;
     const uint64_t vtid = front_block(blockIdx.x, gridDim.x, a.fronts_log2) * kBlock + threadIdx.x;
     const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kBlock;
-    for (uint64_t c = vtid; c < chunks; c += stride) sync_chunk<MOM, GDT, E>(a, c * E);
-    if (tid < a.n - chunks * E) sync_chunk<MOM, GDT, 1>(a, chunks * E + tid);
+    for (uint64_t c = vtid; c < chunks; c += stride) sync_chunk<MOM, GDT, E, G>(a, c * E);
+    if (tid < a.n - chunks * E) sync_chunk<MOM, GDT, 1, G>(a, chunks * E + tid);
 }
 
 // Vector path: lane t of the grid owns E-coordinate chunks t', t' + stride,
 // ... where t' is t with its block renumbered by front_block. The n mod E
 // trailing coordinates go to the first lanes of the grid.
-template <bool MOM, int GDT, int PDT, int E>
+template <bool MOM, int GDT, int PDT, int E, int G>
 __global__ void __launch_bounds__(kBlock) apply_vec(const ApplyArgs a) {
     const uint64_t chunks = a.n / E;
     const uint64_t tid = static_cast<uint64_t>(blockIdx.x) * kBlock + threadIdx.x;
     const uint64_t vtid = front_block(blockIdx.x, gridDim.x, a.fronts_log2) * kBlock + threadIdx.x;
     const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kBlock;
-    for (uint64_t c = vtid; c < chunks; c += stride) apply_chunk<MOM, GDT, PDT, E>(a, c * E);
-    if (tid < a.n - chunks * E) apply_chunk<MOM, GDT, PDT, 1>(a, chunks * E + tid);
+    for (uint64_t c = vtid; c < chunks; c += stride) apply_chunk<MOM, GDT, PDT, E, G>(a, c * E);
+    if (tid < a.n - chunks * E) apply_chunk<MOM, GDT, PDT, 1, G>(a, chunks * E + tid);
 }
 
 // Scalar path for buffers without vector alignment: one coordinate per lane.
@@ -350,7 +354,7 @@ template <bool MOM, int GDT, int PDT>
 __global__ void __launch_bounds__(kBlock) apply_scalar(const ApplyArgs a) {
     const uint64_t tid = static_cast<uint64_t>(blockIdx.x) * kBlock + threadIdx.x;
     const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kBlock;
-    for (uint64_t i = tid; i < a.n; i += stride) apply_chunk<MOM, GDT, PDT, 1>(a, i);
+    for (uint64_t i = tid; i < a.n; i += stride) apply_chunk<MOM, GDT, PDT, 1, kGroup>(a, i);
 }
 
 // ---------------------------------------------------------------- pull
@@ -499,81 +503,96 @@ unsigned grid_for(uint64_t items, const Geometry &geo) {
     return static_cast<unsigned>(blocks < cap ? blocks : cap);
 }
 
+template <bool MOM, int GDT, int PDT, int E, int G>
+hipError_t launch_vec(const ApplyArgs &a, unsigned lds, const Geometry &geo, hipStream_t s) {
+    hipLaunchKernelGGL((apply_vec<MOM, GDT, PDT, E, G>), dim3(grid_for(a.n / E, geo)), dim3(kBlock),
+                       lds, s, a);
+    return hipGetLastError();
+}
+
+template <bool MOM, int GDT, int PDT, int E>
+hipError_t launch_vec_g(const ApplyArgs &a, int group, unsigned lds, const Geometry &geo,
+                        hipStream_t s) {
+    switch (group) {
+        case 4: return launch_vec<MOM, GDT, PDT, E, 4>(a, lds, geo, s);
+        case 8: return launch_vec<MOM, GDT, PDT, E, 8>(a, lds, geo, s);
+        case 12: return launch_vec<MOM, GDT, PDT, E, 12>(a, lds, geo, s);
+        default: return launch_vec<MOM, GDT, PDT, E, 16>(a, lds, geo, s);
+    }
+}
+
 template <bool MOM, int GDT, int PDT>
-hipError_t go_apply(const ApplyArgs &a, int level, int bpc, const Geometry &geo, hipStream_t s) {
+hipError_t go_apply(const ApplyArgs &a, int level, const Shape &sh, const Geometry &geo,
+                    hipStream_t s) {
     if (level == 0) {
         hipLaunchKernelGGL((apply_scalar<MOM, GDT, PDT>), dim3(grid_for(a.n, geo)), dim3(kBlock),
                            0, s, a);
         return hipGetLastError();
     }
+    // Residency as the caller asks (apply_shape, ps_layout.h), reserved via
+    // dynamic LDS that the kernel does not use; 0 blocks = as many as fit.
+    const unsigned lds =
+        (sh.blocks_per_cu >= 1 && sh.blocks_per_cu <= 4) ? geo.lds_for_blocks[sh.blocks_per_cu] : 0;
     // bf16 gradients move 16 bytes per lane as 8 values when every buffer is
     // 16-byte aligned; otherwise (and for fp32) a lane's chunk is 4 values.
-    const bool e8 = GDT == PS_BF16 && level == 2;
-    // fp32 gradients: the caller's residency (apply_shape_f32), reserved via
-    // dynamic LDS that the kernel does not use. bf16 gradients (half the
-    // bytes per value) measured best at full residency.
-    unsigned lds = 0;
-    if constexpr (GDT == PS_F32) {
-        if (bpc >= 1 && bpc <= 4) lds = geo.lds_for_blocks[bpc];
-    }
     if constexpr (GDT == PS_BF16) {
-        if (e8) {
-            hipLaunchKernelGGL((apply_vec<MOM, GDT, PDT, 8>), dim3(grid_for(a.n / 8, geo)),
-                               dim3(kBlock), lds, s, a);
-            return hipGetLastError();
-        }
+        if (level == 2) return launch_vec_g<MOM, GDT, PDT, 8>(a, sh.group, lds, geo, s);
     }
-    hipLaunchKernelGGL((apply_vec<MOM, GDT, PDT, 4>), dim3(grid_for(a.n / 4, geo)), dim3(kBlock),
-                       lds, s, a);
-    return hipGetLastError();
+    return launch_vec_g<MOM, GDT, PDT, 4>(a, sh.group, lds, geo, s);
 }
 
-template <bool MOM, int GDT>
-hipError_t go_sync(const ApplyArgs &a, int level, const Geometry &geo, hipStream_t s) {
-    if (level == 0) {
-        hipLaunchKernelGGL((sync_vec<MOM, GDT, 1>), dim3(grid_for(a.n, geo)), dim3(kBlock), 0, s,
-                           a);
-        return hipGetLastError();
-    }
-    // one block per CU from sync_one_block_min_k fp32 gradients on (VGG-16
-    // size, 16 learners: 1.58-1.61 ms vs 1.62 with two blocks, 1.74 full)
-    const unsigned lds =
-        (GDT == PS_F32 && a.k >= geo.sync_one_block_min_k) ? geo.lds_for_blocks[1] : 0;
-    if constexpr (GDT == PS_BF16) {
-        if (level == 2) {
-            hipLaunchKernelGGL((sync_vec<MOM, GDT, 8>), dim3(grid_for(a.n / 8, geo)),
-                               dim3(kBlock), lds, s, a);
-            return hipGetLastError();
-        }
-    }
-    hipLaunchKernelGGL((sync_vec<MOM, GDT, 4>), dim3(grid_for(a.n / 4, geo)), dim3(kBlock), lds,
+template <bool MOM, int GDT, int E, int G>
+hipError_t launch_sync_vec(const ApplyArgs &a, unsigned lds, const Geometry &geo, hipStream_t s) {
+    hipLaunchKernelGGL((sync_vec<MOM, GDT, E, G>), dim3(grid_for(a.n / E, geo)), dim3(kBlock), lds,
                        s, a);
     return hipGetLastError();
 }
 
+template <bool MOM, int GDT, int E>
+hipError_t launch_sync_g(const ApplyArgs &a, int group, unsigned lds, const Geometry &geo,
+                         hipStream_t s) {
+    switch (group) {
+        case 4: return launch_sync_vec<MOM, GDT, E, 4>(a, lds, geo, s);
+        case 8: return launch_sync_vec<MOM, GDT, E, 8>(a, lds, geo, s);
+        case 12: return launch_sync_vec<MOM, GDT, E, 12>(a, lds, geo, s);
+        default: return launch_sync_vec<MOM, GDT, E, 16>(a, lds, geo, s);
+    }
+}
+
 template <bool MOM, int GDT>
-hipError_t go_apply_p(const ApplyArgs &a, int pdt, int level, int bpc, const Geometry &geo,
+hipError_t go_sync(const ApplyArgs &a, int level, const Shape &sh, const Geometry &geo,
+                   hipStream_t s) {
+    if (level == 0) return launch_sync_vec<MOM, GDT, 1, kGroup>(a, 0, geo, s);
+    const unsigned lds =
+        (sh.blocks_per_cu >= 1 && sh.blocks_per_cu <= 4) ? geo.lds_for_blocks[sh.blocks_per_cu] : 0;
+    if constexpr (GDT == PS_BF16) {
+        if (level == 2) return launch_sync_g<MOM, GDT, 8>(a, sh.group, lds, geo, s);
+    }
+    return launch_sync_g<MOM, GDT, 4>(a, sh.group, lds, geo, s);
+}
+
+template <bool MOM, int GDT>
+hipError_t go_apply_p(const ApplyArgs &a, int pdt, int level, const Shape &sh, const Geometry &geo,
                       hipStream_t s) {
-    if (pdt == PS_F32) return go_apply<MOM, GDT, PS_F32>(a, level, bpc, geo, s);
-    if (pdt == PS_BF16) return go_apply<MOM, GDT, PS_BF16>(a, level, bpc, geo, s);
-    return go_apply<MOM, GDT, -1>(a, level, bpc, geo, s);
+    if (pdt == PS_F32) return go_apply<MOM, GDT, PS_F32>(a, level, sh, geo, s);
+    if (pdt == PS_BF16) return go_apply<MOM, GDT, PS_BF16>(a, level, sh, geo, s);
+    return go_apply<MOM, GDT, -1>(a, level, sh, geo, s);
 }
 
 template <bool MOM>
-hipError_t go_apply_g(const ApplyArgs &a, int gdt, int pdt, int level, int bpc,
+hipError_t go_apply_g(const ApplyArgs &a, int gdt, int pdt, int level, const Shape &sh,
                       const Geometry &geo, hipStream_t s) {
-    if (gdt == PS_BF16) return go_apply_p<MOM, PS_BF16>(a, pdt, level, bpc, geo, s);
-    return go_apply_p<MOM, PS_F32>(a, pdt, level, bpc, geo, s);
+    if (gdt == PS_BF16) return go_apply_p<MOM, PS_BF16>(a, pdt, level, sh, geo, s);
+    return go_apply_p<MOM, PS_F32>(a, pdt, level, sh, geo, s);
 }
 
 }  // namespace
 
 hipError_t launch_apply(const ApplyArgs &a, int grad_dtype, int pull_dtype, int level,
-                        int blocks_per_cu, const Geometry &geo, hipStream_t s) {
+                        const Shape &shape, const Geometry &geo, hipStream_t s) {
     if (a.r == 0) pull_dtype = -1;
-    if (a.v != nullptr)
-        return go_apply_g<true>(a, grad_dtype, pull_dtype, level, blocks_per_cu, geo, s);
-    return go_apply_g<false>(a, grad_dtype, pull_dtype, level, blocks_per_cu, geo, s);
+    if (a.v != nullptr) return go_apply_g<true>(a, grad_dtype, pull_dtype, level, shape, geo, s);
+    return go_apply_g<false>(a, grad_dtype, pull_dtype, level, shape, geo, s);
 }
 
 template <int PDT, int E>
@@ -624,14 +643,14 @@ void go_pull(const PullArgs &a, int level, const Geometry &geo, hipStream_t s) {
     }
 }
 
-hipError_t launch_sync(const ApplyArgs &a, int grad_dtype, int level, const Geometry &geo,
-                       hipStream_t s) {
+hipError_t launch_sync(const ApplyArgs &a, int grad_dtype, int level, const Shape &shape,
+                       const Geometry &geo, hipStream_t s) {
     if (a.v != nullptr) {
-        return grad_dtype == PS_BF16 ? go_sync<true, PS_BF16>(a, level, geo, s)
-                                     : go_sync<true, PS_F32>(a, level, geo, s);
+        return grad_dtype == PS_BF16 ? go_sync<true, PS_BF16>(a, level, shape, geo, s)
+                                     : go_sync<true, PS_F32>(a, level, shape, geo, s);
     }
-    return grad_dtype == PS_BF16 ? go_sync<false, PS_BF16>(a, level, geo, s)
-                                 : go_sync<false, PS_F32>(a, level, geo, s);
+    return grad_dtype == PS_BF16 ? go_sync<false, PS_BF16>(a, level, shape, geo, s)
+                                 : go_sync<false, PS_F32>(a, level, shape, geo, s);
 }
 
 hipError_t launch_pull(const PullArgs &a, int pull_dtype, int level, const Geometry &geo,

@@ -43,22 +43,66 @@ int fronts_log2_for(const void *const *ptrs, int count) {
     return (streams >= 8 && 2 * most > streams) ? 2 : 0;
 }
 
-ApplyShape apply_shape_f32(int k, bool momentum) {
-    if (momentum) {
-        if (k <= 1) return {0, 0};
-        if (k == 2) return {4, 0};
-        if (k <= 5) return {3, 0};
-        if (k == 16) return {1, 0};
-        if (k <= 23) return {2, 0};
-        return {1, 0};
+ApplyShape apply_shape(int k, bool momentum, bool bf16) {
+    if (bf16) {
+        if (momentum) {
+            if (k <= 16) return {0, 0, 16};
+            if (k <= 56) return {1, 0, 12};
+            return {1, 0, 8};
+        }
+        if (k <= 11) return {2, 0, 12};
+        if (k <= 19) return {2, 0, 4};
+        if (k <= 27) return {1, 0, 12};
+        if (k <= 39) return {1, 0, 16};
+        if (k <= 55) return {1, 0, 12};
+        return {1, 0, 16};
     }
-    if (k <= 2) return {0, 0};
-    if (k == 3) return {4, 0};
-    if (k <= 7) return {3, 0};
-    if (k <= 11) return {2, 0};
-    if (k <= 23) return {3, 1};
-    if (k <= 31) return {2, 1};
-    return {2, 0};
+    if (momentum) {
+        if (k <= 1) return {0, 0, 16};
+        if (k == 2) return {4, 0, 16};
+        if (k <= 5) return {3, 0, 16};
+        if (k <= 7) return {2, 0, 16};
+        if (k <= 23) return {2, 0, 4};
+        return {1, 0, 16};
+    }
+    if (k <= 2) return {0, 0, 16};
+    if (k == 3) return {4, 0, 16};
+    if (k <= 7) return {3, 0, 16};
+    if (k <= 11) return {2, 0, 16};
+    if (k <= 27) return {2, 0, 4};
+    if (k <= 39) return {1, 0, 12};
+    return {1, 0, 8};
+}
+
+ApplyShape sync_shape(int k, bool momentum, bool bf16) {
+    // Measured at 138,357,544 fp32 / 200,000,000 bf16 parameters with one
+    // gradient per learner, for 4, 8, 12, 16, 20, 24 and 32 learners; the
+    // counts between take the next measured one's shape.
+    if (bf16) {
+        if (momentum) {
+            if (k <= 4) return {3, 0, 16};
+            if (k <= 8) return {2, 0, 12};
+            if (k <= 12) return {2, 0, 4};
+            if (k <= 16) return {1, 0, 16};
+            if (k <= 20) return {1, 0, 12};
+            if (k <= 24) return {1, 0, 16};
+            return {1, 0, 8};
+        }
+        if (k <= 4) return {3, 0, 4};
+        if (k <= 16) return {2, 0, 4};
+        return {1, 0, 12};
+    }
+    if (momentum) {
+        if (k <= 4) return {2, 0, 16};
+        if (k <= 8) return {2, 0, 4};
+        if (k <= 12) return {1, 0, 12};
+        if (k <= 16) return {1, 0, 16};
+        if (k <= 20) return {1, 0, 12};
+        return {1, 0, 16};
+    }
+    if (k <= 4) return {3, 0, 16};
+    if (k <= 12) return {2, 0, 4};
+    return {1, 0, 16};
 }
 
 }  // namespace gadei

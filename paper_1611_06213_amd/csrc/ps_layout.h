@@ -61,30 +61,23 @@ RowLayout row_layout(size_t row_bytes, int count);
 // no better with four.
 int fronts_log2_for(const void *const *ptrs, int count);
 
-// Launch shape of an apply of k fp32 gradients: how many 256-thread blocks
-// one compute unit may hold (0 = as many as fit) and, for buffers at
-// distinct phases (where fronts_log2_for gives 0), how many fronts to sweep
-// (log2). Fewer resident blocks keep fewer DRAM pages and address
-// translations live across the k + 2 streams; many gradients per lane need
-// fewer waves to keep enough loads in flight. Measured at the VGG-16 size
-// (138M coordinates) from server rows, % of 8 TB/s, alternating settings in
-// one process, two processes:
-//   momentum, k = 2: 4 blocks 81.1-82.4, full residency 77.4-79.4;
-//   k = 3..5: 3 blocks 80.4-82.9 (full 72.8-77.1); k = 6..12: 2 blocks
-//   79.1-82.1 (full 69.9-71.8 at k = 6, 7); k = 16: 1 block 75.7-75.9,
-//   2 blocks 74.1-74.6; k = 20: 2 blocks 75.0-75.3, 1 block 70.1-72.4;
-//   k = 24, 32: 1 block 77.2-77.4 and 79.4-79.8, 2 blocks 74.0-74.5.
-//   no momentum, k = 2: full 79.5-80.4; k = 3: 4 blocks 80.2-80.7 (full
-//   76.3-77.5); k = 4..7: 3 blocks 78.7-83.9 (full 72.5-75.6); k = 8: 2
-//   blocks 76.9-77.4, 3 blocks 74.2-75.2; k = 12..20: 3 blocks with two
-//   fronts 75.0-77.0, 2 blocks with one 73.6-74.9; k = 24: 2 blocks with two
-//   fronts 77.4-77.7 (one front 75.3-75.4); k = 32: 2 blocks, one front
-//   79.0-79.3.
-// bf16 gradients measured best at full residency and take no extra front.
+// Launch shape of an apply of k gradients (fp32, or bf16): how many 256-thread
+// blocks one compute unit may hold (0 = as many as fit), for buffers at
+// distinct phases (where fronts_log2_for gives 0) how many fronts to sweep
+// (log2), and how many gradients each lane loads at once (4, 8, 12 or 16).
+// Fewer resident blocks and smaller groups keep fewer DRAM pages and address
+// translations live across the k + 2 streams; too few loads in flight starve
+// the memory system. Chosen from sweeps at the VGG-16 (fp32) and Mixed (bf16)
+// sizes from server rows; the measured values are in the design notes.
 struct ApplyShape {
     int blocks_per_cu;
     int fronts_log2;
+    int group;
 };
-ApplyShape apply_shape_f32(int k, bool momentum);
+ApplyShape apply_shape(int k, bool momentum, bool bf16);
+
+// The same for a synchronous step over k gradients (one per learner; no
+// fronts choice beyond the phase rule: fronts_log2 is 0).
+ApplyShape sync_shape(int k, bool momentum, bool bf16);
 
 }  // namespace gadei

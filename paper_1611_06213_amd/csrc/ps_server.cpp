@@ -143,10 +143,10 @@ int drain_pulls(ps_server *ps) {
     return PS_OK;
 }
 
-// Fronts for an apply over a.g[0..k) of dtype gdt, w and v: the server's
-// setting, or chosen from the buffers' offsets (fronts_log2_for), and for
-// fp32 gradients at distinct offsets from the gradient count
-// (apply_shape_f32).
+// Fronts for an apply over a.g[0..k) of dtype gdt (-1: no shape table), w
+// and v: the server's setting, or chosen from the buffers' offsets
+// (fronts_log2_for), and for buffers at distinct offsets from the apply's
+// shape (apply_shape).
 int fronts_for(const ps_server *ps, const gadei::ApplyArgs &a, int gdt) {
     if (ps->geo.fronts_log2 >= 0) return ps->geo.fronts_log2;
     const void *p[PS_MAX_QUEUE_DEPTH + 2];
@@ -155,7 +155,7 @@ int fronts_for(const ps_server *ps, const gadei::ApplyArgs &a, int gdt) {
     p[c++] = a.w;
     p[c++] = a.v;   // null without momentum: not a stream
     const int f = gadei::fronts_log2_for(p, c);
-    if (f == 0 && gdt == PS_F32) return gadei::apply_shape_f32(a.k, a.v != nullptr).fronts_log2;
+    if (f == 0 && gdt >= 0) return gadei::apply_shape(a.k, a.v != nullptr, gdt == PS_BF16).fronts_log2;
     return f;
 }
 
@@ -185,8 +185,10 @@ int launch_batch(ps_server *ps, const std::vector<PushDesc> &items, int pull_dty
         a.k = static_cast<int>(end - start);
         a.r = 0;
         a.fronts_log2 = fronts_for(ps, a, gdt);
-        const int bpc =
-            gdt == PS_F32 ? gadei::apply_shape_f32(a.k, a.v != nullptr).blocks_per_cu : 0;
+        const gadei::ApplyShape as = gadei::apply_shape(a.k, a.v != nullptr, gdt == PS_BF16);
+        gadei::Shape shape;
+        shape.blocks_per_cu = as.blocks_per_cu;
+        shape.group = as.group;
         int pdt = -1;
         if (end == q && pull_dtype >= 0 && !write.empty()) {
             pdt = pull_dtype;
@@ -196,7 +198,7 @@ int launch_batch(ps_server *ps, const std::vector<PushDesc> &items, int pull_dty
                 level = std::min(level, level_of(a.dst[j], pull_dtype));
             }
         }
-        hipError_t e = gadei::launch_apply(a, gdt, pdt, level, bpc, ps->geo, ps->stream);
+        hipError_t e = gadei::launch_apply(a, gdt, pdt, level, shape, ps->geo, ps->stream);
         if (e != hipSuccess) return fail_hip(e, "apply kernel launch");
         start = end;
     }
@@ -492,8 +494,12 @@ int ps_apply_sync(ps_server *ps) {
         a.g[j] = b.items[j].grad;
         level = std::min(level, level_of(a.g[j], gdt));
     }
-    a.fronts_log2 = fronts_for(ps, a, -1);   // the phase rule only (no apply_shape_f32)
-    hipError_t e = gadei::launch_sync(a, gdt, level, ps->geo, ps->stream);
+    a.fronts_log2 = fronts_for(ps, a, -1);   // the phase rule only (no apply_shape)
+    const gadei::ApplyShape ss = gadei::sync_shape(a.k, a.v != nullptr, gdt == PS_BF16);
+    gadei::Shape shape;
+    shape.blocks_per_cu = ss.blocks_per_cu;
+    shape.group = ss.group;
+    hipError_t e = gadei::launch_sync(a, gdt, level, shape, ps->geo, ps->stream);
     if (e != hipSuccess) return fail_hip(e, "synchronous step launch");
     ps->proto.commit_sync(b);
     return PS_OK;

@@ -13,7 +13,8 @@
 //   drop L | retire L | depth K | mode M S | skip 0|1 | state
 //   fronts A1 A2 ...      front choice for streams at addresses Ai (0 = none)
 //   rows B C              row layout of C rows of B bytes: head stride span
-//   shape K M             launch shape of a K-gradient fp32 apply (M = 1: momentum)
+//   shape K M B           launch shape of a K-gradient apply (M = 1: momentum; B = 1: bf16)
+//   sync_shape K M B      the same for a synchronous step over K learners
 #include <cstdio>
 #include <iostream>
 #include <sstream>
@@ -155,11 +156,13 @@ int main() {
             const gadei::RowLayout r = gadei::row_layout(bytes, static_cast<int>(count));
             std::printf("rows %zu %zu %zu %zu", r.head, r.stride, r.span,
                         gadei::velocity_offset(bytes));
-        } else if (cmd == "shape") {
-            long k, m;
-            in >> k >> m;
-            const gadei::ApplyShape sh = gadei::apply_shape_f32(static_cast<int>(k), m != 0);
-            std::printf("shape %d %d", sh.blocks_per_cu, sh.fronts_log2);
+        } else if (cmd == "shape" || cmd == "sync_shape") {
+            long k, m, b = 0;
+            in >> k >> m >> b;
+            const gadei::ApplyShape sh =
+                cmd == "shape" ? gadei::apply_shape(static_cast<int>(k), m != 0, b != 0)
+                               : gadei::sync_shape(static_cast<int>(k), m != 0, b != 0);
+            std::printf("%s %d %d %d", cmd.c_str(), sh.blocks_per_cu, sh.fronts_log2, sh.group);
         } else if (cmd == "state") {
             std::printf("state ts=%llu pending=%zu pulls=%llu skipped=%llu smax=%llu ssum=%llu hist=",
                         static_cast<unsigned long long>(p.ts), p.pending(),

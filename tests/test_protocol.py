@@ -257,20 +257,37 @@ def test_small_rows_are_packed(driver):
 
 
 def test_apply_shape_table(driver):
-    """The launch shapes fp32-gradient applies take (blocks per CU, 0 = no
-    cap; fronts log2), as measured at the VGG-16 size: momentum K = 2: 4
-    blocks, K = 3..5: 3, K = 6..15 and 17..23: 2, K = 16 and >= 24: 1; without
-    momentum K <= 2: no cap, K = 3: 4, K = 4..7: 3, K = 8..11: 2, K = 12..23: 3
-    with two fronts, K = 24..31: 2 with two fronts, K >= 32: 2."""
-    want_m = {1: (0, 0), 2: (4, 0), 3: (3, 0), 5: (3, 0), 6: (2, 0), 15: (2, 0), 16: (1, 0),
-              17: (2, 0), 23: (2, 0), 24: (1, 0), 32: (1, 0), 64: (1, 0)}
-    want_0 = {1: (0, 0), 2: (0, 0), 3: (4, 0), 4: (3, 0), 7: (3, 0), 8: (2, 0), 11: (2, 0),
-              12: (3, 1), 23: (3, 1), 24: (2, 1), 31: (2, 1), 32: (2, 0), 64: (2, 0)}
-    lines = [f"shape {k} 1" for k in want_m] + [f"shape {k} 0" for k in want_0]
-    got = run_driver(driver, lines)
-    assert got == [f"shape {b} {f}" for b, f in list(want_m.values()) + list(want_0.values())]
-    # every depth gets a shape within the launcher's range
-    allk = run_driver(driver, [f"shape {k} {m}" for k in range(1, 65) for m in (0, 1)])
-    for line in allk:
-        b, f = map(int, line.split()[1:])
-        assert 0 <= b <= 4 and f in (0, 1)
+    """The launch shapes applies and synchronous steps take (blocks per CU,
+    0 = no cap; fronts log2; gradients per load group), as measured at the
+    VGG-16 (fp32) and Mixed (bf16) sizes; every depth gets a shape the
+    launcher supports."""
+    for cmd, want in (("shape", SHAPES), ("sync_shape", SYNC_SHAPES)):
+        got = run_driver(driver, [f"{cmd} {k} {m} {b}" for (k, m, b) in want])
+        assert got == [f"{cmd} {x} {y} {z}" for (x, y, z) in want.values()]
+        allk = run_driver(driver, [f"{cmd} {k} {m} {b}" for k in range(1, 65) for m in (0, 1)
+                                   for b in (0, 1)])
+        for line in allk:
+            b, f, g = map(int, line.split()[1:])
+            assert 0 <= b <= 4 and f in (0, 1) and g in (4, 8, 12, 16)
+
+
+# (K, momentum, bf16) -> (blocks per CU, fronts log2, group)
+SHAPES = {
+    (1, 1, 0): (0, 0, 16), (2, 1, 0): (4, 0, 16), (4, 1, 0): (3, 0, 16), (6, 1, 0): (2, 0, 16),
+    (8, 1, 0): (2, 0, 4), (16, 1, 0): (2, 0, 4), (23, 1, 0): (2, 0, 4), (24, 1, 0): (1, 0, 16),
+    (32, 1, 0): (1, 0, 16), (64, 1, 0): (1, 0, 16),
+    (2, 0, 0): (0, 0, 16), (3, 0, 0): (4, 0, 16), (4, 0, 0): (3, 0, 16), (8, 0, 0): (2, 0, 16),
+    (12, 0, 0): (2, 0, 4), (27, 0, 0): (2, 0, 4), (32, 0, 0): (1, 0, 12), (48, 0, 0): (1, 0, 8),
+    (16, 1, 1): (0, 0, 16), (32, 1, 1): (1, 0, 12), (64, 1, 1): (1, 0, 8),
+    (8, 0, 1): (2, 0, 12), (16, 0, 1): (2, 0, 4), (32, 0, 1): (1, 0, 16), (48, 0, 1): (1, 0, 12),
+}
+
+# (learners, momentum, bf16) -> (blocks per CU, fronts log2, group)
+SYNC_SHAPES = {
+    (4, 1, 0): (2, 0, 16), (8, 1, 0): (2, 0, 4), (12, 1, 0): (1, 0, 12), (16, 1, 0): (1, 0, 16),
+    (20, 1, 0): (1, 0, 12), (32, 1, 0): (1, 0, 16),
+    (4, 0, 0): (3, 0, 16), (12, 0, 0): (2, 0, 4), (16, 0, 0): (1, 0, 16), (32, 0, 0): (1, 0, 16),
+    (4, 1, 1): (3, 0, 16), (8, 1, 1): (2, 0, 12), (12, 1, 1): (2, 0, 4), (16, 1, 1): (1, 0, 16),
+    (20, 1, 1): (1, 0, 12), (24, 1, 1): (1, 0, 16), (32, 1, 1): (1, 0, 8),
+    (4, 0, 1): (3, 0, 4), (16, 0, 1): (2, 0, 4), (32, 0, 1): (1, 0, 12),
+}
