@@ -54,10 +54,10 @@ namespace {
 #endif
 
 constexpr int kBlock = PS_BLOCK;      // threads per block (waves of 64 lanes)
-// Gradients whose loads are issued together: the synchronous step always
-// takes kGroup; an apply takes the group size its launcher chooses (4, 8,
-// 12 or 16). Full groups, then one of 8, then a predicated group of at most
-// 7 cover every K for group sizes up to 16.
+// Gradients whose loads are issued together: the vector kernels take the
+// group size their launcher chooses (4, 8, 12 or 16); the scalar paths take
+// kGroup. Full groups, then one of 8, then the remainder (at most 7) cover
+// every K for group sizes up to 16.
 constexpr int kGroup = PS_GROUP;
 static_assert(kGroup >= 1 && kGroup <= 16, "gradient group size must be 1..16");
 // w and v are read once and written once per launch and are not touched
@@ -120,33 +120,67 @@ __device__ __forceinline__ void st_f32(float *p, const float (&x)[E]) {
 __device__ __forceinline__ float lo_bf16(uint32_t u) { return __uint_as_float(u << 16); }
 __device__ __forceinline__ float hi_bf16(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
 
-// Gradient values for coordinates i .. i+E-1 (i is a multiple of E).
-// Gradients are read exactly once per launch, so the loads carry the
-// non-temporal hint. fp32 chunks are 4 values (16 bytes); bf16 chunks are 8
-// values (16 bytes) or 4 (8 bytes) when a buffer is only 8-byte aligned.
+// Gradient lanes for coordinates i .. i+E-1 (i is a multiple of E) as
+// loaded: fp32 chunks are 4 values (16 bytes); bf16 chunks are 8 values (16
+// bytes) or 4 (8 bytes) when a buffer is only 8-byte aligned. Gradients are
+// read exactly once per launch, so the loads carry the non-temporal hint.
+// Loading and widening are separate steps so that a group's loads can all be
+// issued before the first of its values is widened.
+template <int GDT, int E> struct GradBits;
+template <> struct GradBits<PS_F32, 4> { f32x4 u; };
+template <> struct GradBits<PS_F32, 1> { float u; };
+template <> struct GradBits<PS_BF16, 8> { u32x4 u; };
+template <> struct GradBits<PS_BF16, 4> { u32x2 u; };
+template <> struct GradBits<PS_BF16, 1> { uint32_t u; };
+
 template <int GDT, int E>
-__device__ __forceinline__ void ld_grad(float (&x)[E], const void *g, uint64_t i) {
+__device__ __forceinline__ GradBits<GDT, E> ld_bits(const void *g, uint64_t i) {
+    GradBits<GDT, E> r;
     if constexpr (GDT == PS_F32) {
         if constexpr (E == 1) {
-            x[0] = static_cast<const float *>(g)[i];
+            r.u = static_cast<const float *>(g)[i];
         } else {
-            ld_f32<E, true>(x, static_cast<const float *>(g) + i);
+            r.u = __builtin_nontemporal_load(
+                reinterpret_cast<const f32x4 *>(static_cast<const float *>(g) + i));
         }
     } else {
         if constexpr (E == 8) {
-            u32x4 u = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(g) + (i >> 3));
-            x[0] = lo_bf16(u.x); x[1] = hi_bf16(u.x);
-            x[2] = lo_bf16(u.y); x[3] = hi_bf16(u.y);
-            x[4] = lo_bf16(u.z); x[5] = hi_bf16(u.z);
-            x[6] = lo_bf16(u.w); x[7] = hi_bf16(u.w);
+            r.u = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(g) + (i >> 3));
         } else if constexpr (E == 4) {
-            u32x2 u = __builtin_nontemporal_load(reinterpret_cast<const u32x2 *>(g) + (i >> 2));
-            x[0] = lo_bf16(u.x); x[1] = hi_bf16(u.x);
-            x[2] = lo_bf16(u.y); x[3] = hi_bf16(u.y);
+            r.u = __builtin_nontemporal_load(reinterpret_cast<const u32x2 *>(g) + (i >> 2));
         } else {
-            x[0] = lo_bf16(static_cast<const uint16_t *>(g)[i]);
+            r.u = static_cast<const uint16_t *>(g)[i];
         }
     }
+    return r;
+}
+
+template <int GDT, int E>
+__device__ __forceinline__ void widen(float (&x)[E], const GradBits<GDT, E> &r) {
+    if constexpr (GDT == PS_F32) {
+        if constexpr (E == 1) {
+            x[0] = r.u;
+        } else {
+            x[0] = r.u.x; x[1] = r.u.y; x[2] = r.u.z; x[3] = r.u.w;
+        }
+    } else {
+        if constexpr (E == 8) {
+            x[0] = lo_bf16(r.u.x); x[1] = hi_bf16(r.u.x);
+            x[2] = lo_bf16(r.u.y); x[3] = hi_bf16(r.u.y);
+            x[4] = lo_bf16(r.u.z); x[5] = hi_bf16(r.u.z);
+            x[6] = lo_bf16(r.u.w); x[7] = hi_bf16(r.u.w);
+        } else if constexpr (E == 4) {
+            x[0] = lo_bf16(r.u.x); x[1] = hi_bf16(r.u.x);
+            x[2] = lo_bf16(r.u.y); x[3] = hi_bf16(r.u.y);
+        } else {
+            x[0] = lo_bf16(r.u);
+        }
+    }
+}
+
+template <int GDT, int E>
+__device__ __forceinline__ void ld_grad(float (&x)[E], const void *g, uint64_t i) {
+    widen<GDT, E>(x, ld_bits<GDT, E>(g, i));
 }
 
 // Two fp32 values -> two bf16 in one 32-bit word (a in the low half), each
@@ -214,22 +248,32 @@ __device__ __forceinline__ void step(float (&w)[E], float (&v)[E], const float (
     }
 }
 
-// Coordinates i .. i+E-1 through all K pending gradients, oldest first.
-// Gradients go in groups whose loads are all issued before the group's
-// updates, so each lane keeps several independent loads in flight: full
-// groups of G, then one of 8 if that many remain (neither carries predicates,
-// so their pointer loads batch and the waits count down one load at a
-// time), then a predicated group for the last 0..7.
+// Coordinates i .. i+E-1 through all K pending gradients, oldest first, in
+// groups whose loads are all issued before the group's updates, so each lane
+// keeps G independent loads in flight. The scheduling barrier keeps the
+// compiler from pulling the updates (and the bf16 widening) up between the
+// loads, which would make the later loads of a group wait for the earlier
+// ones to arrive.
 template <bool MOM, int GDT, int E, int G>
 __device__ __forceinline__ void apply_group(const ApplyArgs &a, int k0, uint64_t i, float (&w)[E],
                                             float (&v)[E], float lr, float m) {
-    float g[G][E];
+    GradBits<GDT, E> r[G];
 #pragma unroll
-    for (int j = 0; j < G; ++j) ld_grad<GDT, E>(g[j], a.g[k0 + j], i);
+    for (int j = 0; j < G; ++j) r[j] = ld_bits<GDT, E>(a.g[k0 + j], i);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int j = 0; j < G; ++j) step<MOM, E>(w, v, g[j], lr, m);
+    for (int j = 0; j < G; ++j) {
+        float g[E];
+        widen<GDT, E>(g, r[j]);
+        step<MOM, E>(w, v, g, lr, m);
+    }
 }
 
+// The first group is straight-line code after the w/v loads, so its loads
+// overlap theirs (the compiler waits for every outstanding load a loop reads
+// before entering the loop). The remainder after the full groups (and one
+// group of 8) is one straight-line group of its exact size: loads under
+// per-gradient conditions would each wait for the memory in turn.
 template <bool MOM, int GDT, int PDT, int E, int G>
 __device__ __forceinline__ void apply_chunk(const ApplyArgs &a, uint64_t i) {
     static_assert(G >= 1 && G <= 16, "gradient group size must be 1..16");
@@ -240,6 +284,10 @@ __device__ __forceinline__ void apply_chunk(const ApplyArgs &a, uint64_t i) {
     const float m = a.m;
     const int k = a.k;
     int k0 = 0;
+    if (k >= G) {
+        apply_group<MOM, GDT, E, G>(a, 0, i, w, v, lr, m);
+        k0 = G;
+    }
     for (; k0 + G <= k; k0 += G) apply_group<MOM, GDT, E, G>(a, k0, i, w, v, lr, m);
     if constexpr (G > 8) {
         if (k0 + 8 <= k) {
@@ -247,14 +295,15 @@ __device__ __forceinline__ void apply_chunk(const ApplyArgs &a, uint64_t i) {
             k0 += 8;
         }
     }
-    if (k0 < k) {
-        float g[8][E];
-#pragma unroll
-        for (int j = 0; j < 8; ++j)
-            if (k0 + j < k) ld_grad<GDT, E>(g[j], a.g[k0 + j], i);
-#pragma unroll
-        for (int j = 0; j < 8; ++j)
-            if (k0 + j < k) step<MOM, E>(w, v, g[j], lr, m);
+    switch (k - k0) {
+        case 1: apply_group<MOM, GDT, E, 1>(a, k0, i, w, v, lr, m); break;
+        case 2: apply_group<MOM, GDT, E, 2>(a, k0, i, w, v, lr, m); break;
+        case 3: apply_group<MOM, GDT, E, 3>(a, k0, i, w, v, lr, m); break;
+        case 4: apply_group<MOM, GDT, E, 4>(a, k0, i, w, v, lr, m); break;
+        case 5: apply_group<MOM, GDT, E, 5>(a, k0, i, w, v, lr, m); break;
+        case 6: apply_group<MOM, GDT, E, 6>(a, k0, i, w, v, lr, m); break;
+        case 7: apply_group<MOM, GDT, E, 7>(a, k0, i, w, v, lr, m); break;
+        default: break;
     }
     st_f32<E, nt_wv_st<E>()>(a.w + i, w);
     if constexpr (MOM) st_f32<E, nt_wv_st<E>()>(a.v + i, v);
@@ -266,7 +315,9 @@ __device__ __forceinline__ void apply_chunk(const ApplyArgs &a, uint64_t i) {
 // Synchronous SGD (Eq. "ssgd"): the K pending gradients (one per learner)
 // are summed per coordinate in push order from +0, divided by K (correctly
 // rounded division), and the average is applied as one step. Same streams
-// and grouping as the apply; only the reduction differs.
+// and gradient groups as the apply, loaded and waited for as the compiler
+// schedules them (the apply's load arrangement measured no faster here), the
+// remainder as one predicated group.
 template <int GDT, int E, int G>
 __device__ __forceinline__ void sum_group(const ApplyArgs &a, int k0, uint64_t i, float (&s)[E]) {
     float g[G][E];

@@ -44,33 +44,30 @@ int fronts_log2_for(const void *const *ptrs, int count) {
 }
 
 ApplyShape apply_shape(int k, bool momentum, bool bf16) {
+    // Measured at 138,357,544 fp32 / 200,000,000 bf16 parameters for the
+    // depths 1, 2, 3, 4, 6, 8, 12, 16, 20, 24, 32, 48 and 64 (bf16: from 8);
+    // the depths between take a neighbour's shape.
     if (bf16) {
-        if (momentum) {
-            if (k <= 16) return {0, 0, 16};
-            if (k <= 56) return {1, 0, 12};
-            return {1, 0, 8};
-        }
-        if (k <= 11) return {2, 0, 12};
-        if (k <= 19) return {2, 0, 4};
-        if (k <= 27) return {1, 0, 12};
-        if (k <= 39) return {1, 0, 16};
-        if (k <= 55) return {1, 0, 12};
-        return {1, 0, 16};
+        if (momentum) return k <= 11 ? ApplyShape{2, 0, 16} : ApplyShape{1, 0, 16};
+        if (k <= 11) return {2, 0, 8};
+        if (k <= 56) return {1, 0, 16};
+        return {1, 0, 8};
     }
     if (momentum) {
-        if (k <= 1) return {0, 0, 16};
-        if (k == 2) return {4, 0, 16};
-        if (k <= 5) return {3, 0, 16};
-        if (k <= 7) return {2, 0, 16};
-        if (k <= 23) return {2, 0, 4};
-        return {1, 0, 16};
+        if (k <= 1) return {4, 0, 16};
+        if (k == 2) return {3, 0, 4};
+        if (k <= 9) return {2, 0, 4};
+        if (k <= 13) return {1, 0, 12};
+        if (k <= 17) return {1, 0, 16};
+        if (k <= 21) return {1, 0, 12};
+        if (k <= 40) return {1, 0, 16};
+        return {1, 0, 8};
     }
     if (k <= 2) return {0, 0, 16};
-    if (k == 3) return {4, 0, 16};
-    if (k <= 7) return {3, 0, 16};
-    if (k <= 11) return {2, 0, 16};
-    if (k <= 27) return {2, 0, 4};
-    if (k <= 39) return {1, 0, 12};
+    if (k <= 6) return {3, 0, 4};
+    if (k <= 13) return {2, 0, 4};
+    if (k <= 17) return {1, 0, 16};
+    if (k <= 21) return {2, 0, 4};
     return {1, 0, 8};
 }
 
@@ -98,7 +95,8 @@ ApplyShape sync_shape(int k, bool momentum, bool bf16) {
         if (k <= 12) return {1, 0, 12};
         if (k <= 16) return {1, 0, 16};
         if (k <= 20) return {1, 0, 12};
-        return {1, 0, 16};
+        if (k <= 24) return {1, 0, 16};
+        return {1, 0, 8};
     }
     if (k <= 4) return {3, 0, 16};
     if (k <= 12) return {2, 0, 4};

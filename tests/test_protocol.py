@@ -273,19 +273,19 @@ def test_apply_shape_table(driver):
 
 # (K, momentum, bf16) -> (blocks per CU, fronts log2, group)
 SHAPES = {
-    (1, 1, 0): (0, 0, 16), (2, 1, 0): (4, 0, 16), (4, 1, 0): (3, 0, 16), (6, 1, 0): (2, 0, 16),
-    (8, 1, 0): (2, 0, 4), (16, 1, 0): (2, 0, 4), (23, 1, 0): (2, 0, 4), (24, 1, 0): (1, 0, 16),
-    (32, 1, 0): (1, 0, 16), (64, 1, 0): (1, 0, 16),
-    (2, 0, 0): (0, 0, 16), (3, 0, 0): (4, 0, 16), (4, 0, 0): (3, 0, 16), (8, 0, 0): (2, 0, 16),
-    (12, 0, 0): (2, 0, 4), (27, 0, 0): (2, 0, 4), (32, 0, 0): (1, 0, 12), (48, 0, 0): (1, 0, 8),
-    (16, 1, 1): (0, 0, 16), (32, 1, 1): (1, 0, 12), (64, 1, 1): (1, 0, 8),
-    (8, 0, 1): (2, 0, 12), (16, 0, 1): (2, 0, 4), (32, 0, 1): (1, 0, 16), (48, 0, 1): (1, 0, 12),
+    (1, 1, 0): (4, 0, 16), (2, 1, 0): (3, 0, 4), (4, 1, 0): (2, 0, 4), (8, 1, 0): (2, 0, 4),
+    (12, 1, 0): (1, 0, 12), (16, 1, 0): (1, 0, 16), (20, 1, 0): (1, 0, 12), (32, 1, 0): (1, 0, 16),
+    (40, 1, 0): (1, 0, 16), (48, 1, 0): (1, 0, 8), (64, 1, 0): (1, 0, 8),
+    (2, 0, 0): (0, 0, 16), (3, 0, 0): (3, 0, 4), (8, 0, 0): (2, 0, 4), (16, 0, 0): (1, 0, 16),
+    (20, 0, 0): (2, 0, 4), (32, 0, 0): (1, 0, 8), (64, 0, 0): (1, 0, 8),
+    (8, 1, 1): (2, 0, 16), (16, 1, 1): (1, 0, 16), (32, 1, 1): (1, 0, 16), (64, 1, 1): (1, 0, 16),
+    (8, 0, 1): (2, 0, 8), (16, 0, 1): (1, 0, 16), (48, 0, 1): (1, 0, 16), (64, 0, 1): (1, 0, 8),
 }
 
 # (learners, momentum, bf16) -> (blocks per CU, fronts log2, group)
 SYNC_SHAPES = {
     (4, 1, 0): (2, 0, 16), (8, 1, 0): (2, 0, 4), (12, 1, 0): (1, 0, 12), (16, 1, 0): (1, 0, 16),
-    (20, 1, 0): (1, 0, 12), (32, 1, 0): (1, 0, 16),
+    (20, 1, 0): (1, 0, 12), (32, 1, 0): (1, 0, 8),
     (4, 0, 0): (3, 0, 16), (12, 0, 0): (2, 0, 4), (16, 0, 0): (1, 0, 16), (32, 0, 0): (1, 0, 16),
     (4, 1, 1): (3, 0, 16), (8, 1, 1): (2, 0, 12), (12, 1, 1): (2, 0, 4), (16, 1, 1): (1, 0, 16),
     (20, 1, 1): (1, 0, 12), (24, 1, 1): (1, 0, 16), (32, 1, 1): (1, 0, 8),
