@@ -56,6 +56,9 @@ struct ps_server {
     // earlier lock-free pulls into the same buffers
     hipEvent_t pulls_done = nullptr;
     int fuse_max_r = 1;   // ps_apply_pull writes up to this many replicas in the apply pass
+    // ps_set_launch_shape: -1 / 0 = the shape tables' choice
+    int force_blocks_per_cu = -1;
+    int force_group = 0;
     gadei::Geometry geo;
     gadei::Protocol proto;
     // Every call on the handle holds this lock, so several host threads (a
@@ -159,6 +162,14 @@ int fronts_for(const ps_server *ps, const gadei::ApplyArgs &a, int gdt) {
     return f;
 }
 
+// The launch shape for a table entry, with the caller's overrides.
+gadei::Shape shape_for(const ps_server *ps, const gadei::ApplyShape &t) {
+    gadei::Shape shape;
+    shape.blocks_per_cu = ps->force_blocks_per_cu >= 0 ? ps->force_blocks_per_cu : t.blocks_per_cu;
+    shape.group = ps->force_group > 0 ? ps->force_group : t.group;
+    return shape;
+}
+
 // Launch a batch as runs of equal gradient dtype, in order. The last run
 // also writes the replicas listed in `write` when pull_dtype >= 0.
 int launch_batch(ps_server *ps, const std::vector<PushDesc> &items, int pull_dtype,
@@ -185,10 +196,8 @@ int launch_batch(ps_server *ps, const std::vector<PushDesc> &items, int pull_dty
         a.k = static_cast<int>(end - start);
         a.r = 0;
         a.fronts_log2 = fronts_for(ps, a, gdt);
-        const gadei::ApplyShape as = gadei::apply_shape(a.k, a.v != nullptr, gdt == PS_BF16);
-        gadei::Shape shape;
-        shape.blocks_per_cu = as.blocks_per_cu;
-        shape.group = as.group;
+        const gadei::Shape shape =
+            shape_for(ps, gadei::apply_shape(a.k, a.v != nullptr, gdt == PS_BF16));
         int pdt = -1;
         if (end == q && pull_dtype >= 0 && !write.empty()) {
             pdt = pull_dtype;
@@ -495,10 +504,7 @@ int ps_apply_sync(ps_server *ps) {
         level = std::min(level, level_of(a.g[j], gdt));
     }
     a.fronts_log2 = fronts_for(ps, a, -1);   // the phase rule only (no apply_shape)
-    const gadei::ApplyShape ss = gadei::sync_shape(a.k, a.v != nullptr, gdt == PS_BF16);
-    gadei::Shape shape;
-    shape.blocks_per_cu = ss.blocks_per_cu;
-    shape.group = ss.group;
+    const gadei::Shape shape = shape_for(ps, gadei::sync_shape(a.k, a.v != nullptr, gdt == PS_BF16));
     hipError_t e = gadei::launch_sync(a, gdt, level, shape, ps->geo, ps->stream);
     if (e != hipSuccess) return fail_hip(e, "synchronous step launch");
     ps->proto.commit_sync(b);
@@ -747,6 +753,18 @@ int ps_set_fronts(ps_server *ps, int fronts_log2) {
     if (fronts_log2 < -1 || fronts_log2 > 3)
         return fail(PS_EINVAL, "fronts_log2 %d outside [-1, 3]", fronts_log2);
     ps->geo.fronts_log2 = fronts_log2;
+    return PS_OK;
+}
+
+int ps_set_launch_shape(ps_server *ps, int blocks_per_cu, int group) {
+    if (int rc = check(ps)) return rc;
+    PS_LOCK(ps);
+    if (blocks_per_cu < -1 || blocks_per_cu > 4)
+        return fail(PS_EINVAL, "blocks_per_cu %d outside [-1, 4]", blocks_per_cu);
+    if (group != 0 && group != 4 && group != 8 && group != 12 && group != 16)
+        return fail(PS_EINVAL, "group %d is not 0, 4, 8, 12 or 16", group);
+    ps->force_blocks_per_cu = blocks_per_cu;
+    ps->force_group = group;
     return PS_OK;
 }
 

@@ -86,6 +86,7 @@ _SIGS = {
     "ps_set_queue_depth": (ctypes.c_int, [_VP, ctypes.c_int]),
     "ps_set_pull_skip": (ctypes.c_int, [_VP, ctypes.c_int]),
     "ps_set_fronts": (ctypes.c_int, [_VP, ctypes.c_int]),
+    "ps_set_launch_shape": (ctypes.c_int, [_VP, ctypes.c_int, ctypes.c_int]),
     "ps_set_queue_mode": (ctypes.c_int, [_VP, ctypes.c_int, ctypes.c_int]),
     "ps_last_applied": (ctypes.c_int, [_VP, ctypes.POINTER(ctypes.c_int), ctypes.c_int]),
     "ps_set_pull_fusion": (ctypes.c_int, [_VP, ctypes.c_int]),
@@ -369,6 +370,10 @@ def ps_set_fronts(h: int, fronts_log2: int) -> int:
     return load_library().ps_set_fronts(h, fronts_log2)
 
 
+def ps_set_launch_shape(h: int, blocks_per_cu: int, group: int) -> int:
+    return load_library().ps_set_launch_shape(h, blocks_per_cu, group)
+
+
 def ps_alloc_rows(h: int, count: int, dtype: int):
     """(status, [row addresses])."""
     out = (_VP * max(1, count))()
@@ -472,6 +477,9 @@ class ParameterServer:
 
     def set_fronts(self, fronts_log2: int) -> None:
         self._check(ps_set_fronts(self.h, fronts_log2), "set_fronts")
+
+    def set_launch_shape(self, blocks_per_cu: int = -1, group: int = 0) -> None:
+        self._check(ps_set_launch_shape(self.h, blocks_per_cu, group), "set_launch_shape")
 
     def set_pull_skip(self, enabled: bool) -> None:
         self._check(ps_set_pull_skip(self.h, enabled), "set_pull_skip")

@@ -1444,6 +1444,64 @@ def test_fronts_give_identical_bits(torch, layout, gdt):
     free(torch)
 
 
+@pytest.mark.parametrize("m", [0.0, 0.9])
+@pytest.mark.parametrize("gdt", ["f32", "bf16"])
+def test_every_group_and_remainder(torch, gdt, m):
+    """Every gradient group size the launcher takes (4, 8, 12, 16), forced
+    with ps_set_launch_shape at every depth from 1 to two groups and 8 more,
+    so that the first group, the loop over further groups, the group of 8 and
+    each exact remainder of 1..7 all run, under residency caps 0..4 in turn:
+    w and v equal the oracle's bits after the same gradients (batched is
+    sequential, so one oracle run gives every depth). The synchronous step
+    at every group size and depth too."""
+    n, lr, kmax = 3 * 8192 + 5, 0.01, 40
+    say(f"[case] groups x remainders gradients={gdt} m={m} n={n}")
+    tdt = torch.bfloat16 if gdt == "bf16" else torch.float32
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(41)
+    w0 = (torch.rand(n, generator=gen, device="cuda") - 0.5) * 0.1
+    grads = [(torch.randn(n, generator=gen, device="cuda") * 1e-3).to(tdt) for _ in range(kmax)]
+    host = [_host_grad(torch, g) for g in grads]
+    o = orc.OracleServer(w0.cpu().numpy(), lr, m, depth=1)
+    want = {}
+    for k in range(1, kmax + 1):
+        assert o.push(0, host[k - 1]) == orc.OK
+        o.apply_pending()
+        want[k] = (o.w.view(np.uint32).copy(), None if m == 0 else o.v.view(np.uint32).copy())
+    want_sync = {}
+    for k in range(1, kmax + 1):
+        so = orc.OracleServer(w0.cpu().numpy(), lr, m, depth=k)
+        for j in range(k):
+            assert so.push(j, host[j]) == orc.OK
+        so.apply_sync()
+        want_sync[k] = so.w.view(np.uint32).copy()
+    srv = ps.ParameterServer(n, lr, m, queue_depth=kmax)
+    case = 0
+    for group in (4, 8, 12, 16):
+        for k in range(1, min(2 * group + 8, kmax) + 1):
+            srv.set_launch_shape(case % 5, group)
+            case += 1
+            srv.set_weights(w0)
+            for j in range(k):
+                assert srv.push(j % 7, grads[j])
+            srv.apply_pending()
+            ww, wv = want[k]
+            assert parity.bitwise(parity.np_bits(srv.weights_copy()), ww), (group, k)
+            if m != 0:
+                assert parity.bitwise(parity.np_bits(srv.velocity_copy()), wv), (group, k)
+            srv.set_weights(w0)
+            for j in range(k):
+                assert srv.push(j, grads[j])
+            srv.apply_sync()
+            assert parity.bitwise(parity.np_bits(srv.weights_copy()), want_sync[k]), ("sync", group, k)
+    srv.set_launch_shape()
+    for bad in ((-2, 0), (5, 0), (1, 3), (1, 20)):
+        with pytest.raises(ps.PSError):
+            srv.set_launch_shape(*bad)
+    srv.close()
+    free(torch)
+
+
 # ---------------------------------------------------------------- host threads
 
 def test_learner_threads_push_while_server_applies(torch):
