@@ -362,7 +362,10 @@ int ps_export_rows(ps_server *ps, void *first_row, void *handle, size_t *offset)
  * follow at the stride the server's ps_alloc_rows reported). The learner
  * writes gradients into its slots and reads replicas there; every write must
  * have completed on the device before the server is told to push it.
- * ps_release_rows waits for this process's device work, then unmaps. */
+ * PS_EINVAL if offset lies outside the allocation or the row set is already
+ * imported in this process (import once, release once); PS_EHIP if the
+ * handle cannot be opened. ps_release_rows waits for this process's device
+ * work, then unmaps; PS_EINVAL for a row not imported here. */
 int ps_import_rows(const void *handle, size_t offset, void **first_row);
 int ps_release_rows(void *first_row);
 

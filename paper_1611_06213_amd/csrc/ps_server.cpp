@@ -305,9 +305,13 @@ int save_array(FILE *f, const float *dev, size_t n, std::vector<float> &buf, Fnv
 }
 
 // Row sets this process mapped with ps_import_rows: first row -> the base
-// hipIpcOpenMemHandle returned.
+// hipIpcOpenMemHandle returned and the handle it was opened from.
+struct Import {
+    void *base;
+    hipIpcMemHandle_t handle;
+};
 std::mutex g_import_mu;
-std::map<void *, void *> g_imports;
+std::map<void *, Import> g_imports;
 
 }  // namespace
 
@@ -319,13 +323,25 @@ int ps_import_rows(const void *handle, size_t offset, void **first_row) {
     if (handle == nullptr || first_row == nullptr) return fail(PS_EINVAL, "null argument");
     hipIpcMemHandle_t h;
     std::memcpy(&h, handle, sizeof h);
+    std::lock_guard<std::mutex> lock(g_import_mu);
+    for (const auto &kv : g_imports)
+        if (std::memcmp(&kv.second.handle, &h, sizeof h) == 0)
+            return fail(PS_EINVAL, "row set already imported in this process");
     void *base = nullptr;
     hipError_t e = hipIpcOpenMemHandle(&base, h, hipIpcMemLazyEnablePeerAccess);
     if (e != hipSuccess) return fail_hip(e, "hipIpcOpenMemHandle");
+    // the offset must name a byte of the mapped allocation
+    void *range_base = nullptr;
+    size_t range_size = 0;
+    e = hipMemGetAddressRange(&range_base, &range_size, base);
+    if (e != hipSuccess || range_base != base || offset >= range_size) {
+        (void)hipIpcCloseMemHandle(base);
+        if (e != hipSuccess) return fail_hip(e, "hipMemGetAddressRange");
+        return fail(PS_EINVAL, "offset %zu outside the %zu-byte allocation", offset, range_size);
+    }
     void *first = static_cast<char *>(base) + offset;
     try {
-        std::lock_guard<std::mutex> lock(g_import_mu);
-        g_imports[first] = base;
+        g_imports[first] = Import{base, h};
     } catch (...) {
         (void)hipIpcCloseMemHandle(base);
         return fail(PS_ENOMEM, "host allocation failed");
@@ -340,7 +356,7 @@ int ps_release_rows(void *first_row) {
         std::lock_guard<std::mutex> lock(g_import_mu);
         auto it = g_imports.find(first_row);
         if (it == g_imports.end()) return fail(PS_EINVAL, "not a row set imported here");
-        base = it->second;
+        base = it->second.base;
         g_imports.erase(it);
     }
     hipError_t e = hipDeviceSynchronize();

@@ -352,8 +352,15 @@ def learner(conf, l):
     ch = Lines(c)
     ch.send({"hello": l})
     offer = ch.recv()
+    if l == 0:   # the import refuses an offset outside the allocation, leaving nothing mapped
+        bad, _ = ps.ps_import_rows(bytes.fromhex(offer["grad"]), 1 << 50)
+        assert bad == ps.PS_EINVAL, bad
     rc, g0 = ps.ps_import_rows(bytes.fromhex(offer["grad"]), offer["goff"])
     check(rc, "import_rows")
+    if l == 0:   # ... and a second import of a mapped row set; release wants a first row
+        again, _ = ps.ps_import_rows(bytes.fromhex(offer["grad"]), offer["goff"])
+        assert again == ps.PS_EINVAL, again
+        assert ps.ps_release_rows(g0 + 16) == ps.PS_EINVAL
     rc, r0 = ps.ps_import_rows(bytes.fromhex(offer["rep"]), offer["roff"])
     check(rc, "import_rows")
     gtd = torch.bfloat16 if cfg.grad_dtype == wl.BF16 else torch.float32
