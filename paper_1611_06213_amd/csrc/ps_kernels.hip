@@ -428,37 +428,31 @@ __global__ void __launch_bounds__(kBlock) pull_vec(const PullArgs a) {
     if (tid < a.n - (chunks << 2)) pull_chunk<PDT, 1, true>(a, (chunks << 2) + tid);
 }
 
-// Tiled fan-out for R >= 2 replicas. w is cut into tiles (tile_coords); the
-// block index enumerates (tile, replica, block within the tile) with the last
-// fastest, so in-order dispatch walks replica 0 of tile 0, replica 1 of tile
-// 0, ... The R re-reads of a tile then hit the memory-side cache (the tile
-// is loaded with ordinary, allocating loads) and HBM sees one replica's
-// write stream at a time instead of R interleaved ones, which the memory
-// system serves markedly faster. HBM traffic stays one read of w plus the R
-// replica writes.
-// A tile is 4 Mi coordinates (16 MiB of w). fp32 replicas take one 16-byte
-// chunk per lane (4096 blocks per tile and replica), bf16 replicas two
-// 8-value chunks per lane (1024 blocks): with every block of a (tile,
-// replica) group resident at once, the chip writes one replica stream at a
-// time. Measured best of 4/8/16/32 MiB tiles and 1/2/4/8 chunks per lane for
-// each replica dtype.
-// Blocks are dispatched round-robin over the chip's 8 XCDs (block index mod
-// 8). When a group's block count is a multiple of 8 (every full-size group),
-// block b of the group works on slice (b mod 8) * (bpt / 8) + b / 8, so each
-// XCD writes one contiguous eighth of the tile per replica instead of 4 KiB
-// pieces interleaved with the other seven: fewer pages per XCD and per DRAM
-// row at a time (VGG-16's 16 fp32 replicas: 1.39 ms vs 1.45 ms). The same
-// XCD handles the same eighth for every replica, so its re-reads of the tile
-// stay in its own L2.
-template <int PDT>
-constexpr uint64_t tile_coords() { return uint64_t(4) << 20; }
-template <int PDT>
-constexpr uint64_t lane_chunks() { return PDT == PS_BF16 ? 2 : 1; }
+// Tiled fan-outs for R >= 2 replicas. w is cut into tiles; blocks enumerate
+// (tile, replica, block within the tile) with the last fastest, so in-order
+// dispatch walks replica 0 of tile 0, replica 1 of tile 0, ... The R
+// re-reads of a tile then hit the memory-side cache (the tile is loaded with
+// ordinary, allocating loads) and HBM sees one replica's write stream at a
+// time instead of R interleaved ones, which the memory system serves
+// markedly faster. HBM traffic stays one read of w plus the R replica
+// writes. One 16-byte chunk of w per lane (4 fp32 or 8 bf16 values): two
+// chunks per lane measured 4-5% slower for bf16 replicas.
+//
+// pull_tiled: 4 Mi-coordinate tiles on a 1-D grid (4096 blocks per tile and
+// replica). Blocks are dispatched round-robin over the chip's 8 XCDs (block
+// index mod 8); when a group's block count is a multiple of 8, block b of the
+// group works on slice (b mod 8) * (bpt / 8) + b / 8, so each XCD writes one
+// contiguous eighth of the tile per replica instead of 4 KiB pieces
+// interleaved with the other seven, and re-reads only its own eighth of the
+// tile from its own L2. Used for fp32 replicas of 8 or more tiles, where it
+// measured faster in whole steps (AlexNet's pulls 0.422 vs 0.426 ms, VGG-16's
+// 16 replicas 1.36-1.37 vs 1.38 ms); pull_slices below elsewhere.
+constexpr uint64_t kTiledCoords = uint64_t(4) << 20;
 constexpr unsigned kTileBlocks = 4096;      // most blocks per (tile, replica)
 
 template <int PDT, int E>
 __global__ void __launch_bounds__(kBlock) pull_tiled(const PullArgs a, unsigned bpt) {
-    constexpr uint64_t kTileChunksE = tile_coords<PDT>() / E;
+    constexpr uint64_t kTileChunksE = kTiledCoords / E;
     const uint64_t chunks = a.n / E;
     const unsigned b0 = blockIdx.x % bpt;
     const unsigned b = (bpt & 7u) == 0 ? (b0 & 7u) * (bpt >> 3) + (b0 >> 3) : b0;
@@ -482,21 +476,22 @@ __global__ void __launch_bounds__(kBlock) pull_tiled(const PullArgs a, unsigned 
     }
 }
 
-// The same fan-out on a 3-D grid (x: block within the tile, y: replica, z:
-// tile; dispatch order x fastest, as above). Each tile is cut into 8
-// contiguous slices, whole multiples of kBlock * M chunks (the last slices
-// short or empty for a short tile), and the blocks of XCD x (x = block mod 8,
-// the grid's x extent being a multiple of 8) stride through slice x, M chunks
-// per lane. Unlike pull_tiled's remap this keeps each XCD's writes in one
-// contiguous slice also when a lane takes two chunks, and spreads a short
-// last tile over all 8 XCDs. Used for bf16 replicas (32 Mixed replicas: 2.07-
-// 2.10 ms vs 2.31 ms) and for vectors of fewer than 8 tiles, where the short
-// tile is a large share (Text-CNN's 7 fp32 replicas: 0.045 vs 0.049 ms). For
-// fp32 replicas of many tiles pull_tiled's 1-D grid measured 2% faster.
-template <int PDT, int E, int M>
+// pull_slices: the same fan-out over 2 Mi-coordinate tiles on a 3-D grid
+// (x: block within the tile, y: replica, z: tile; dispatch order x
+// fastest). Each tile is cut into 8 contiguous slices, whole multiples of
+// kBlock chunks (the last slices short or empty for a short tile), and the
+// blocks of XCD x (x = block mod 8, the grid's x extent being a multiple of
+// 8) stride through slice x. This keeps each XCD's writes in one contiguous
+// slice and spreads a short last tile over all 8 XCDs. Used for bf16
+// replicas (Mixed's 32: 1.98 ms; 2.08 ms with two chunks per lane) and for
+// vectors of fewer than 8 tiles of pull_tiled, where its smaller tiles and
+// short-tile spreading pay (the 17.3M-coordinate shard's 16 fp32 replicas:
+// 0.172 vs 0.185 ms).
+constexpr uint64_t kSliceTileCoords = uint64_t(2) << 20;
+
+template <int PDT, int E>
 __global__ void __launch_bounds__(kBlock) pull_slices(const PullArgs a) {
-    constexpr uint64_t kTileChunksE = tile_coords<PDT>() / E;
-    constexpr uint64_t kSliceUnit = static_cast<uint64_t>(kBlock) * M;
+    constexpr uint64_t kTileChunksE = kSliceTileCoords / E;
     const uint64_t chunks = a.n / E;
     const unsigned b = blockIdx.x;
     const uint64_t t = blockIdx.z;
@@ -504,7 +499,7 @@ __global__ void __launch_bounds__(kBlock) pull_slices(const PullArgs a) {
     const uint64_t c1 = c0 + kTileChunksE < chunks ? c0 + kTileChunksE : chunks;
     uint64_t lo = c0, hi = c1, j = b, nj = gridDim.x;
     if ((gridDim.x & 7u) == 0) {
-        const uint64_t per = (c1 - c0 + 8 * kSliceUnit - 1) / (8 * kSliceUnit) * kSliceUnit;
+        const uint64_t per = (c1 - c0 + 8 * kBlock - 1) / (8 * kBlock) * kBlock;
         const uint64_t x = b & 7u;
         lo = c0 + x * per < c1 ? c0 + x * per : c1;
         hi = lo + per < c1 ? lo + per : c1;
@@ -513,14 +508,10 @@ __global__ void __launch_bounds__(kBlock) pull_slices(const PullArgs a) {
     }
     void *d = a.dst[blockIdx.y];
     const uint64_t step = nj * kBlock;
-    for (uint64_t base = lo + j * kBlock + threadIdx.x; base < hi; base += M * step) {
-        float w[M][E];
-#pragma unroll
-        for (int i = 0; i < M; ++i)
-            if (base + i * step < hi) ld_f32<E, false>(w[i], a.w + (base + i * step) * E);
-#pragma unroll
-        for (int i = 0; i < M; ++i)
-            if (base + i * step < hi) st_dst<PDT, E>(d, (base + i * step) * E, w[i]);
+    for (uint64_t c = lo + j * kBlock + threadIdx.x; c < hi; c += step) {
+        float w[E];
+        ld_f32<E, false>(w, a.w + c * E);
+        st_dst<PDT, E>(d, c * E, w);
     }
     if (t == 0 && b == 0 && threadIdx.x < a.n - chunks * E) {
         const uint64_t i = chunks * E + threadIdx.x;
@@ -648,28 +639,32 @@ hipError_t launch_apply(const ApplyArgs &a, int grad_dtype, int pull_dtype, int 
 
 template <int PDT, int E>
 void go_pull_tiled(const PullArgs &a, const Geometry &geo, hipStream_t s) {
-    // tiles * R * bpt blocks; a tile smaller than a full one needs fewer blocks
-    constexpr uint64_t kTileChunksE = tile_coords<PDT>() / E;
     const uint64_t chunks = a.n / E;
-    const uint64_t tiles = chunks == 0 ? 1 : (chunks + kTileChunksE - 1) / kTileChunksE;
-    const uint64_t per_tile = chunks < kTileChunksE ? chunks : kTileChunksE;
-    uint64_t bpt = (per_tile + lane_chunks<PDT>() * kBlock - 1) / (lane_chunks<PDT>() * kBlock);
-    if (bpt < 1) bpt = 1;
-    if (bpt > kTileBlocks) bpt = kTileBlocks;
-    if (PDT == PS_BF16 || tiles < 8) {
-        // pull_slices: x extent a multiple of 8 once there are more than 8 blocks
-        constexpr uint64_t M = lane_chunks<PDT>();
-        uint64_t bx = (per_tile + M * kBlock - 1) / (M * kBlock);
+    const bool one_d = PDT == PS_F32 && chunks / (kTiledCoords / E) >= 8;
+    if (!one_d) {
+        // tiles * R * bx blocks, the x extent a multiple of 8 once there are
+        // more than 8 blocks per tile
+        constexpr uint64_t kTileChunksE = kSliceTileCoords / E;
+        const uint64_t tiles = chunks == 0 ? 1 : (chunks + kTileChunksE - 1) / kTileChunksE;
+        const uint64_t per_tile = chunks < kTileChunksE ? chunks : kTileChunksE;
+        uint64_t bx = (per_tile + kBlock - 1) / kBlock;
         if (bx < 1) bx = 1;
         if (bx > 8) bx = (bx + 7) / 8 * 8;
         if (tiles <= 65535 && bx * tiles * static_cast<uint64_t>(a.r) <= kMaxBlocks) {
-            hipLaunchKernelGGL((pull_slices<PDT, E, static_cast<int>(M)>),
+            hipLaunchKernelGGL((pull_slices<PDT, E>),
                                dim3(static_cast<unsigned>(bx), static_cast<unsigned>(a.r),
                                     static_cast<unsigned>(tiles)),
                                dim3(kBlock), 0, s, a);
             return;
         }
     }
+    // tiles * R * bpt blocks; a tile smaller than a full one needs fewer blocks
+    constexpr uint64_t kTileChunksE = kTiledCoords / E;
+    const uint64_t tiles = chunks == 0 ? 1 : (chunks + kTileChunksE - 1) / kTileChunksE;
+    const uint64_t per_tile = chunks < kTileChunksE ? chunks : kTileChunksE;
+    uint64_t bpt = (per_tile + kBlock - 1) / kBlock;
+    if (bpt < 1) bpt = 1;
+    if (bpt > kTileBlocks) bpt = kTileBlocks;
     const uint64_t groups = tiles * static_cast<uint64_t>(a.r);
     if (groups * bpt > kMaxBlocks) bpt = kMaxBlocks / groups;   // lanes stride further
     if (bpt < 1) {

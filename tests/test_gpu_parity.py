@@ -297,7 +297,7 @@ def test_misaligned_buffers_scalar_path(torch, og, od):
 
 @pytest.mark.parametrize("r", [2, 3, 16, 64])
 def test_tiled_pull_many_tiles_ragged(torch, r):
-    """The tiled fan-out over two full tiles (4 Mi coordinates each), a
+    """The sliced fan-out over four full tiles (2 Mi coordinates each), a
     partial tile and a ragged tail: every replica equals w (fp32) or RNE(w)
     (bf16)."""
     n = 2 * (4 << 20) + 1234567 + 3
@@ -320,13 +320,12 @@ def test_tiled_pull_many_tiles_ragged(torch, r):
 
 
 @pytest.mark.parametrize("n,r", [
-    (7 * (4 << 20) - 3, 2),      # 7 tiles: the sliced 3-D fan-out for fp32 too
-    (7 * (4 << 20) + 5, 5),      # 8 tiles, the last of one chunk plus a 1-value tail: 1-D fan-out for fp32
-    (9 * (4 << 20) + 4097 * 4 + 2, 3),   # 10 tiles, the last short
+    (7 * (2 << 20) - 3, 2),      # 7 slice tiles, the last short
+    (7 * (2 << 20) + 5, 5),      # 8 slice tiles, the last of one chunk plus a 1-value tail
+    (9 * (2 << 20) + 4097 * 4 + 2, 3),   # 10 slice tiles, the last short
 ])
 def test_pull_paths_every_element(torch, n, r):
-    """Both tiled fan-outs (1-D for fp32 replicas of 8 tiles or more, sliced
-    3-D otherwise and for bf16) write every element of every replica exactly
+    """The sliced 3-D fan-out writes every element of every replica exactly
     as w (fp32) or RNE(w) (bf16): replicas start as a NaN sentinel and are
     compared whole, bitwise, against the oracle's copy."""
     gen = torch.Generator(device="cuda")
@@ -344,6 +343,35 @@ def test_pull_paths_every_element(torch, n, r):
             assert parity.bitwise(parity.np_bits(reps[j]), want), (n, r, dt, j)
         del reps
     srv.close()
+
+
+@pytest.mark.parametrize("n,r", [
+    (8 * (4 << 20) + 5, 5),              # 8 full tiles, a tile of one chunk, a 1-value tail
+    (9 * (4 << 20) + 4097 * 4 + 2, 3),   # 10 tiles, the last short
+])
+def test_one_d_tiled_pull_every_element(torch, n, r):
+    """The 1-D tiled fan-out (fp32 replicas of 8 or more 4 Mi tiles): every
+    element of every replica, NaN sentinels first, equals w bit for bit (an
+    fp32 pull is a copy), compared on the device; bf16 replicas of the same
+    vector (sliced fan-out) equal RNE(w) from the oracle."""
+    say(f"[case] 1-D tiled pull n={n} R={r}")
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(53 + r)
+    w0 = (torch.rand(n, generator=gen, device="cuda") - 0.5) * 0.1
+    srv = ps.ParameterServer(n, 0.01, 0.0, queue_depth=1)
+    srv.set_weights(w0)
+    w_host = parity.np_bits(w0)
+    for dt, tdt in ((ps.PS_F32, torch.float32), (ps.PS_BF16, torch.bfloat16)):
+        want = w_host if dt == ps.PS_F32 else orc.f32_to_bf16(w_host)
+        want = torch.from_numpy(want.view(np.int32 if dt == ps.PS_F32 else np.int16)).to("cuda")
+        reps = [torch.full((n,), float("nan"), dtype=tdt, device="cuda") for _ in range(r)]
+        srv.pull_many(list(range(r)), reps)
+        srv.sync()
+        for j in range(r):
+            assert torch.equal(reps[j].view(torch.int32 if dt == ps.PS_F32 else torch.int16), want), (dt, j)
+        del reps, want
+    srv.close()
+    free(torch)
 
 
 @pytest.mark.parametrize("n", [5, 4096 * 256 + 3, 10_000_019])
