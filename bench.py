@@ -47,7 +47,8 @@ CSRC = os.path.join(ROOT, "paper_1611_06213_amd", "csrc")
 # buffers' placement: recorded counters stay valid only while all are unchanged
 KERNEL_SRC = [os.path.join(CSRC, f) for f in ("ps_kernels.hip", "ps_kernels.h", "ps_server.cpp",
                                               "ps_layout.cpp", "ps_layout.h")]
-COUNTERS = os.path.join(ROOT, "profiles", "traffic_apply_vec_vgg16.txt")
+# counter summaries of the dominant (apply) kernel, one per measured workload and mode
+COUNTERS = os.path.join(ROOT, "profiles", "traffic_apply_vec_*.txt")
 
 
 def algorithmic_bytes(cfg, mode: str, r: int):
@@ -106,22 +107,29 @@ def kernel_source_digest(paths=KERNEL_SRC) -> str:
     return h.hexdigest()
 
 
-def recorded_traffic(kernel_label: str):
-    """HBM bytes per launch from the committed counter summary, or None when
-    it is missing or was taken on different kernel code."""
-    if not os.path.exists(COUNTERS):
-        return None
+def read_summary(path: str) -> dict:
     vals = {}
-    for line in open(COUNTERS):
+    for line in open(path):
         if ":" in line and not line.startswith("#"):
             k, v = line.split(":", 1)
             vals[k.strip()] = v.strip()
-    if vals.get("kernel_code_digest") != kernel_source_digest() or vals.get("mode") != kernel_label:
-        return None
-    try:
-        return float(vals["hbm_bytes_per_launch"])
-    except (KeyError, ValueError):
-        return None
+    return vals
+
+
+def recorded_traffic(kernel_label: str, pattern: str = COUNTERS):
+    """HBM bytes per launch of the apply from the committed counter summary
+    of this workload and mode, or None when there is none or it was taken
+    on different kernel code."""
+    import glob
+    digest = kernel_source_digest()
+    for path in sorted(glob.glob(pattern)):
+        vals = read_summary(path)
+        if vals.get("mode") == kernel_label and vals.get("kernel_code_digest") == digest:
+            try:
+                return float(vals["hbm_bytes_per_launch"])
+            except (KeyError, ValueError):
+                return None
+    return None
 
 
 def cpu_baseline(cfg, pool, w0, pulls_per_step: int, seconds: float, distinct: int = 16):

@@ -68,3 +68,20 @@ def test_algorithmic_bytes_per_step_and_launch():
     assert bench.algorithmic_bytes(cfg, "separate", 0) == (19_923_486_336, 19_923_486_336)
     mixed = wl.CONFIGS["mixed"]
     assert bench.algorithmic_bytes(mixed, "separate", 32)[0] == 29_600_000_000
+
+
+def test_recorded_traffic_matches_mode_and_digest(tmp_path):
+    """Counter bytes are reported for the workload and mode they were taken
+    on, and only while the kernel code digest still matches."""
+    d = bench.kernel_source_digest()
+    (tmp_path / "traffic_apply_vec_a.txt").write_text(
+        f"# header\nmode: vgg16-separate\nkernel_code_digest: {d}\nhbm_bytes_per_launch: 123\n")
+    (tmp_path / "traffic_apply_vec_b.txt").write_text(
+        f"mode: mixed-separate\nkernel_code_digest: {d}\nhbm_bytes_per_launch: 456\n")
+    (tmp_path / "traffic_apply_vec_c.txt").write_text(
+        "mode: alexnet-separate\nkernel_code_digest: 0000\nhbm_bytes_per_launch: 789\n")
+    pat = str(tmp_path / "traffic_apply_vec_*.txt")
+    assert bench.recorded_traffic("vgg16-separate", pat) == 123.0
+    assert bench.recorded_traffic("mixed-separate", pat) == 456.0
+    assert bench.recorded_traffic("alexnet-separate", pat) is None     # other kernel code
+    assert bench.recorded_traffic("vgg16-fused", pat) is None          # not measured
