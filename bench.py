@@ -47,8 +47,8 @@ CSRC = os.path.join(ROOT, "paper_1611_06213_amd", "csrc")
 # buffers' placement: recorded counters stay valid only while all are unchanged
 KERNEL_SRC = [os.path.join(CSRC, f) for f in ("ps_kernels.hip", "ps_kernels.h", "ps_server.cpp",
                                               "ps_layout.cpp", "ps_layout.h")]
-# counter summaries of the dominant (apply) kernel, one per measured workload and mode
-COUNTERS = os.path.join(ROOT, "profiles", "traffic_apply_vec_*.txt")
+# counter summaries, one per measured kernel, workload and mode (the mode line names them)
+COUNTERS = os.path.join(ROOT, "profiles", "traffic_*.txt")
 
 
 def algorithmic_bytes(cfg, mode: str, r: int):
