@@ -36,7 +36,7 @@ gradients (its buffers may have died with it); retire_learner keeps them
 queued, to be applied exactly once in their turn, as the paper's stateless
 server does with gradients already in its shared slots.
 
-Readings where the paper is silent (each also listed in the design notes):
+Readings where the paper is silent:
   * one global FIFO in push-call order stands in for the per-learner queues;
   * a batch of K pending gradients is applied as K sequential steps, each over
     the whole vector, oldest first;
