@@ -246,9 +246,10 @@ int ps_set_queue_mode(ps_server *ps, int mode, int slots_per_learner);
  * either way; only the order in which the grid visits coordinates changes. */
 int ps_set_fronts(ps_server *ps, int fronts_log2);
 
-/* Override the launch shape of the apply and synchronous-step kernels, which
- * is otherwise chosen per call from the number of gradients, momentum and the
- * gradient type (tables measured at the VGG-16 and Mixed sizes):
+/* Override the launch shape of the apply (Eq. "asgd") and synchronous-step
+ * (Eq. "ssgd") kernels, which is otherwise chosen per call from the number of
+ * gradients, momentum and the gradient type (tables measured at the VGG-16
+ * and Mixed sizes):
  * blocks_per_cu 1..4 caps the resident 256-thread blocks per compute unit, 0
  * lifts the cap, -1 restores the library's choice; group 4, 8, 12 or 16 sets
  * how many gradients' loads are issued together, 0 restores the library's
