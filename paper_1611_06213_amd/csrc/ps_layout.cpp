@@ -103,4 +103,6 @@ ApplyShape sync_shape(int k, bool momentum, bool bf16) {
     return {1, 0, 16};
 }
 
+bool fuse_replicas(int r, int k) { return r <= 1 || (r <= 4 && k <= 16); }
+
 }  // namespace gadei

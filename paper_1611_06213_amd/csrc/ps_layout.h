@@ -83,4 +83,16 @@ ApplyShape apply_shape(int k, bool momentum, bool bf16);
 // fronts choice beyond the phase rule: fronts_log2 is 0).
 ApplyShape sync_shape(int k, bool momentum, bool bf16);
 
+// Whether ps_apply_pull writes its r replicas from the apply pass over k
+// gradients (else the apply is followed by the tiled fan-out): one replica
+// always; up to 4 when at most 16 gradients are folded. Writing replicas from
+// the apply adds write streams to its read streams, which costs more than a
+// separate fan-out once there are many of either; for few of both it saves
+// the fan-out's launch and its second read of w. Measured from server rows
+// (apply+pull time, fused vs separate): k = 8, r = 2: 10M coordinates
+// 0.079 vs 0.086 ms, 138M 1.07 vs 1.10 ms; k = 16, r = 2: 138M 1.89-1.90 vs
+// 1.93-1.94 ms; k = 16, r = 8: 138M 2.47 vs 2.42-2.43 ms; k = 32, r = 2:
+// 61M 1.55 vs 1.51 ms.
+bool fuse_replicas(int r, int k);
+
 }  // namespace gadei

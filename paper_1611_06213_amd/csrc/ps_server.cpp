@@ -55,7 +55,9 @@ struct ps_server {
     // recorded on pull_stream so that ps_apply_pull's replica writes follow
     // earlier lock-free pulls into the same buffers
     hipEvent_t pulls_done = nullptr;
-    int fuse_max_r = 1;   // ps_apply_pull writes up to this many replicas in the apply pass
+    // ps_apply_pull writes up to this many replicas in the apply pass; -1:
+    // chosen per call (fuse_replicas)
+    int fuse_max_r = -1;
     // ps_set_launch_shape: -1 / 0 = the shape tables' choice
     int force_blocks_per_cu = -1;
     int force_group = 0;
@@ -564,7 +566,10 @@ int ps_apply_pull(ps_server *ps, int n, const int *learner_ids, void *const *dst
     if (int rc = use_device(ps)) return rc;
     if (!write.empty())
         if (int rc = order_after_pulls(ps)) return rc;
-    if (static_cast<int>(write.size()) <= ps->fuse_max_r) {
+    const int r = static_cast<int>(write.size());
+    const bool fuse = ps->fuse_max_r >= 0 ? r <= ps->fuse_max_r
+                                           : gadei::fuse_replicas(r, static_cast<int>(b.items.size()));
+    if (fuse) {
         if (int rc = launch_batch(ps, b.items, dst_dtype, dsts, write)) return rc;
     } else {
         static const std::vector<int> none;
@@ -757,8 +762,8 @@ int ps_set_queue_mode(ps_server *ps, int mode, int slots_per_learner) {
 int ps_set_pull_fusion(ps_server *ps, int max_replicas) {
     if (int rc = check(ps)) return rc;
     PS_LOCK(ps);
-    if (max_replicas < 0 || max_replicas > PS_MAX_REPLICAS)
-        return fail(PS_EINVAL, "fusion limit %d outside [0, %d]", max_replicas, PS_MAX_REPLICAS);
+    if (max_replicas < -1 || max_replicas > PS_MAX_REPLICAS)
+        return fail(PS_EINVAL, "fusion limit %d outside [-1, %d]", max_replicas, PS_MAX_REPLICAS);
     ps->fuse_max_r = max_replicas;
     return PS_OK;
 }

@@ -15,6 +15,7 @@
 //   rows B C              row layout of C rows of B bytes: head stride span
 //   shape K M B           launch shape of a K-gradient apply (M = 1: momentum; B = 1: bf16)
 //   sync_shape K M B      the same for a synchronous step over K learners
+//   fuse R K              1 if ps_apply_pull writes R replicas from the apply of K gradients
 #include <cstdio>
 #include <iostream>
 #include <sstream>
@@ -156,6 +157,10 @@ int main() {
             const gadei::RowLayout r = gadei::row_layout(bytes, static_cast<int>(count));
             std::printf("rows %zu %zu %zu %zu", r.head, r.stride, r.span,
                         gadei::velocity_offset(bytes));
+        } else if (cmd == "fuse") {
+            long r, k;
+            in >> r >> k;
+            std::printf("fuse %d", gadei::fuse_replicas(static_cast<int>(r), static_cast<int>(k)) ? 1 : 0);
         } else if (cmd == "shape" || cmd == "sync_shape") {
             long k, m, b = 0;
             in >> k >> m >> b;

@@ -45,14 +45,15 @@ def free(torch):
 SMALL_N = 3 * 65536 + 7   # several 256-lane tiles and a ragged tail
 
 
-@pytest.mark.parametrize("fused,fusion", [(False, None), (True, None), (True, 64)],
-                         ids=["separate", "fused", "fused-one-pass"])
+@pytest.mark.parametrize("fused,fusion", [(False, None), (True, None), (True, 0), (True, 64)],
+                         ids=["separate", "fused", "fused-never-one-pass", "fused-one-pass"])
 @pytest.mark.parametrize("name", list(wl.CONFIGS))
 def test_workload_small_full_oracle(torch, name, fused, fusion):
     """Each workload's whole schedule at a reduced parameter count; the
-    oracle covers every coordinate. "fused-one-pass" writes every replica
-    from the apply pass; "fused" uses the default (tiled fan-out after the
-    apply for more than one replica)."""
+    oracle covers every coordinate. "fused" takes ps_apply_pull's per-call
+    choice (replicas from the apply pass for one, or up to 4 with at most 16
+    gradients; else the tiled fan-out after it); "fused-never-one-pass"
+    always the fan-out; "fused-one-pass" every replica from the apply pass."""
     cfg = wl.CONFIGS[name].scaled(SMALL_N, pool=min(wl.CONFIGS[name].pool, 64))
     say(f"[small] {name} n={cfg.n} fused={fused} fusion={fusion}")
     ev = wl.schedule(cfg)

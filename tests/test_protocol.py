@@ -271,6 +271,16 @@ def test_apply_shape_table(driver):
             assert 0 <= b <= 4 and f in (0, 1) and g in (4, 8, 12, 16)
 
 
+def test_replica_fusion_rule(driver):
+    """ps_apply_pull writes one replica from the apply pass always, up to 4
+    when the apply folds at most 16 gradients, and otherwise leaves the
+    replicas to the tiled fan-out (the measured rule)."""
+    cases = {(1, 1): 1, (1, 64): 1, (2, 8): 1, (4, 16): 1, (5, 8): 0, (2, 17): 0, (4, 32): 0,
+             (8, 8): 0, (0, 32): 1}
+    got = run_driver(driver, [f"fuse {r} {k}" for (r, k) in cases])
+    assert got == [f"fuse {v}" for v in cases.values()]
+
+
 # (K, momentum, bf16) -> (blocks per CU, fronts log2, group)
 SHAPES = {
     (1, 1, 0): (4, 0, 16), (2, 1, 0): (3, 0, 4), (4, 1, 0): (2, 0, 4), (8, 1, 0): (2, 0, 4),
