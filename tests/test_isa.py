@@ -1,0 +1,87 @@
+"""The gfx950 code of the kernels, compiled here with the library's own flags
+(no GPU needed): properties the parity and speed of the path rest on.
+
+* The apply and pull kernels contain no packed-fp32 and no fused
+  multiply-add instructions: every product and sum is rounded on its own
+  (the binary32 reading of Eq. "gd"), and packed fp32 stays disabled.
+* No kernel uses private (scratch) memory: registers hold every value.
+* The fused applies of the VGG-16 shape (fp32 gradients, groups of 16) and
+  of the Mixed shape (bf16 gradients, groups of 16) issue each group's 16
+  gradient loads back to back, non-temporal, before waiting for the first:
+  the loads a lane keeps in flight set the apply's bandwidth.
+"""
+import os
+import re
+import shutil
+import subprocess
+
+import pytest
+
+from paper_1611_06213_amd import build as B
+
+KERNELS = os.path.join(B.CSRC, "ps_kernels.hip")
+VGG16_APPLY = "_ZN5gadei12_GLOBAL__N_19apply_vecILb1ELi0ELin1ELi4ELi16EEEvNS_9ApplyArgsE"
+MIXED_APPLY = "_ZN5gadei12_GLOBAL__N_19apply_vecILb1ELi1ELin1ELi8ELi16EEEvNS_9ApplyArgsE"
+
+
+@pytest.fixture(scope="module")
+def asm(tmp_path_factory):
+    if not os.path.exists(B.HIPCC) and shutil.which("hipcc") is None:
+        pytest.skip("hipcc not available")
+    out = str(tmp_path_factory.mktemp("isa") / "ps_kernels.s")
+    flags = [f for f in B.FLAGS if f not in ("-fPIC", "-shared")]
+    r = subprocess.run([B.HIPCC, *flags, "--cuda-device-only", "-S", KERNELS, "-o", out],
+                       capture_output=True, text=True, timeout=600)
+    assert r.returncode == 0, r.stderr[-2000:]
+    with open(out) as f:
+        return f.read()
+
+
+def kernels(asm):
+    """name -> (instruction lines of the kernel body, metadata block)."""
+    names = re.findall(r"^\s*\.amdhsa_kernel (\S+)$", asm, re.M)
+    out = {}
+    for name in names:
+        start = asm.index("\n" + name + ":")
+        end = asm.index(".Lfunc_end", start)
+        body = [l.split(";")[0].strip() for l in asm[start:end].splitlines()[1:]]
+        meta_start = asm.index(".amdhsa_kernel " + name)
+        meta = asm[meta_start:asm.index(".end_amdhsa_kernel", meta_start)]
+        out[name] = ([l for l in body if l and not l.startswith(".")], meta)
+    return out
+
+
+def test_no_fused_or_packed_fp32_in_apply_and_pull(asm):
+    ks = kernels(asm)
+    checked = 0
+    for name, (body, _) in ks.items():
+        if not re.search(r"apply_vec|apply_scalar|pull_", name):
+            continue
+        checked += 1
+        bad = [l for l in body if re.match(r"v_(pk_\w+|fma\w*|mac\w*|fmac\w*)\b", l)]
+        assert not bad, (name, bad[:3])
+    assert checked >= 60
+
+
+def test_no_kernel_uses_scratch(asm):
+    ks = kernels(asm)
+    assert len(ks) >= 90
+    for name, (_, meta) in ks.items():
+        m = re.search(r"\.amdhsa_private_segment_fixed_size (\d+)", meta)
+        assert m and int(m.group(1)) == 0, name
+
+
+@pytest.mark.parametrize("name", [VGG16_APPLY, MIXED_APPLY], ids=["vgg16-fp32", "mixed-bf16"])
+def test_group_loads_issued_together(asm, name):
+    body, _ = kernels(asm)[name]
+    runs, run = [], 0
+    for l in body:
+        if l.startswith("global_load_dwordx4"):
+            assert re.search(r"\bnt\b", l), l
+            run += 1
+        elif l.startswith("s_waitcnt") and "vmcnt" in l:
+            runs.append(run)
+            run = 0
+    runs.append(run)
+    # the first group (after the 2 or 4 w/v loads) and the loop's groups
+    assert sum(1 for r in runs if r >= 16) >= 2, runs
