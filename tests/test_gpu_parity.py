@@ -1643,8 +1643,8 @@ def test_buffers_overlapping_w_or_v_are_refused(torch):
 
 
 def test_alloc_rows_argument_errors(torch):
-    """ps_alloc_rows / ps_free_rows / ps_set_fronts refuse bad arguments with
-    PS_EINVAL and change nothing."""
+    """ps_alloc_rows / ps_free_rows / ps_set_fronts / ps_set_pull_fusion
+    refuse bad arguments with PS_EINVAL and change nothing."""
     srv = ps.ParameterServer(1000, 0.01, 0.0)
     assert ps.ps_alloc_rows(srv.h, 0, ps.PS_F32)[0] == ps.PS_EINVAL
     assert ps.ps_alloc_rows(srv.h, ps.PS_MAX_ROWS + 1, ps.PS_F32)[0] == ps.PS_EINVAL
@@ -1652,6 +1652,9 @@ def test_alloc_rows_argument_errors(torch):
     assert ps.load_library().ps_alloc_rows(srv.h, 2, ps.PS_F32, None) == ps.PS_EINVAL
     assert ps.ps_free_rows(srv.h, 0) == ps.PS_EINVAL
     assert ps.ps_set_fronts(srv.h, -2) == ps.PS_EINVAL and ps.ps_set_fronts(srv.h, 4) == ps.PS_EINVAL
+    assert ps.ps_set_pull_fusion(srv.h, -2) == ps.PS_EINVAL
+    assert ps.ps_set_pull_fusion(srv.h, ps.PS_MAX_REPLICAS + 1) == ps.PS_EINVAL
+    assert ps.ps_set_pull_fusion(srv.h, -1) == ps.PS_OK and ps.ps_set_pull_fusion(srv.h, 0) == ps.PS_OK
     rc, rows = ps.ps_alloc_rows(srv.h, ps.PS_MAX_ROWS, ps.PS_BF16)   # 4096 rows of 1000 values
     assert rc == ps.PS_OK and len(set(rows)) == ps.PS_MAX_ROWS
     assert ps.ps_free_rows(srv.h, rows[1]) == ps.PS_EINVAL           # not a first row

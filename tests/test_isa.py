@@ -8,7 +8,9 @@
 * The fused applies of the VGG-16 shape (fp32 gradients, groups of 16) and
   of the Mixed shape (bf16 gradients, groups of 16) issue each group's 16
   gradient loads back to back, non-temporal, before waiting for the first:
-  the loads a lane keeps in flight set the apply's bandwidth.
+  the loads a lane keeps in flight set the apply's bandwidth. The remainder
+  after the full groups is one straight-line group too (7 loads together for
+  a remainder of 7), not one load and one wait per gradient.
 """
 import os
 import re
@@ -85,3 +87,6 @@ def test_group_loads_issued_together(asm, name):
     runs.append(run)
     # the first group (after the 2 or 4 w/v loads) and the loop's groups
     assert sum(1 for r in runs if r >= 16) >= 2, runs
+    # remainder groups of 1..7 loads, each issued whole
+    for size in range(2, 8):
+        assert size in runs, (size, runs)
