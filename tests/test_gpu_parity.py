@@ -1481,8 +1481,9 @@ def test_every_group_and_remainder(torch, gdt, m):
     so that the first group, the loop over further groups, the group of 8 and
     each exact remainder of 1..7 all run, under residency caps 0..4 in turn:
     w and v equal the oracle's bits after the same gradients (batched is
-    sequential, so one oracle run gives every depth). The synchronous step
-    at every group size and depth too."""
+    sequential, so one oracle run gives every depth); the same applies writing
+    two fp32 or bf16 replicas from their own pass give those bits and RNE of
+    them; the synchronous step at every group size and depth too."""
     n, lr, kmax = 3 * 8192 + 5, 0.01, 40
     say(f"[case] groups x remainders gradients={gdt} m={m} n={n}")
     tdt = torch.bfloat16 if gdt == "bf16" else torch.float32
@@ -1518,6 +1519,19 @@ def test_every_group_and_remainder(torch, gdt, m):
             assert parity.bitwise(parity.np_bits(srv.weights_copy()), ww), (group, k)
             if m != 0:
                 assert parity.bitwise(parity.np_bits(srv.velocity_copy()), wv), (group, k)
+            # the same apply writing two replicas from its own pass
+            rdt = torch.float32 if case % 2 else torch.bfloat16
+            reps = [torch.full((n,), float("nan"), dtype=rdt, device="cuda") for _ in range(2)]
+            srv.set_pull_fusion(64)
+            srv.set_weights(w0)
+            for j in range(k):
+                assert srv.push(j % 7, grads[j])
+            srv.apply_pull([0, 1], reps)
+            srv.set_pull_fusion(-1)
+            assert parity.bitwise(parity.np_bits(srv.weights_copy()), ww), ("fused", group, k)
+            rw = ww.view(np.float32) if rdt == torch.float32 else orc.f32_to_bf16(ww.view(np.float32))
+            for rep in reps:
+                assert parity.bitwise(parity.np_bits(rep), rw), ("replica", group, k, rdt)
             srv.set_weights(w0)
             for j in range(k):
                 assert srv.push(j, grads[j])
