@@ -14,7 +14,11 @@ Timing. After W warm-up steps, `runs` (default 5) timed runs of exactly K
 steps each, w and v reset to w0 and 0 before every run (ps_set_weights);
 each run is one ps_run call (the library's native executor walks the
 prepared schedule of pushes, applies and pulls), bracketed by device
-synchronisation, and `value` is the median run's pushes/s. One more run
+synchronisation, and `value` is the median run's pushes/s. The same runs are
+timed again replaying the schedule captured once as a HIP graph
+(ps_graph_create / ps_graph_launch: the host protocol still runs per call,
+the kernels go out as one graph); with --graph `value` is the median of
+those (launch-bound workloads gain, HBM-bound ones do not). One more run
 drives the same calls one by one from Python (`python_driven_pushes_per_s`),
 and a last one records HIP events around every kernel on the stream it runs
 on, for the per-kernel durations behind `roofline` (events between kernels
@@ -336,6 +340,10 @@ def main():
     ap.add_argument("--runs", type=int, default=5,
                     help="timed runs of --steps steps each, w and v reset before each; "
                          "value is the median run")
+    ap.add_argument("--graph", action="store_true",
+                    help="value from runs that replay the prepared steps captured once as a HIP "
+                         "graph (ps_graph_launch) instead of one ps_run call; both rates are "
+                         "reported either way")
     ap.add_argument("--config", default="vgg16")
     ap.add_argument("--mode", choices=["fused", "separate", "hogwild"], default="separate",
                     help="separate: ps_apply_pending + ps_pull_many (one kernel each, timed "
@@ -380,7 +388,10 @@ def main():
         # one gradient per learner per step; every learner pulls after it
         cfg = wl.dataclasses.replace(cfg, depth=cfg.learners)
     n, K, R = cfg.n, cfg.depth, cfg.replicas
-    stream = torch.cuda.current_stream()
+    # a stream of its own (default priority), current for torch's work too:
+    # the legacy null stream cannot be captured into a graph
+    stream = torch.cuda.Stream()
+    torch.cuda.set_stream(stream)
 
     h = ps.ps_create(n, cfg.lr, cfg.momentum)
     if not h:
@@ -501,7 +512,40 @@ def main():
         if rc != 0 or done != len(timed):
             raise RuntimeError(f"ps_run stopped at call {done}: {ps.ps_last_error()}")
         run_s.append(t1 - t0)
-    elapsed = sorted(run_s)[len(run_s) // 2]
+
+    # the same steps as HIP graph replays (ordered pulls only): one cycle of
+    # the plan captured once and enqueued back to back (the host plans replay
+    # i + 1 while the device runs replay i), the steps left over as a second
+    # graph
+    graph_s = []
+    if pstream is None:
+        cycle = len(calls)
+        q, rem = divmod(args.steps, cycle)
+        graphs = []
+        for steps_, count in ((cycle, q), (rem, 1 if rem else 0)):
+            if count == 0:
+                continue
+            reset()
+            rc, g_ = ps.ps_graph_create(h, script(steps_))
+            if rc != 0:
+                raise RuntimeError(f"ps_graph_create: {ps.ps_last_error()}")
+            graphs.append((g_, count))
+        for _ in range(args.runs):
+            reset()
+            t0 = time.perf_counter()
+            for g_, count in graphs:
+                for _ in range(count):
+                    if ps.ps_graph_launch(h, g_) != 0:
+                        raise RuntimeError(f"ps_graph_launch: {ps.ps_last_error()}")
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+            graph_s.append(t1 - t0)
+        for g_, _ in graphs:
+            ps.ps_graph_destroy(g_)
+    elif args.graph:
+        raise SystemExit("--graph needs ordered pulls (not --mode hogwild)")
+    value_s = graph_s if args.graph else run_s
+    elapsed = sorted(value_s)[len(value_s) // 2]
 
     # the same steps driven call by call from Python
     reset()
@@ -566,9 +610,15 @@ def main():
         "ms_per_step": round(elapsed / args.steps * 1e3, 4),
         "timing": {
             "runs": args.runs,
-            "pushes_per_s_each_run": [round(pushes / t, 2) for t in run_s],
-            "value_is": "median run; each run one ps_run call over the prepared steps, after "
-                        "ps_set_weights(w0) reset w, v and the timestamp",
+            "pushes_per_s_each_run": [round(pushes / t, 2) for t in value_s],
+            "value_is": ("median run; each run " + ("the prepared steps as HIP graph replays "
+                         "(one cycle of the plan captured once, replayed back to back with "
+                         "ps_graph_launch)" if args.graph else "one ps_run call over the "
+                         "prepared steps") + ", after ps_set_weights(w0) reset w, v and the "
+                         "timestamp"),
+            "ps_run_pushes_per_s": round(pushes / sorted(run_s)[len(run_s) // 2], 2),
+            "graph_pushes_per_s": (round(pushes / sorted(graph_s)[len(graph_s) // 2], 2)
+                                   if graph_s else None),
             "python_driven_pushes_per_s": round(pushes / py_elapsed, 2),
         },
         "higher_is_better": True,

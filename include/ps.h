@@ -400,6 +400,37 @@ typedef struct ps_op {
  * PS_EINVAL for an unknown kind or ops == NULL with count > 0. */
 int ps_run(ps_server *ps, const ps_op *ops, int count, int *done);
 
+/* A script captured once as a HIP graph and replayed, for launch-bound
+ * loops (small vectors, one gradient per apply): a replay enqueues all of
+ * the script's kernels at once, without a launch per kernel.
+ *
+ * ps_graph_create: the script's calls are made as by ps_run, but their
+ * kernels are captured into a graph on the server's stream instead of
+ * running, and the server's host state is left as it was: nothing has run.
+ * The script is copied; its gradient and replica buffers must stay valid
+ * while the graph lives.
+ *
+ * ps_graph_launch: the calls again, planned and committed on the host as
+ * by ps_run (timestamps, staleness, pull history, statistics), and the graph
+ * enqueued on the server's stream, ordered with every other call. The
+ * result is identical to ps_run of the same script. Every launch checks that
+ * the calls would now launch exactly the captured kernels (same buffers,
+ * gradients per apply, replicas written, launch shapes); if not -- say a
+ * pull that was written at capture would now be skipped -- it returns
+ * PS_ESTATE and changes nothing. A call of the script that fails returns
+ * its status and changes nothing either.
+ *
+ * Both need a server stream other than the legacy null stream
+ * (ps_set_stream), ordered pulls (no ps_set_pull_stream) and an empty queue
+ * (PS_ESTATE otherwise); scripts start from an empty queue. PS_EINVAL for a
+ * bad script, a script that launches nothing, or a graph of another
+ * server. Destroy graphs before their server; a graph is launched only on
+ * the server it was created for. */
+typedef struct ps_graph ps_graph;
+int ps_graph_create(ps_server *ps, const ps_op *ops, int count, ps_graph **graph);
+int ps_graph_launch(ps_server *ps, ps_graph *graph);
+void ps_graph_destroy(ps_graph *graph);
+
 /* Block until all work enqueued by the server has completed. */
 int ps_sync(ps_server *ps);
 

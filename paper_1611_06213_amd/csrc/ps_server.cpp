@@ -40,6 +40,21 @@ struct RowSet {
 
 }  // namespace
 
+// One kernel launch of a call, with every argument it was given: the plan
+// that a captured graph (ps_graph_create) replays. Zero-filled before use,
+// so two records compare equal byte for byte exactly when the launches are
+// the same.
+struct LaunchRecord {
+    int kind;   // 0 apply, 1 synchronous step, 2 pull fan-out
+    int grad_dtype;
+    int pull_dtype;
+    int level;
+    int blocks_per_cu;
+    int group;
+    gadei::ApplyArgs apply;
+    gadei::PullArgs pull;
+};
+
 struct ps_server {
     size_t n = 0;
     float lr = 0.0f;
@@ -63,6 +78,10 @@ struct ps_server {
     int force_group = 0;
     gadei::Geometry geo;
     gadei::Protocol proto;
+    // ps_graph_create / ps_graph_launch: the launches of the calls in
+    // progress are recorded here; with plan_only they are not made
+    std::vector<LaunchRecord> *record = nullptr;
+    bool plan_only = false;
     // Every call on the handle holds this lock, so several host threads (a
     // push thread per learner, as in Sec. 4.1) may share one server; device
     // work is enqueued in lock order. Recursive: some calls use others.
@@ -172,6 +191,40 @@ gadei::Shape shape_for(const ps_server *ps, const gadei::ApplyShape &t) {
     return shape;
 }
 
+// The three kernel launches of the calls, through the recorder.
+hipError_t run_apply(ps_server *ps, const gadei::ApplyArgs &a, int gdt, int pdt, int level,
+                     const gadei::Shape &shape, bool sync) {
+    if (ps->record) {
+        LaunchRecord r;
+        std::memset(&r, 0, sizeof r);
+        r.kind = sync ? 1 : 0;
+        r.grad_dtype = gdt;
+        r.pull_dtype = pdt;
+        r.level = level;
+        r.blocks_per_cu = shape.blocks_per_cu;
+        r.group = shape.group;
+        r.apply = a;
+        ps->record->push_back(r);
+    }
+    if (ps->plan_only) return hipSuccess;
+    return sync ? gadei::launch_sync(a, gdt, level, shape, ps->geo, ps->stream)
+                : gadei::launch_apply(a, gdt, pdt, level, shape, ps->geo, ps->stream);
+}
+
+hipError_t run_pull(ps_server *ps, const gadei::PullArgs &a, int dtype, int level, hipStream_t s) {
+    if (ps->record) {
+        LaunchRecord r;
+        std::memset(&r, 0, sizeof r);
+        r.kind = 2;
+        r.pull_dtype = dtype;
+        r.level = level;
+        r.pull = a;
+        ps->record->push_back(r);
+    }
+    if (ps->plan_only) return hipSuccess;
+    return gadei::launch_pull(a, dtype, level, ps->geo, s);
+}
+
 // Launch a batch as runs of equal gradient dtype, in order. The last run
 // also writes the replicas listed in `write` when pull_dtype >= 0.
 int launch_batch(ps_server *ps, const std::vector<PushDesc> &items, int pull_dtype,
@@ -209,7 +262,7 @@ int launch_batch(ps_server *ps, const std::vector<PushDesc> &items, int pull_dty
                 level = std::min(level, level_of(a.dst[j], pull_dtype));
             }
         }
-        hipError_t e = gadei::launch_apply(a, gdt, pdt, level, shape, ps->geo, ps->stream);
+        hipError_t e = run_apply(ps, a, gdt, pdt, level, shape, false);
         if (e != hipSuccess) return fail_hip(e, "apply kernel launch");
         start = end;
     }
@@ -244,7 +297,7 @@ int launch_pulls(ps_server *ps, void *const *dsts, int dtype, const std::vector<
         a.dst[j] = dsts[write[j]];
         level = std::min(level, level_of(a.dst[j], dtype));
     }
-    hipError_t e = gadei::launch_pull(a, dtype, level, ps->geo, s);
+    hipError_t e = run_pull(ps, a, dtype, level, s);
     if (e != hipSuccess) return fail_hip(e, "pull kernel launch");
     return PS_OK;
 }
@@ -314,6 +367,61 @@ struct Import {
 };
 std::mutex g_import_mu;
 std::map<void *, Import> g_imports;
+
+}  // namespace
+
+// A captured script: its device work as one HIP graph, the launches it was
+// captured from, and its own copy of the script (ids and buffer lists).
+struct ps_graph {
+    ps_server *server = nullptr;
+    hipGraph_t graph = nullptr;
+    hipGraphExec_t exec = nullptr;
+    std::vector<ps_op> ops;
+    std::vector<std::vector<int>> ids;
+    std::vector<std::vector<void *>> dsts;
+    std::vector<LaunchRecord> plan;
+};
+
+namespace {
+
+// What a script needs of the server to be captured or replayed: a stream
+// other than the legacy null stream (which cannot be captured), ordered
+// pulls only (lock-free pulls run on a second stream), and an empty queue
+// (so that the script's applies take only its own pushes).
+int graph_state(const ps_server *ps) {
+    if (ps->stream == nullptr)
+        return fail(PS_ESTATE, "graphs need a server stream other than the null stream");
+    if (ps->pull_lock_free) return fail(PS_ESTATE, "graphs need ordered pulls");
+    if (ps->proto.pending() != 0) return fail(PS_ESTATE, "gradients pending");
+    return PS_OK;
+}
+
+// The script's calls made for real or, with plan_only, planned and
+// committed on the host without launching; the launches land in *rec.
+int run_recorded(ps_server *ps, const ps_graph &g, std::vector<LaunchRecord> &rec, bool plan_only) {
+    ps->record = &rec;
+    ps->plan_only = plan_only;
+    int rc;
+    try {
+        rc = ps_run(ps, g.ops.data(), static_cast<int>(g.ops.size()), nullptr);
+    } catch (...) {
+        rc = fail(PS_ENOMEM, "host allocation failed");
+    }
+    ps->record = nullptr;
+    ps->plan_only = false;
+    return rc;
+}
+
+bool same_plan(const std::vector<LaunchRecord> &a, const std::vector<LaunchRecord> &b) {
+    return a.size() == b.size() &&
+           (a.empty() || std::memcmp(a.data(), b.data(), a.size() * sizeof(LaunchRecord)) == 0);
+}
+
+void free_graph(ps_graph *g) {
+    if (g->exec) (void)hipGraphExecDestroy(g->exec);
+    if (g->graph) (void)hipGraphDestroy(g->graph);
+    delete g;
+}
 
 }  // namespace
 
@@ -523,7 +631,7 @@ int ps_apply_sync(ps_server *ps) {
     }
     a.fronts_log2 = fronts_for(ps, a, -1);   // the phase rule only (no apply_shape)
     const gadei::Shape shape = shape_for(ps, gadei::sync_shape(a.k, a.v != nullptr, gdt == PS_BF16));
-    hipError_t e = gadei::launch_sync(a, gdt, level, shape, ps->geo, ps->stream);
+    hipError_t e = run_apply(ps, a, gdt, -1, level, shape, true);
     if (e != hipSuccess) return fail_hip(e, "synchronous step launch");
     ps->proto.commit_sync(b);
     return PS_OK;
@@ -871,6 +979,89 @@ int ps_run(ps_server *ps, const ps_op *ops, int count, int *done) {
         if (done) *done = i + 1;
     }
     return PS_OK;
+}
+
+int ps_graph_create(ps_server *ps, const ps_op *ops, int count, ps_graph **out) {
+    if (out) *out = nullptr;
+    if (int rc = check(ps)) return rc;
+    if (out == nullptr || count < 1 || ops == nullptr) return fail(PS_EINVAL, "bad graph script");
+    PS_LOCK(ps);
+    if (int rc = graph_state(ps)) return rc;
+    if (int rc = use_device(ps)) return rc;
+    ps_graph *g = nullptr;
+    try {
+        g = new ps_graph;
+        g->server = ps;
+        g->ops.assign(ops, ops + count);
+        g->ids.resize(count);
+        g->dsts.resize(count);
+        for (int i = 0; i < count; ++i) {
+            ps_op &o = g->ops[i];
+            if (o.kind == PS_OP_PULL || o.kind == PS_OP_APPLY_PULL) {
+                if (o.count < 0 || o.count > PS_MAX_REPLICAS ||
+                    (o.count > 0 && (o.learner_ids == nullptr || o.dsts == nullptr))) {
+                    free_graph(g);
+                    return fail(PS_EINVAL, "op %d: bad pull list", i);
+                }
+                g->ids[i].assign(o.learner_ids, o.learner_ids + o.count);
+                g->dsts[i].assign(o.dsts, o.dsts + o.count);
+                o.learner_ids = g->ids[i].data();
+                o.dsts = g->dsts[i].data();
+            }
+        }
+    } catch (...) {
+        if (g) free_graph(g);
+        return fail(PS_ENOMEM, "host allocation failed");
+    }
+    // Capture: the calls run as usual, their kernels go into the graph
+    // instead of running, and the server's host state is put back, since
+    // nothing has run yet.
+    const gadei::Protocol saved = ps->proto;
+    hipError_t e = hipStreamBeginCapture(ps->stream, hipStreamCaptureModeThreadLocal);
+    if (e != hipSuccess) {
+        free_graph(g);
+        return fail_hip(e, "hipStreamBeginCapture");
+    }
+    int rc = run_recorded(ps, *g, g->plan, false);
+    e = hipStreamEndCapture(ps->stream, &g->graph);
+    ps->proto = saved;
+    if (rc == PS_OK && e != hipSuccess) rc = fail_hip(e, "hipStreamEndCapture");
+    if (rc == PS_OK && g->plan.empty()) rc = fail(PS_EINVAL, "the script launches no kernel");
+    if (rc == PS_OK) {
+        e = hipGraphInstantiate(&g->exec, g->graph, nullptr, nullptr, 0);
+        if (e != hipSuccess) rc = fail_hip(e, "hipGraphInstantiate");
+    }
+    if (rc != PS_OK) {
+        free_graph(g);
+        return rc;
+    }
+    *out = g;
+    return PS_OK;
+}
+
+int ps_graph_launch(ps_server *ps, ps_graph *g) {
+    if (int rc = check(ps)) return rc;
+    if (g == nullptr || g->server != ps) return fail(PS_EINVAL, "not a graph of this server");
+    PS_LOCK(ps);
+    if (int rc = graph_state(ps)) return rc;
+    if (int rc = use_device(ps)) return rc;
+    // The calls again, planned and committed on the host only: the replay
+    // is valid if they would launch exactly the captured kernels.
+    const gadei::Protocol saved = ps->proto;
+    std::vector<LaunchRecord> now;
+    int rc = run_recorded(ps, *g, now, true);
+    if (rc == PS_OK && !same_plan(now, g->plan))
+        rc = fail(PS_ESTATE, "the script would now launch other kernels than were captured");
+    if (rc == PS_OK) {
+        const hipError_t e = hipGraphLaunch(g->exec, ps->stream);
+        if (e != hipSuccess) rc = fail_hip(e, "hipGraphLaunch");
+    }
+    if (rc != PS_OK) ps->proto = saved;
+    return rc;
+}
+
+void ps_graph_destroy(ps_graph *g) {
+    if (g != nullptr) free_graph(g);
 }
 
 int ps_sync(ps_server *ps) {

@@ -107,6 +107,10 @@ _SIGS = {
     "ps_sync": (ctypes.c_int, [_VP]),
     "ps_run": (ctypes.c_int, [_VP, ctypes.POINTER(ps_op), ctypes.c_int,
                               ctypes.POINTER(ctypes.c_int)]),
+    "ps_graph_create": (ctypes.c_int, [_VP, ctypes.POINTER(ps_op), ctypes.c_int,
+                                       ctypes.POINTER(_VP)]),
+    "ps_graph_launch": (ctypes.c_int, [_VP, _VP]),
+    "ps_graph_destroy": (None, [_VP]),
     "ps_get_stats": (ctypes.c_int, [_VP, ctypes.POINTER(ps_stats)]),
     "ps_alloc_rows": (ctypes.c_int, [_VP, ctypes.c_int, ctypes.c_int, ctypes.POINTER(_VP)]),
     "ps_free_rows": (ctypes.c_int, [_VP, _VP]),
@@ -364,6 +368,25 @@ def ps_run(h: int, script: "OpScript"):
     done = ctypes.c_int()
     rc = load_library().ps_run(h, script.array, len(script), ctypes.byref(done))
     return rc, done.value
+
+
+def ps_graph_create(h: int, script: "OpScript"):
+    """(status, graph handle): the script captured as a HIP graph (nothing
+    runs; ps_graph_launch replays it). The script's buffers must outlive the
+    graph."""
+    if script.array is None:
+        script.build()
+    out = _VP()
+    rc = load_library().ps_graph_create(h, script.array, len(script), ctypes.byref(out))
+    return rc, (out.value or 0)
+
+
+def ps_graph_launch(h: int, graph: int) -> int:
+    return load_library().ps_graph_launch(h, graph)
+
+
+def ps_graph_destroy(graph: int) -> None:
+    load_library().ps_graph_destroy(graph)
 
 
 def ps_set_fronts(h: int, fronts_log2: int) -> int:

@@ -82,6 +82,9 @@ def test_validation_without_device(lib):
     assert lib.ps_set_fronts(None, 0) == ps.PS_EINVAL
     assert lib.ps_set_launch_shape(None, 1, 16) == ps.PS_EINVAL
     assert lib.ps_set_pull_fusion(None, -1) == ps.PS_EINVAL
+    assert lib.ps_graph_launch(None, None) == ps.PS_EINVAL
+    assert ps.ps_graph_create(None, ps.OpScript())[0] == ps.PS_EINVAL
+    lib.ps_graph_destroy(None)   # no-op
     assert lib.ps_timestamp(None) == 0 and lib.ps_num_params(None) == 0
     assert not lib.ps_weights(None)
     lib.ps_destroy(None)   # no-op

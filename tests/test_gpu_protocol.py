@@ -259,3 +259,157 @@ def test_run_script_equals_calls(torch, fused):
     srv.apply_pending()
     srv.close()
     del pool
+
+
+def _schedule_script(cfg, ev, pool, reps, fused):
+    """An OpScript of a workload schedule: pushes, applies (or apply+pull
+    with the first pull round) and pull rounds."""
+    sc = ps.OpScript()
+    i = 0
+    while i < len(ev):
+        e = ev[i]
+        if isinstance(e, wl.Push):
+            sc.push(e.learner, pool[e.buf].data_ptr())
+        elif isinstance(e, wl.Apply):
+            nxt = ev[i + 1] if i + 1 < len(ev) else None
+            if fused and isinstance(nxt, wl.Pull):
+                ls = parity.pull_rounds(nxt.learners)
+                sc.apply_pull(ls[0], [reps[l].data_ptr() for l in ls[0]])
+                for rnd in ls[1:]:
+                    sc.pull(rnd, [reps[l].data_ptr() for l in rnd])
+                i += 2
+                continue
+            sc.apply()
+        else:
+            for rnd in parity.pull_rounds(e.learners):
+                sc.pull(rnd, [reps[l].data_ptr() for l in rnd])
+        i += 1
+    return sc
+
+
+def _state(srv, reps, n_reps):
+    st = srv.stats()
+    return (parity.np_bits(srv.weights_copy()), parity.np_bits(srv.velocity_copy()),
+            [parity.np_bits(reps[l]) for l in range(n_reps)], srv.last_staleness(),
+            (st.timestamp, st.pushes_applied, st.pulls, st.pulls_skipped, st.staleness_sum))
+
+
+@pytest.mark.parametrize("fused", [False, True], ids=["separate", "fused"])
+def test_graph_replays_equal_run(torch, fused):
+    """A schedule captured as a HIP graph (ps_graph_create) and replayed
+    (ps_graph_launch) three times, each after resetting the weights and with
+    other work enqueued and synchronized on the same stream in between,
+    gives every time the bits, staleness and counters of ps_run of the same
+    schedule; capturing runs nothing and leaves the server's state as it
+    was."""
+    cfg = wl.CONFIGS["alexnet"].scaled(200_003, pushes=96, pool=16)
+    ev = wl.schedule(cfg)
+    pool = wl.make_pool(cfg, "cuda")
+    w0 = wl.make_w0(cfg, "cuda")
+    ref = ps.ParameterServer(cfg.n, cfg.lr, cfg.momentum, queue_depth=cfg.depth)
+    ref.set_stream(torch.cuda.current_stream())
+    ref.set_weights(w0)
+    ref_reps = wl.Rows(cfg.replicas, cfg.n, torch.float32, "cuda")
+    sc = _schedule_script(cfg, ev, pool, ref_reps, fused)
+    assert ps.ps_run(ref.h, sc) == (ps.PS_OK, len(sc))
+    want = _state(ref, ref_reps, cfg.replicas)
+    ref.close()
+
+    stream = torch.cuda.Stream()
+    srv = ps.ParameterServer(cfg.n, cfg.lr, cfg.momentum, queue_depth=cfg.depth, stream=stream)
+    srv.set_weights(w0)
+    srv.sync()
+    reps = wl.Rows(cfg.replicas, cfg.n, torch.float32, "cuda")
+    reps.buf.fill_(7.0)
+    w_before = parity.np_bits(srv.weights_copy())
+    rc, graph = ps.ps_graph_create(srv.h, _schedule_script(cfg, ev, pool, reps, fused))
+    assert rc == ps.PS_OK and graph
+    srv.sync()
+    assert srv.timestamp == 0 and ps.ps_pending(srv.h) == 0 and srv.stats().pulls == 0
+    assert parity.bitwise(parity.np_bits(srv.weights_copy()), w_before)
+    assert float(reps.buf.max()) == 7.0 == float(reps.buf.min())
+    side = torch.ones(1 << 20, device="cuda")
+    for rep in range(3):
+        srv.set_weights(w0)
+        with torch.cuda.stream(stream):
+            side.mul_(1.5)
+        torch.cuda.synchronize()
+        assert ps.ps_graph_launch(srv.h, graph) == ps.PS_OK, ps.ps_last_error()
+        srv.sync()
+        got = _state(srv, reps, cfg.replicas)
+        assert parity.bitwise(got[0], want[0]) and parity.bitwise(got[1], want[1]), rep
+        for a, b in zip(got[2], want[2]):
+            assert parity.bitwise(a, b), rep
+        assert got[3] == want[3] and got[4] == want[4], rep
+    ps.ps_graph_destroy(graph)
+    srv.close()
+
+
+def test_graph_launch_checks_the_plan(torch):
+    """A replay runs only if the calls would launch exactly the captured
+    kernels: a pull written at capture that would now be skipped refuses the
+    launch with PS_ESTATE and nothing changes; after a reset it runs again.
+    Graphs need a stream other than the null stream, ordered pulls and an
+    empty queue; a script that launches nothing, one that fails, and a graph
+    of another server are refused."""
+    n = 100_003
+    stream = torch.cuda.Stream()
+    srv = ps.ParameterServer(n, 0.01, 0.0, queue_depth=2, stream=stream)
+    w0 = torch.rand(n, device="cuda")
+    srv.set_weights(w0)
+    g = torch.full((n,), 0.25, device="cuda")
+    rep = torch.empty(n, device="cuda")
+
+    pull_only = ps.OpScript()
+    pull_only.pull([0], [rep.data_ptr()])
+    rc, graph = ps.ps_graph_create(srv.h, pull_only)
+    assert rc == ps.PS_OK
+    assert ps.ps_graph_launch(srv.h, graph) == ps.PS_OK        # written, as at capture
+    srv.sync()
+    assert parity.bitwise(parity.np_bits(rep), parity.np_bits(w0))
+    pulls = srv.stats().pulls
+    assert ps.ps_graph_launch(srv.h, graph) == ps.PS_ESTATE    # would be skipped now
+    assert srv.stats().pulls == pulls and srv.stats().pulls_skipped == 0
+    srv.set_weights(w0)                                         # pull history cleared
+    assert ps.ps_graph_launch(srv.h, graph) == ps.PS_OK
+
+    step = ps.OpScript()
+    step.push(0, g.data_ptr())
+    step.apply_pull([0], [rep.data_ptr()])
+    rc, g2 = ps.ps_graph_create(srv.h, step)
+    assert rc == ps.PS_OK
+    for k in range(1, 4):                                       # each replay one more step
+        assert ps.ps_graph_launch(srv.h, g2) == ps.PS_OK
+        assert srv.timestamp == k
+    srv.sync()
+    want = (w0.cpu().numpy().astype(np.float32) - np.float32(3 * np.float32(0.01) * np.float32(0.25)))
+    assert np.allclose(parity.np_bits(rep), want, rtol=0, atol=1e-6)
+
+    assert ps.ps_push(srv.h, 0, g.data_ptr()) == ps.PS_OK      # a pending gradient
+    assert ps.ps_graph_launch(srv.h, g2) == ps.PS_ESTATE
+    assert ps.ps_graph_create(srv.h, step)[0] == ps.PS_ESTATE
+    srv.apply_pending()
+    ts = srv.timestamp
+    pushes_only = ps.OpScript()
+    pushes_only.push(0, g.data_ptr())
+    assert ps.ps_graph_create(srv.h, pushes_only)[0] == ps.PS_EINVAL   # launches nothing
+    full = ps.OpScript()
+    for _ in range(3):
+        full.push(0, g.data_ptr())
+    full.apply()
+    assert ps.ps_graph_create(srv.h, full)[0] == ps.PS_EFULL          # the third push fails
+    assert srv.timestamp == ts and ps.ps_pending(srv.h) == 0
+
+    other = ps.ParameterServer(n, 0.01, 0.0, queue_depth=2, stream=stream)
+    assert ps.ps_graph_launch(other.h, g2) == ps.PS_EINVAL
+    null_stream = ps.ParameterServer(n, 0.01, 0.0, queue_depth=2)
+    assert ps.ps_graph_create(null_stream.h, step)[0] == ps.PS_ESTATE
+    side = torch.cuda.Stream()
+    srv.set_pull_stream(side)
+    assert ps.ps_graph_launch(srv.h, g2) == ps.PS_ESTATE
+    assert ps.ps_graph_create(srv.h, step)[0] == ps.PS_ESTATE
+    srv.sync()
+    for gr in (graph, g2):
+        ps.ps_graph_destroy(gr)
+    for s_ in (other, null_stream, srv):
+        s_.close()
