@@ -518,6 +518,7 @@ def main():
     # i + 1 while the device runs replay i), the steps left over as a second
     # graph
     graph_s = []
+    graph_note = None
     if pstream is None:
         cycle = len(calls)
         q, rem = divmod(args.steps, cycle)
@@ -533,12 +534,20 @@ def main():
         for _ in range(args.runs):
             reset()
             t0 = time.perf_counter()
+            rc = 0
             for g_, count in graphs:
                 for _ in range(count):
-                    if ps.ps_graph_launch(h, g_) != 0:
-                        raise RuntimeError(f"ps_graph_launch: {ps.ps_last_error()}")
+                    rc = rc or ps.ps_graph_launch(h, g_)
             torch.cuda.synchronize()
             t1 = time.perf_counter()
+            if rc == ps.PS_ESTATE and not args.graph:
+                # the plan changes from cycle to cycle (round-robin service
+                # order): the replay refuses, and there is no graph rate
+                graph_note = ps.ps_last_error()
+                graph_s = []
+                break
+            if rc != 0:
+                raise RuntimeError(f"ps_graph_launch: {ps.ps_last_error()}")
             graph_s.append(t1 - t0)
         for g_, _ in graphs:
             ps.ps_graph_destroy(g_)
@@ -619,6 +628,7 @@ def main():
             "ps_run_pushes_per_s": round(pushes / sorted(run_s)[len(run_s) // 2], 2),
             "graph_pushes_per_s": (round(pushes / sorted(graph_s)[len(graph_s) // 2], 2)
                                    if graph_s else None),
+            "graph_not_replayable": graph_note,
             "python_driven_pushes_per_s": round(pushes / py_elapsed, 2),
         },
         "higher_is_better": True,
