@@ -254,9 +254,9 @@ int ps_set_fronts(ps_server *ps, int fronts_log2);
  * gradients, momentum and the gradient type (tables measured at the VGG-16
  * and Mixed sizes):
  * blocks_per_cu 1..4 caps the resident 256-thread blocks per compute unit, 0
- * lifts the cap, -1 restores the library's choice; group 4, 8, 12 or 16 sets
- * how many gradients' loads are issued together, 0 restores the library's
- * choice. Results are identical for every shape; only speed changes. For
+ * lifts the cap, -1 restores the library's choice; group 4, 8, 12, 16, 24 or
+ * 32 sets how many gradients' loads are issued together (the synchronous step
+ * takes 16 for 24 and 32), 0 restores the library's choice. Results are identical for every shape; only speed changes. For
  * callers tuning other sizes. PS_EINVAL for other values, setting unchanged. */
 int ps_set_launch_shape(ps_server *ps, int blocks_per_cu, int group);
 

@@ -46,7 +46,8 @@ struct Geometry {
 };
 
 // How one apply launch runs: resident blocks per compute unit (1..4; 0 = as
-// many as fit) and gradients per load group (4, 8, 12 or 16; others = 16).
+// many as fit) and gradients per load group (4, 8, 12, 16, 24 or 32; others
+// = 16; the synchronous step takes 4, 8, 12 or 16, others = 16).
 struct Shape {
     int blocks_per_cu = 0;
     int group = 16;

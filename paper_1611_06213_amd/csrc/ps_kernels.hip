@@ -55,9 +55,10 @@ namespace {
 
 constexpr int kBlock = PS_BLOCK;      // threads per block (waves of 64 lanes)
 // Gradients whose loads are issued together: the vector kernels take the
-// group size their launcher chooses (4, 8, 12 or 16); the scalar paths take
-// kGroup. Full groups, then one of 8, then the remainder (at most 7) cover
-// every K for group sizes up to 16.
+// group size their launcher chooses (4, 8, 12, 16, 24 or 32 for the apply,
+// up to 16 for the synchronous step); the scalar paths take kGroup. Full
+// groups, then one of 16 (groups above 16), one of 8 (groups above 8) and
+// the remainder (at most 7) cover every K.
 constexpr int kGroup = PS_GROUP;
 static_assert(kGroup >= 1 && kGroup <= 16, "gradient group size must be 1..16");
 // w and v are read once and written once per launch and are not touched
@@ -276,7 +277,7 @@ __device__ __forceinline__ void apply_group(const ApplyArgs &a, int k0, uint64_t
 // per-gradient conditions would each wait for the memory in turn.
 template <bool MOM, int GDT, int PDT, int E, int G>
 __device__ __forceinline__ void apply_chunk(const ApplyArgs &a, uint64_t i) {
-    static_assert(G >= 1 && G <= 16, "gradient group size must be 1..16");
+    static_assert(G >= 1 && G <= 32, "gradient group size must be 1..32");
     float w[E], v[E];
     ld_f32<E, nt_wv_ld<E>()>(w, a.w + i);
     if constexpr (MOM) ld_f32<E, nt_wv_ld<E>()>(v, a.v + i);
@@ -289,6 +290,12 @@ __device__ __forceinline__ void apply_chunk(const ApplyArgs &a, uint64_t i) {
         k0 = G;
     }
     for (; k0 + G <= k; k0 += G) apply_group<MOM, GDT, E, G>(a, k0, i, w, v, lr, m);
+    if constexpr (G > 16) {
+        if (k0 + 16 <= k) {
+            apply_group<MOM, GDT, E, 16>(a, k0, i, w, v, lr, m);
+            k0 += 16;
+        }
+    }
     if constexpr (G > 8) {
         if (k0 + 8 <= k) {
             apply_group<MOM, GDT, E, 8>(a, k0, i, w, v, lr, m);
@@ -559,6 +566,8 @@ hipError_t launch_vec_g(const ApplyArgs &a, int group, unsigned lds, const Geome
         case 4: return launch_vec<MOM, GDT, PDT, E, 4>(a, lds, geo, s);
         case 8: return launch_vec<MOM, GDT, PDT, E, 8>(a, lds, geo, s);
         case 12: return launch_vec<MOM, GDT, PDT, E, 12>(a, lds, geo, s);
+        case 24: return launch_vec<MOM, GDT, PDT, E, 24>(a, lds, geo, s);
+        case 32: return launch_vec<MOM, GDT, PDT, E, 32>(a, lds, geo, s);
         default: return launch_vec<MOM, GDT, PDT, E, 16>(a, lds, geo, s);
     }
 }

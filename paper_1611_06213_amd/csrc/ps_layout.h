@@ -64,14 +64,15 @@ int fronts_log2_for(const void *const *ptrs, int count);
 // Launch shape of an apply of k gradients (fp32, or bf16): how many 256-thread
 // blocks one compute unit may hold (0 = as many as fit), for buffers at
 // distinct phases (where fronts_log2_for gives 0) how many fronts to sweep
-// (log2), and how many gradients each lane loads at once (4, 8, 12 or 16).
+// (log2), and how many gradients each lane loads at once (4, 8, 12, 16, 24 or
+// 32; the synchronous step's table stops at 16).
 // Fewer resident blocks and smaller groups keep fewer DRAM pages and address
 // translations live across the k + 2 streams; too few loads in flight starve
 // the memory system. Chosen from sweeps at the VGG-16 (fp32) and Mixed (bf16)
-// sizes from server rows, % of 8 TB/s: fp32 with momentum, k = 32: groups of
-// 16 at one block per CU 80.7, groups of 4 at two blocks 76.2; k = 4: groups
-// of 4 at two blocks 82.9, groups of 16 at three 80.0; bf16 with momentum,
-// k = 32: groups of 16 at one block 78.2, groups of 12 at one block 75.4.
+// sizes from server rows, % of 8 TB/s: fp32 with momentum, k = 32: one group
+// of 32 at one block per CU 82.2, groups of 16 81.7, groups of 4 at two blocks
+// 76.2; k = 4: groups of 4 at two blocks 82.9, groups of 16 at three 80.0;
+// bf16 with momentum, k = 24: groups of 24 at one block 79.9, of 16 77.9.
 struct ApplyShape {
     int blocks_per_cu;
     int fronts_log2;

@@ -890,8 +890,9 @@ int ps_set_launch_shape(ps_server *ps, int blocks_per_cu, int group) {
     PS_LOCK(ps);
     if (blocks_per_cu < -1 || blocks_per_cu > 4)
         return fail(PS_EINVAL, "blocks_per_cu %d outside [-1, 4]", blocks_per_cu);
-    if (group != 0 && group != 4 && group != 8 && group != 12 && group != 16)
-        return fail(PS_EINVAL, "group %d is not 0, 4, 8, 12 or 16", group);
+    if (group != 0 && group != 4 && group != 8 && group != 12 && group != 16 && group != 24 &&
+        group != 32)
+        return fail(PS_EINVAL, "group %d is not 0, 4, 8, 12, 16, 24 or 32", group);
     ps->force_blocks_per_cu = blocks_per_cu;
     ps->force_group = group;
     return PS_OK;

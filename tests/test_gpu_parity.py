@@ -1476,15 +1476,15 @@ def test_fronts_give_identical_bits(torch, layout, gdt):
 @pytest.mark.parametrize("m", [0.0, 0.9])
 @pytest.mark.parametrize("gdt", ["f32", "bf16"])
 def test_every_group_and_remainder(torch, gdt, m):
-    """Every gradient group size the launcher takes (4, 8, 12, 16), forced
-    with ps_set_launch_shape at every depth from 1 to two groups and 8 more,
-    so that the first group, the loop over further groups, the group of 8 and
-    each exact remainder of 1..7 all run, under residency caps 0..4 in turn:
+    """Every gradient group size the launcher takes (4, 8, 12, 16, 24, 32),
+    forced with ps_set_launch_shape at every depth from 1 to two groups and 8
+    more (at most 64), so that the first group, the loop over further groups,
+    the groups of 16 and 8 and each exact remainder of 1..7 all run, under residency caps 0..4 in turn:
     w and v equal the oracle's bits after the same gradients (batched is
     sequential, so one oracle run gives every depth); the same applies writing
     two fp32 or bf16 replicas from their own pass give those bits and RNE of
     them; the synchronous step at every group size and depth too."""
-    n, lr, kmax = 3 * 8192 + 5, 0.01, 40
+    n, lr, kmax = 3 * 8192 + 5, 0.01, 64
     say(f"[case] groups x remainders gradients={gdt} m={m} n={n}")
     tdt = torch.bfloat16 if gdt == "bf16" else torch.float32
     gen = torch.Generator(device="cuda")
@@ -1507,7 +1507,7 @@ def test_every_group_and_remainder(torch, gdt, m):
         want_sync[k] = so.w.view(np.uint32).copy()
     srv = ps.ParameterServer(n, lr, m, queue_depth=kmax)
     case = 0
-    for group in (4, 8, 12, 16):
+    for group in (4, 8, 12, 16, 24, 32):
         for k in range(1, min(2 * group + 8, kmax) + 1):
             srv.set_launch_shape(case % 5, group)
             case += 1
@@ -1538,7 +1538,7 @@ def test_every_group_and_remainder(torch, gdt, m):
             srv.apply_sync()
             assert parity.bitwise(parity.np_bits(srv.weights_copy()), want_sync[k]), ("sync", group, k)
     srv.set_launch_shape()
-    for bad in ((-2, 0), (5, 0), (1, 3), (1, 20)):
+    for bad in ((-2, 0), (5, 0), (1, 3), (1, 20), (1, 40)):
         with pytest.raises(ps.PSError):
             srv.set_launch_shape(*bad)
     srv.close()

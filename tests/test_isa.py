@@ -5,12 +5,13 @@
   multiply-add instructions: every product and sum is rounded on its own
   (the binary32 reading of Eq. "gd"), and packed fp32 stays disabled.
 * No kernel uses private (scratch) memory: registers hold every value.
-* The fused applies of the VGG-16 shape (fp32 gradients, groups of 16) and
-  of the Mixed shape (bf16 gradients, groups of 16) issue each group's 16
+* The fused applies of the VGG-16 shape (fp32 gradients, one group of 32)
+  and of the Mixed shape (bf16 gradients, groups of 24) issue each group's
   gradient loads back to back, non-temporal, before waiting for the first:
-  the loads a lane keeps in flight set the apply's bandwidth. The remainder
-  after the full groups is one straight-line group too (7 loads together for
-  a remainder of 7), not one load and one wait per gradient.
+  the loads a lane keeps in flight set the apply's bandwidth. The first group
+  goes out together with the w/v loads. The remainder after the full groups
+  is straight-line groups too (16, 8, then 7 loads together for a remainder
+  of 7), not one load and one wait per gradient.
 """
 import os
 import re
@@ -22,8 +23,8 @@ import pytest
 from paper_1611_06213_amd import build as B
 
 KERNELS = os.path.join(B.CSRC, "ps_kernels.hip")
-VGG16_APPLY = "_ZN5gadei12_GLOBAL__N_19apply_vecILb1ELi0ELin1ELi4ELi16EEEvNS_9ApplyArgsE"
-MIXED_APPLY = "_ZN5gadei12_GLOBAL__N_19apply_vecILb1ELi1ELin1ELi8ELi16EEEvNS_9ApplyArgsE"
+VGG16_APPLY = "_ZN5gadei12_GLOBAL__N_19apply_vecILb1ELi0ELin1ELi4ELi32EEEvNS_9ApplyArgsE"
+MIXED_APPLY = "_ZN5gadei12_GLOBAL__N_19apply_vecILb1ELi1ELin1ELi8ELi24EEEvNS_9ApplyArgsE"
 
 
 @pytest.fixture(scope="module")
@@ -73,8 +74,9 @@ def test_no_kernel_uses_scratch(asm):
         assert m and int(m.group(1)) == 0, name
 
 
-@pytest.mark.parametrize("name", [VGG16_APPLY, MIXED_APPLY], ids=["vgg16-fp32", "mixed-bf16"])
-def test_group_loads_issued_together(asm, name):
+@pytest.mark.parametrize("name,group,wv", [(VGG16_APPLY, 32, 2), (MIXED_APPLY, 24, 4)],
+                         ids=["vgg16-fp32", "mixed-bf16"])
+def test_group_loads_issued_together(asm, name, group, wv):
     body, _ = kernels(asm)[name]
     runs, run = [], 0
     for l in body:
@@ -85,8 +87,11 @@ def test_group_loads_issued_together(asm, name):
             runs.append(run)
             run = 0
     runs.append(run)
-    # the first group (after the 2 or 4 w/v loads) and the loop's groups
-    assert sum(1 for r in runs if r >= 16) >= 2, runs
+    runs = [r for r in runs if r]
+    # the first group with the w/v loads (w and v: 1 load each of 4 fp32, 2
+    # each of 8), the loop's groups, then the groups of 16 and 8
+    assert runs[0] == wv + group, runs
+    assert group in runs[1:] and 16 in runs and 8 in runs, runs
     # remainder groups of 1..7 loads, each issued whole
     for size in range(2, 8):
         assert size in runs, (size, runs)

@@ -260,15 +260,19 @@ def test_apply_shape_table(driver):
     """The launch shapes applies and synchronous steps take (blocks per CU,
     0 = no cap; fronts log2; gradients per load group), as measured at the
     VGG-16 (fp32) and Mixed (bf16) sizes; every depth gets a shape the
-    launcher supports."""
+    launcher supports, groups of 24 and 32 only for applies that fill them."""
     for cmd, want in (("shape", SHAPES), ("sync_shape", SYNC_SHAPES)):
         got = run_driver(driver, [f"{cmd} {k} {m} {b}" for (k, m, b) in want])
         assert got == [f"{cmd} {x} {y} {z}" for (x, y, z) in want.values()]
-        allk = run_driver(driver, [f"{cmd} {k} {m} {b}" for k in range(1, 65) for m in (0, 1)
-                                   for b in (0, 1)])
-        for line in allk:
+        cases = [(k, m, b) for k in range(1, 65) for m in (0, 1) for b in (0, 1)]
+        allk = run_driver(driver, [f"{cmd} {k} {m} {b}" for (k, m, b) in cases])
+        groups = (4, 8, 12, 16, 24, 32) if cmd == "shape" else (4, 8, 12, 16)
+        for (k, _, _), line in zip(cases, allk):
             b, f, g = map(int, line.split()[1:])
-            assert 0 <= b <= 4 and f in (0, 1) and g in (4, 8, 12, 16)
+            assert 0 <= b <= 4 and f in (0, 1) and g in groups
+            # a group above 16 only from its own depth on (below it the
+            # first group would not overlap the w/v loads)
+            assert g <= 16 or g <= k, (cmd, k, g)
 
 
 def test_replica_fusion_rule(driver):
@@ -284,12 +288,15 @@ def test_replica_fusion_rule(driver):
 # (K, momentum, bf16) -> (blocks per CU, fronts log2, group)
 SHAPES = {
     (1, 1, 0): (4, 0, 16), (2, 1, 0): (3, 0, 4), (4, 1, 0): (2, 0, 4), (8, 1, 0): (2, 0, 4),
-    (12, 1, 0): (1, 0, 12), (16, 1, 0): (1, 0, 16), (20, 1, 0): (1, 0, 12), (32, 1, 0): (1, 0, 16),
-    (40, 1, 0): (1, 0, 16), (48, 1, 0): (1, 0, 8), (64, 1, 0): (1, 0, 8),
+    (12, 1, 0): (1, 0, 12), (16, 1, 0): (1, 0, 16), (20, 1, 0): (1, 0, 12), (24, 1, 0): (1, 0, 16),
+    (31, 1, 0): (1, 0, 16), (32, 1, 0): (1, 0, 32), (40, 1, 0): (1, 0, 32), (41, 1, 0): (1, 0, 8),
+    (48, 1, 0): (1, 0, 8), (64, 1, 0): (1, 0, 8),
     (2, 0, 0): (0, 0, 16), (3, 0, 0): (3, 0, 4), (8, 0, 0): (2, 0, 4), (16, 0, 0): (1, 0, 16),
     (20, 0, 0): (2, 0, 4), (32, 0, 0): (1, 0, 8), (64, 0, 0): (1, 0, 8),
-    (8, 1, 1): (2, 0, 16), (16, 1, 1): (1, 0, 16), (32, 1, 1): (1, 0, 16), (64, 1, 1): (1, 0, 16),
-    (8, 0, 1): (2, 0, 8), (16, 0, 1): (1, 0, 16), (48, 0, 1): (1, 0, 16), (64, 0, 1): (1, 0, 8),
+    (8, 1, 1): (2, 0, 16), (16, 1, 1): (1, 0, 16), (23, 1, 1): (1, 0, 16), (24, 1, 1): (1, 0, 24),
+    (32, 1, 1): (1, 0, 24), (40, 1, 1): (1, 0, 24), (48, 1, 1): (1, 0, 16), (64, 1, 1): (1, 0, 16),
+    (8, 0, 1): (2, 0, 8), (16, 0, 1): (1, 0, 16), (24, 0, 1): (1, 0, 24), (32, 0, 1): (1, 0, 32),
+    (40, 0, 1): (1, 0, 32), (48, 0, 1): (1, 0, 16), (64, 0, 1): (1, 0, 8),
 }
 
 # (learners, momentum, bf16) -> (blocks per CU, fronts log2, group)
