@@ -45,21 +45,21 @@ int fronts_log2_for(const void *const *ptrs, int count) {
 
 ApplyShape apply_shape(int k, bool momentum, bool bf16) {
     // Measured at 138,357,544 fp32 / 200,000,000 bf16 parameters for the
-    // depths 1, 2, 3, 4, 6, 8, 12, 16, 20, 24, 32, 48 and 64 (bf16: from 8);
-    // the depths between take a neighbour's shape. A group of 24 or 32 pays
-    // only from its own depth on: below it the w/v loads would be waited for
-    // before the first (smaller) group.
+    // depths 1, 2, 3, 4, 6, 8, 12, 16, 20, 24, 32, 36, 40, 44, 48 and 64
+    // (bf16: from 8); the depths between take a neighbour's shape. A group of
+    // 24 or 32 pays only from its own depth on: below it the w/v loads would
+    // be waited for before the first (smaller) group.
     if (bf16) {
         if (momentum) {
             if (k <= 11) return {2, 0, 16};
             if (k <= 23) return {1, 0, 16};
-            if (k <= 40) return {1, 0, 24};
+            if (k <= 44) return {1, 0, 24};
             return {1, 0, 16};
         }
         if (k <= 11) return {2, 0, 8};
         if (k <= 23) return {1, 0, 16};
         if (k <= 31) return {1, 0, 24};
-        if (k <= 40) return {1, 0, 32};
+        if (k <= 47) return {1, 0, 32};
         if (k <= 56) return {1, 0, 16};
         return {1, 0, 8};
     }
@@ -71,7 +71,7 @@ ApplyShape apply_shape(int k, bool momentum, bool bf16) {
         if (k <= 17) return {1, 0, 16};
         if (k <= 21) return {1, 0, 12};
         if (k <= 31) return {1, 0, 16};
-        if (k <= 40) return {1, 0, 32};
+        if (k <= 44) return {1, 0, 32};
         return {1, 0, 8};
     }
     if (k <= 2) return {0, 0, 16};

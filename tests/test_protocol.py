@@ -289,14 +289,14 @@ def test_replica_fusion_rule(driver):
 SHAPES = {
     (1, 1, 0): (4, 0, 16), (2, 1, 0): (3, 0, 4), (4, 1, 0): (2, 0, 4), (8, 1, 0): (2, 0, 4),
     (12, 1, 0): (1, 0, 12), (16, 1, 0): (1, 0, 16), (20, 1, 0): (1, 0, 12), (24, 1, 0): (1, 0, 16),
-    (31, 1, 0): (1, 0, 16), (32, 1, 0): (1, 0, 32), (40, 1, 0): (1, 0, 32), (41, 1, 0): (1, 0, 8),
+    (31, 1, 0): (1, 0, 16), (32, 1, 0): (1, 0, 32), (44, 1, 0): (1, 0, 32), (45, 1, 0): (1, 0, 8),
     (48, 1, 0): (1, 0, 8), (64, 1, 0): (1, 0, 8),
     (2, 0, 0): (0, 0, 16), (3, 0, 0): (3, 0, 4), (8, 0, 0): (2, 0, 4), (16, 0, 0): (1, 0, 16),
     (20, 0, 0): (2, 0, 4), (32, 0, 0): (1, 0, 8), (64, 0, 0): (1, 0, 8),
     (8, 1, 1): (2, 0, 16), (16, 1, 1): (1, 0, 16), (23, 1, 1): (1, 0, 16), (24, 1, 1): (1, 0, 24),
-    (32, 1, 1): (1, 0, 24), (40, 1, 1): (1, 0, 24), (48, 1, 1): (1, 0, 16), (64, 1, 1): (1, 0, 16),
+    (32, 1, 1): (1, 0, 24), (44, 1, 1): (1, 0, 24), (45, 1, 1): (1, 0, 16), (64, 1, 1): (1, 0, 16),
     (8, 0, 1): (2, 0, 8), (16, 0, 1): (1, 0, 16), (24, 0, 1): (1, 0, 24), (32, 0, 1): (1, 0, 32),
-    (40, 0, 1): (1, 0, 32), (48, 0, 1): (1, 0, 16), (64, 0, 1): (1, 0, 8),
+    (47, 0, 1): (1, 0, 32), (48, 0, 1): (1, 0, 16), (64, 0, 1): (1, 0, 8),
 }
 
 # (learners, momentum, bf16) -> (blocks per CU, fronts log2, group)
