@@ -425,7 +425,8 @@ int ps_run(ps_server *ps, const ps_op *ops, int count, int *done);
  * (PS_ESTATE otherwise); scripts start from an empty queue. PS_EINVAL for a
  * bad script, a script that launches nothing, or a graph of another
  * server. Destroy graphs before their server; a graph is launched only on
- * the server it was created for. */
+ * the server it was created for. ps_graph_destroy waits for the graph's
+ * last launch to finish. */
 typedef struct ps_graph ps_graph;
 int ps_graph_create(ps_server *ps, const ps_op *ops, int count, ps_graph **graph);
 int ps_graph_launch(ps_server *ps, ps_graph *graph);

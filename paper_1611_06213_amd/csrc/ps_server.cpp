@@ -376,6 +376,7 @@ struct ps_graph {
     ps_server *server = nullptr;
     hipGraph_t graph = nullptr;
     hipGraphExec_t exec = nullptr;
+    hipEvent_t done = nullptr;   // recorded after each replay
     std::vector<ps_op> ops;
     std::vector<std::vector<int>> ids;
     std::vector<std::vector<void *>> dsts;
@@ -417,7 +418,12 @@ bool same_plan(const std::vector<LaunchRecord> &a, const std::vector<LaunchRecor
            (a.empty() || std::memcmp(a.data(), b.data(), a.size() * sizeof(LaunchRecord)) == 0);
 }
 
+// Waits for the graph's last replay before freeing it.
 void free_graph(ps_graph *g) {
+    if (g->done) {
+        (void)hipEventSynchronize(g->done);
+        (void)hipEventDestroy(g->done);
+    }
     if (g->exec) (void)hipGraphExecDestroy(g->exec);
     if (g->graph) (void)hipGraphDestroy(g->graph);
     delete g;
@@ -1032,6 +1038,10 @@ int ps_graph_create(ps_server *ps, const ps_op *ops, int count, ps_graph **out) 
         e = hipGraphInstantiate(&g->exec, g->graph, nullptr, nullptr, 0);
         if (e != hipSuccess) rc = fail_hip(e, "hipGraphInstantiate");
     }
+    if (rc == PS_OK) {
+        e = hipEventCreateWithFlags(&g->done, hipEventDisableTiming);
+        if (e != hipSuccess) rc = fail_hip(e, "hipEventCreateWithFlags");
+    }
     if (rc != PS_OK) {
         free_graph(g);
         return rc;
@@ -1055,7 +1065,10 @@ int ps_graph_launch(ps_server *ps, ps_graph *g) {
         rc = fail(PS_ESTATE, "the script would now launch other kernels than were captured");
     if (rc == PS_OK) {
         const hipError_t e = hipGraphLaunch(g->exec, ps->stream);
-        if (e != hipSuccess) rc = fail_hip(e, "hipGraphLaunch");
+        if (e != hipSuccess)
+            rc = fail_hip(e, "hipGraphLaunch");
+        else   // the work is enqueued and committed; the event only serves destroy
+            (void)hipEventRecord(g->done, ps->stream);
     }
     if (rc != PS_OK) ps->proto = saved;
     return rc;

@@ -345,6 +345,36 @@ def test_graph_replays_equal_run(torch, fused):
     srv.close()
 
 
+def test_graph_destroy_waits_for_its_launches(torch):
+    """ps_graph_destroy right after 20 replays, with no synchronization in
+    between, returns only once they have run: the stream is idle then, and
+    the replica holds the 20th step's weights (20 sequential binary32 steps
+    of Eq. gd, computed here in numpy)."""
+    n = 1_000_003
+    stream = torch.cuda.Stream()
+    srv = ps.ParameterServer(n, 0.01, 0.0, queue_depth=2, stream=stream)
+    w0 = torch.rand(n, device="cuda")
+    srv.set_weights(w0)
+    g = torch.full((n,), 0.25, device="cuda")
+    rep = torch.empty(n, device="cuda")
+    step = ps.OpScript()
+    step.push(0, g.data_ptr())
+    step.apply_pull([0], [rep.data_ptr()])
+    rc, graph = ps.ps_graph_create(srv.h, step)
+    assert rc == ps.PS_OK
+    for _ in range(20):
+        assert ps.ps_graph_launch(srv.h, graph) == ps.PS_OK
+    ps.ps_graph_destroy(graph)
+    assert stream.query()
+    w = w0.cpu().numpy().astype(np.float32)
+    p = np.float32(np.float32(0.01) * np.float32(0.25))
+    for _ in range(20):
+        w = (w - p).astype(np.float32)
+    assert parity.bitwise(parity.np_bits(rep), w.view(np.uint32))
+    assert srv.timestamp == 20
+    srv.close()
+
+
 def test_graph_launch_checks_the_plan(torch):
     """A replay runs only if the calls would launch exactly the captured
     kernels: a pull written at capture that would now be skipped refuses the
