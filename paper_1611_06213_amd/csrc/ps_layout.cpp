@@ -43,7 +43,7 @@ int fronts_log2_for(const void *const *ptrs, int count) {
     return (streams >= 8 && 2 * most > streams) ? 2 : 0;
 }
 
-ApplyShape apply_shape(int k, bool momentum, bool bf16) {
+ApplyShape apply_shape(int k, bool momentum, bool bf16, size_t n) {
     // Measured at 138,357,544 fp32 / 200,000,000 bf16 parameters for the
     // depths 1, 2, 3, 4, 6, 8, 12, 16, 20, 24, 32, 36, 40, 44, 48 and 64
     // (bf16: from 8); the depths between take a neighbour's shape. A group of
@@ -76,7 +76,7 @@ ApplyShape apply_shape(int k, bool momentum, bool bf16) {
     }
     if (k <= 2) return {0, 0, 16};
     if (k <= 6) return {3, 0, 4};
-    if (k <= 13) return {2, 0, 4};
+    if (k <= 13) return n < kSmallVector ? ApplyShape{3, 0, 4} : ApplyShape{2, 0, 4};
     if (k <= 17) return {1, 0, 16};
     if (k <= 21) return {2, 0, 4};
     return {1, 0, 8};

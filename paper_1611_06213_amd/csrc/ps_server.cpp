@@ -179,7 +179,8 @@ int fronts_for(const ps_server *ps, const gadei::ApplyArgs &a, int gdt) {
     p[c++] = a.w;
     p[c++] = a.v;   // null without momentum: not a stream
     const int f = gadei::fronts_log2_for(p, c);
-    if (f == 0 && gdt >= 0) return gadei::apply_shape(a.k, a.v != nullptr, gdt == PS_BF16).fronts_log2;
+    if (f == 0 && gdt >= 0)
+        return gadei::apply_shape(a.k, a.v != nullptr, gdt == PS_BF16, a.n).fronts_log2;
     return f;
 }
 
@@ -252,7 +253,7 @@ int launch_batch(ps_server *ps, const std::vector<PushDesc> &items, int pull_dty
         a.r = 0;
         a.fronts_log2 = fronts_for(ps, a, gdt);
         const gadei::Shape shape =
-            shape_for(ps, gadei::apply_shape(a.k, a.v != nullptr, gdt == PS_BF16));
+            shape_for(ps, gadei::apply_shape(a.k, a.v != nullptr, gdt == PS_BF16, a.n));
         int pdt = -1;
         if (end == q && pull_dtype >= 0 && !write.empty()) {
             pdt = pull_dtype;

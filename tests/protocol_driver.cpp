@@ -13,7 +13,8 @@
 //   drop L | retire L | depth K | mode M S | skip 0|1 | state
 //   fronts A1 A2 ...      front choice for streams at addresses Ai (0 = none)
 //   rows B C              row layout of C rows of B bytes: head stride span
-//   shape K M B           launch shape of a K-gradient apply (M = 1: momentum; B = 1: bf16)
+//   shape K M B [N]       launch shape of a K-gradient apply (M = 1: momentum; B = 1: bf16)
+//                         over N coordinates (default 138,357,544)
 //   sync_shape K M B      the same for a synchronous step over K learners
 //   fuse R K              1 if ps_apply_pull writes R replicas from the apply of K gradients
 #include <cstdio>
@@ -163,9 +164,11 @@ int main() {
             std::printf("fuse %d", gadei::fuse_replicas(static_cast<int>(r), static_cast<int>(k)) ? 1 : 0);
         } else if (cmd == "shape" || cmd == "sync_shape") {
             long k, m, b = 0;
+            size_t n = 138357544;
             in >> k >> m >> b;
+            if (!(in >> n)) n = 138357544;
             const gadei::ApplyShape sh =
-                cmd == "shape" ? gadei::apply_shape(static_cast<int>(k), m != 0, b != 0)
+                cmd == "shape" ? gadei::apply_shape(static_cast<int>(k), m != 0, b != 0, n)
                                : gadei::sync_shape(static_cast<int>(k), m != 0, b != 0);
             std::printf("%s %d %d %d", cmd.c_str(), sh.blocks_per_cu, sh.fronts_log2, sh.group);
         } else if (cmd == "state") {

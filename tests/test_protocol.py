@@ -260,7 +260,9 @@ def test_apply_shape_table(driver):
     """The launch shapes applies and synchronous steps take (blocks per CU,
     0 = no cap; fronts log2; gradients per load group), as measured at the
     VGG-16 (fp32) and Mixed (bf16) sizes; every depth gets a shape the
-    launcher supports, groups of 24 and 32 only for applies that fill them."""
+    launcher supports, groups of 24 and 32 only for applies that fill them.
+    Below 20M coordinates a shallow fp32 apply without momentum keeps three
+    blocks per CU instead of two."""
     for cmd, want in (("shape", SHAPES), ("sync_shape", SYNC_SHAPES)):
         got = run_driver(driver, [f"{cmd} {k} {m} {b}" for (k, m, b) in want])
         assert got == [f"{cmd} {x} {y} {z}" for (x, y, z) in want.values()]
@@ -273,6 +275,12 @@ def test_apply_shape_table(driver):
             # a group above 16 only from its own depth on (below it the
             # first group would not overlap the w/v loads)
             assert g <= 16 or g <= k, (cmd, k, g)
+    small = {(8, 0, 0, 10_000_000): (3, 0, 4), (13, 0, 0, 19_999_999): (3, 0, 4),
+             (8, 0, 0, 20_000_000): (2, 0, 4), (14, 0, 0, 10_000_000): (1, 0, 16),
+             (6, 0, 0, 10_000_000): (3, 0, 4), (8, 1, 0, 10_000_000): (2, 0, 4),
+             (8, 0, 1, 10_000_000): (2, 0, 8)}
+    got = run_driver(driver, [f"shape {k} {m} {b} {n}" for (k, m, b, n) in small])
+    assert got == [f"shape {x} {y} {z}" for (x, y, z) in small.values()]
 
 
 def test_replica_fusion_rule(driver):
