@@ -261,28 +261,33 @@ def test_run_script_equals_calls(torch, fused):
     del pool
 
 
-def _schedule_script(cfg, ev, pool, reps, fused):
-    """An OpScript of a workload schedule: pushes, applies (or apply+pull
-    with the first pull round) and pull rounds."""
+def _schedule_script(cfg, ev, pool, reps, fused, sync=False):
+    """An OpScript of a workload schedule in the workload's gradient and
+    replica dtypes: pushes, applies (or apply+pull with the first pull
+    round; with sync, synchronous steps) and pull rounds."""
     sc = ps.OpScript()
+    gdt, pdt = cfg.grad_dtype, cfg.pull_dtype
     i = 0
     while i < len(ev):
         e = ev[i]
         if isinstance(e, wl.Push):
-            sc.push(e.learner, pool[e.buf].data_ptr())
+            sc.push(e.learner, pool[e.buf].data_ptr(), gdt)
         elif isinstance(e, wl.Apply):
             nxt = ev[i + 1] if i + 1 < len(ev) else None
-            if fused and isinstance(nxt, wl.Pull):
+            if sync:
+                sc.apply_sync()
+            elif fused and isinstance(nxt, wl.Pull):
                 ls = parity.pull_rounds(nxt.learners)
-                sc.apply_pull(ls[0], [reps[l].data_ptr() for l in ls[0]])
+                sc.apply_pull(ls[0], [reps[l].data_ptr() for l in ls[0]], pdt)
                 for rnd in ls[1:]:
-                    sc.pull(rnd, [reps[l].data_ptr() for l in rnd])
+                    sc.pull(rnd, [reps[l].data_ptr() for l in rnd], pdt)
                 i += 2
                 continue
-            sc.apply()
+            else:
+                sc.apply()
         else:
             for rnd in parity.pull_rounds(e.learners):
-                sc.pull(rnd, [reps[l].data_ptr() for l in rnd])
+                sc.pull(rnd, [reps[l].data_ptr() for l in rnd], pdt)
         i += 1
     return sc
 
@@ -294,23 +299,29 @@ def _state(srv, reps, n_reps):
             (st.timestamp, st.pushes_applied, st.pulls, st.pulls_skipped, st.staleness_sum))
 
 
-@pytest.mark.parametrize("fused", [False, True], ids=["separate", "fused"])
-def test_graph_replays_equal_run(torch, fused):
+@pytest.mark.parametrize("name,fused,sync", [("alexnet", False, False), ("alexnet", True, False),
+                                             ("mixed", False, False), ("mixed", True, False),
+                                             ("vgg16", False, True)],
+                         ids=["alexnet-separate", "alexnet-fused", "mixed-bf16-separate",
+                              "mixed-bf16-fused", "vgg16-ssgd"])
+def test_graph_replays_equal_run(torch, name, fused, sync):
     """A schedule captured as a HIP graph (ps_graph_create) and replayed
     (ps_graph_launch) three times, each after resetting the weights and with
     other work enqueued and synchronized on the same stream in between,
     gives every time the bits, staleness and counters of ps_run of the same
-    schedule; capturing runs nothing and leaves the server's state as it
-    was."""
-    cfg = wl.CONFIGS["alexnet"].scaled(200_003, pushes=96, pool=16)
+    schedule (fp32, or bf16 gradients and replicas; asynchronous applies,
+    apply+pull, or synchronous steps); capturing runs nothing and leaves the
+    server's state as it was."""
+    cfg = wl.CONFIGS[name].scaled(200_003, pushes=96, pool=16)
     ev = wl.schedule(cfg)
     pool = wl.make_pool(cfg, "cuda")
     w0 = wl.make_w0(cfg, "cuda")
     ref = ps.ParameterServer(cfg.n, cfg.lr, cfg.momentum, queue_depth=cfg.depth)
     ref.set_stream(torch.cuda.current_stream())
     ref.set_weights(w0)
-    ref_reps = wl.Rows(cfg.replicas, cfg.n, torch.float32, "cuda")
-    sc = _schedule_script(cfg, ev, pool, ref_reps, fused)
+    rdt = torch.bfloat16 if cfg.pull_dtype == ps.PS_BF16 else torch.float32
+    ref_reps = wl.Rows(cfg.replicas, cfg.n, rdt, "cuda")
+    sc = _schedule_script(cfg, ev, pool, ref_reps, fused, sync)
     assert ps.ps_run(ref.h, sc) == (ps.PS_OK, len(sc))
     want = _state(ref, ref_reps, cfg.replicas)
     ref.close()
@@ -319,10 +330,10 @@ def test_graph_replays_equal_run(torch, fused):
     srv = ps.ParameterServer(cfg.n, cfg.lr, cfg.momentum, queue_depth=cfg.depth, stream=stream)
     srv.set_weights(w0)
     srv.sync()
-    reps = wl.Rows(cfg.replicas, cfg.n, torch.float32, "cuda")
+    reps = wl.Rows(cfg.replicas, cfg.n, rdt, "cuda")
     reps.buf.fill_(7.0)
     w_before = parity.np_bits(srv.weights_copy())
-    rc, graph = ps.ps_graph_create(srv.h, _schedule_script(cfg, ev, pool, reps, fused))
+    rc, graph = ps.ps_graph_create(srv.h, _schedule_script(cfg, ev, pool, reps, fused, sync))
     assert rc == ps.PS_OK and graph
     srv.sync()
     assert srv.timestamp == 0 and ps.ps_pending(srv.h) == 0 and srv.stats().pulls == 0
@@ -341,6 +352,57 @@ def test_graph_replays_equal_run(torch, fused):
         for a, b in zip(got[2], want[2]):
             assert parity.bitwise(a, b), rep
         assert got[3] == want[3] and got[4] == want[4], rep
+    ps.ps_graph_destroy(graph)
+    srv.close()
+
+
+def test_graph_refuses_a_moved_round_robin_order(torch):
+    """Round-robin queues: a cycle that leaves the service position on
+    another learner makes the next cycle serve the learners in another
+    order, so its kernels differ from the captured ones. The first replay
+    runs (it starts where the capture started) and equals ps_run; the second
+    is refused with PS_ESTATE and nothing changes; after ps_set_weights
+    (which restarts the service order) it runs again."""
+    n = 100_003
+    stream = torch.cuda.Stream()
+    srv = ps.ParameterServer(n, 0.01, 0.9, queue_depth=2, stream=stream)
+    srv.set_queue_mode(ps.PS_QUEUE_ROUND_ROBIN, 2)
+    w0 = torch.rand(n, device="cuda")
+    gs = [torch.full((n,), 0.25 * (j + 1), device="cuda") for j in range(4)]
+    sc = ps.OpScript()
+    for l, j in ((0, 0), (1, 1), (2, 2)):
+        sc.push(l, gs[j].data_ptr())
+    sc.apply()                       # serves learners 0 and 1
+    sc.push(0, gs[3].data_ptr())
+    sc.apply()                       # serves 2, then 0: the position ends on 0
+
+    ref = ps.ParameterServer(n, 0.01, 0.9, queue_depth=2, stream=stream)
+    ref.set_queue_mode(ps.PS_QUEUE_ROUND_ROBIN, 2)
+    ref.set_weights(w0)
+    assert ps.ps_run(ref.h, sc) == (ps.PS_OK, len(sc))
+    ref.sync()
+    want_w, want_v = parity.np_bits(ref.weights_copy()), parity.np_bits(ref.velocity_copy())
+    want_order = ref.last_applied()
+    ref.close()
+
+    srv.set_weights(w0)
+    rc, graph = ps.ps_graph_create(srv.h, sc)
+    assert rc == ps.PS_OK
+    assert ps.ps_graph_launch(srv.h, graph) == ps.PS_OK, ps.ps_last_error()
+    srv.sync()
+    assert parity.bitwise(parity.np_bits(srv.weights_copy()), want_w)
+    assert parity.bitwise(parity.np_bits(srv.velocity_copy()), want_v)
+    assert srv.last_applied() == want_order
+    ts, stats = srv.timestamp, srv.stats()
+    assert ps.ps_graph_launch(srv.h, graph) == ps.PS_ESTATE
+    assert srv.timestamp == ts == 4 and ps.ps_pending(srv.h) == 0
+    assert srv.stats().pushes_applied == stats.pushes_applied
+    srv.sync()
+    assert parity.bitwise(parity.np_bits(srv.weights_copy()), want_w)
+    srv.set_weights(w0)
+    assert ps.ps_graph_launch(srv.h, graph) == ps.PS_OK
+    srv.sync()
+    assert parity.bitwise(parity.np_bits(srv.weights_copy()), want_w)
     ps.ps_graph_destroy(graph)
     srv.close()
 
