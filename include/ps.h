@@ -215,8 +215,8 @@ int ps_record(ps_server *ps, void *event);
  * to (ps_record + hipStreamWaitEvent). A lock-free pull never makes a copy
  * count as current, so the next pull of that learner is not skipped; the
  * learner's timestamp is taken at the call. ps_apply_pull still orders its
- * pull after its apply. NULL (default)
- * restores ordered pulls -- the paper's read-write-lock option. Waits for
+ * pull after its apply. NULL (default) restores ordered pulls -- the
+ * paper's read-write-lock option. Waits for
  * earlier lock-free pulls before switching; ps_sync, ps_set_weights,
  * ps_save, ps_load and ps_destroy wait for them too. */
 int ps_set_pull_stream(ps_server *ps, void *hip_stream);
@@ -245,19 +245,20 @@ int ps_set_queue_mode(ps_server *ps, int mode, int slots_per_learner);
  * offsets within 2 MiB -- four fronts when at least 8 buffers take part and
  * more than half of the gradient, w and v buffers share one 4 KiB offset (as
  * separately allocated, 2 MiB-aligned buffers do), one front otherwise
- * (ps_alloc_rows buffers). Results are identical
- * either way; only the order in which the grid visits coordinates changes. */
+ * (ps_alloc_rows buffers). Results are identical either way; only the
+ * order in which the grid visits coordinates changes. */
 int ps_set_fronts(ps_server *ps, int fronts_log2);
 
 /* Override the launch shape of the apply (Eq. "asgd") and synchronous-step
  * (Eq. "ssgd") kernels, which is otherwise chosen per call from the number of
- * gradients, momentum and the gradient type (tables measured at the VGG-16
- * and Mixed sizes):
+ * gradients, momentum, the gradient type and, for shallow applies, the
+ * vector's length (tables measured at the VGG-16, Mixed and Text-CNN sizes):
  * blocks_per_cu 1..4 caps the resident 256-thread blocks per compute unit, 0
  * lifts the cap, -1 restores the library's choice; group 4, 8, 12, 16, 24 or
  * 32 sets how many gradients' loads are issued together (the synchronous step
- * takes 16 for 24 and 32), 0 restores the library's choice. Results are identical for every shape; only speed changes. For
- * callers tuning other sizes. PS_EINVAL for other values, setting unchanged. */
+ * takes 16 for 24 and 32), 0 restores the library's choice. Results are
+ * identical for every shape; only speed changes. For callers tuning other
+ * sizes. PS_EINVAL for other values, setting unchanged. */
 int ps_set_launch_shape(ps_server *ps, int blocks_per_cu, int group);
 
 /* Enable (1) or disable (0) skipping of pulls that are already current. */
@@ -334,9 +335,9 @@ int ps_load(ps_server *ps, const char *path);
  * Smaller rows are packed on 4 KiB boundaries. An apply then streams its
  * gradients, w and v from spread-out addresses, which the DRAM serves
  * fastest of the layouts measured. Buffers allocated one by one
- * (2 MiB-aligned, all at one phase) are served slower;
- * for them the apply kernels switch to a schedule that recovers part of the
- * difference. Contents are uninitialised. The buffers belong to the server
+ * (2 MiB-aligned, all at one phase) are served slower; for them the apply
+ * kernels switch to a schedule that recovers part of the difference.
+ * Contents are uninitialised. The buffers belong to the server
  * until ps_free_rows(ps, rows[0]) or ps_destroy. PS_ENOMEM if the device
  * allocation fails. */
 int ps_alloc_rows(ps_server *ps, int count, int dtype, void **rows);
