@@ -1,7 +1,7 @@
 """Whole-vector parity at full size (Eq. gd / Eq. asgd hold per coordinate).
 
-The first full K-batches of the VGG-16, Mixed, AlexNet and Text-CNN
-workloads with all their pulls, in the launch configuration bench.py times (gradient pool and
+The first full K-batches of every workload (all 200 of Tiny) with all
+their pulls, in the launch configuration bench.py times (gradient pool and
 replicas in server rows, the apply and the fan-out as separate calls). Every
 replica written by every pull event is snapshotted on the device; then the
 oracle runs block by block (at most 16M coordinates, gradient blocks copied
@@ -47,7 +47,8 @@ def first_batches(cfg, count):
     return out
 
 
-@pytest.mark.parametrize("name,batches", [("vgg16", 3), ("mixed", 2), ("alexnet", 2), ("textcnn", 3)])
+@pytest.mark.parametrize("name,batches", [("vgg16", 3), ("mixed", 2), ("alexnet", 2), ("textcnn", 3),
+                                          ("vgg16_shard8", 4), ("tiny", 200)])
 def test_workload_full_size_whole_vector(torch, name, batches):
     cfg = wl.CONFIGS[name]
     events = first_batches(cfg, batches)
