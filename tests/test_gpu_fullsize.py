@@ -47,16 +47,23 @@ def first_batches(cfg, count):
     return out
 
 
-@pytest.mark.parametrize("name,batches", [("vgg16", 3), ("mixed", 2), ("alexnet", 2), ("textcnn", 3),
-                                          ("vgg16_shard8", 4), ("tiny", 200)])
-def test_workload_full_size_whole_vector(torch, name, batches):
+@pytest.mark.parametrize("name,batches,mode", [
+    ("vgg16", 3, "fifo"), ("mixed", 2, "fifo"), ("alexnet", 2, "fifo"), ("textcnn", 3, "fifo"),
+    ("vgg16_shard8", 4, "fifo"), ("tiny", 200, "fifo"), ("vgg16", 3, "round-robin"),
+    ("vgg16", 2, "ssgd")])
+def test_workload_full_size_whole_vector(torch, name, batches, mode):
+    """mode: fifo (the default queue), round-robin (per-learner queues of K
+    slots, as bench.py --queue rr), ssgd (each apply a synchronous step over
+    the batch, Eq. ssgd)."""
     cfg = wl.CONFIGS[name]
     events = first_batches(cfg, batches)
     n = cfg.n
-    say(f"[whole] {name} n={n:,} events={len(events)}")
+    say(f"[whole] {name} {mode} n={n:,} events={len(events)}")
     rdt = torch.bfloat16 if cfg.pull_dtype == wl.BF16 else torch.float32
     srv = ps.ParameterServer(n, cfg.lr, cfg.momentum, queue_depth=cfg.depth)
     srv.set_stream(torch.cuda.current_stream())
+    if mode == "round-robin":
+        srv.set_queue_mode(ps.PS_QUEUE_ROUND_ROBIN, cfg.depth)
     pool = srv.alloc_rows(cfg.pool, torch.bfloat16 if cfg.grad_dtype == wl.BF16 else torch.float32)
     reps = srv.alloc_rows(cfg.replicas, rdt)
     for j in range(cfg.pool):
@@ -71,7 +78,10 @@ def test_workload_full_size_whole_vector(torch, name, batches):
         if isinstance(ev, wl.Push):
             assert srv.push(ev.learner, pool[ev.buf])
         elif isinstance(ev, wl.Apply):
-            srv.apply_pending()
+            if mode == "ssgd":
+                srv.apply_sync()
+            else:
+                srv.apply_pending()
             stale += srv.last_staleness()
         else:
             for rnd in parity.pull_rounds(ev.learners):
@@ -86,6 +96,8 @@ def test_workload_full_size_whole_vector(torch, name, batches):
     for lo in range(0, n, BLOCK):
         hi = min(n, lo + BLOCK)
         o = orc.OracleServer(parity.np_bits(w0[lo:hi]), cfg.lr, cfg.momentum, depth=cfg.depth)
+        if mode == "round-robin":
+            assert o.set_queue_mode(orc.ROUND_ROBIN, cfg.depth) == orc.OK
         grads = {}
         k = 0
         for ev in events:
@@ -94,7 +106,7 @@ def test_workload_full_size_whole_vector(torch, name, batches):
                     grads[ev.buf] = parity.np_bits(pool[ev.buf][lo:hi])
                 assert o.push(ev.learner, grads[ev.buf]) == orc.OK
             elif isinstance(ev, wl.Apply):
-                o.apply_pending()
+                assert (o.apply_sync() if mode == "ssgd" else o.apply_pending()) == orc.OK
             else:
                 for rnd in parity.pull_rounds(ev.learners):
                     for l in rnd:
