@@ -661,6 +661,16 @@ class ParameterServer:
     def free_rows(self, rows) -> None:
         self._check(ps_free_rows(self.h, rows[0].data_ptr()), "free_rows")
 
+    def capture(self, script: "OpScript") -> "Graph":
+        """The prepared script captured as a HIP graph (ps_graph_create):
+        nothing runs and the server's state is unchanged; Graph.launch()
+        replays it. The script's gradient and replica buffers must outlive
+        the graph (the script itself is kept by the Graph)."""
+        with self._lock:
+            rc, g = ps_graph_create(self.h, script)
+            self._check(rc, "graph_create")
+        return Graph(self, g, script)
+
     def weights_copy(self):
         """A new device tensor holding w (waits for the server's stream)."""
         return self._copy(ps_weights(self.h))
@@ -680,6 +690,37 @@ class ParameterServer:
         if rc != 0:
             raise PSError(PS_EHIP, f"hipMemcpyAsync failed ({rc})")
         return out
+
+
+class Graph:
+    """A script captured by ParameterServer.capture. launch() replays it on
+    the server's stream with the effect of ps_run of the script
+    (ps_graph_launch); it raises PSError with PS_ESTATE, changing nothing,
+    when the server's state would now launch other kernels than were
+    captured. close() frees the graph after its last replay has run
+    (ps_graph_destroy); close it before the server."""
+
+    def __init__(self, server: "ParameterServer", handle: int, script: "OpScript"):
+        self.server = server
+        self.h = handle
+        self.script = script
+
+    def launch(self) -> None:
+        if not self.h:
+            raise PSError(PS_EINVAL, "graph_launch: the graph is closed")
+        with self.server._lock:
+            self.server._check(ps_graph_launch(self.server.h, self.h), "graph_launch")
+
+    def close(self) -> None:
+        if self.h:
+            ps_graph_destroy(self.h)
+            self.h = 0
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
 
 
 _hip_rt = None

@@ -437,6 +437,45 @@ def test_graph_destroy_waits_for_its_launches(torch):
     srv.close()
 
 
+def test_graph_binding(torch):
+    """ParameterServer.capture and Graph: two replays of a push + apply_pull
+    script give the two sequential binary32 steps; a replay whose pull would
+    now be skipped raises PSError(PS_ESTATE) with nothing changed; close()
+    is idempotent and a closed graph refuses to launch."""
+    n = 50_003
+    stream = torch.cuda.Stream()
+    srv = ps.ParameterServer(n, 0.01, 0.0, queue_depth=2, stream=stream)
+    w0 = torch.rand(n, device="cuda")
+    srv.set_weights(w0)
+    g = torch.full((n,), 0.5, device="cuda")
+    rep = torch.empty(n, device="cuda")
+    step = ps.OpScript()
+    step.push(0, g.data_ptr())
+    step.apply_pull([0], [rep.data_ptr()])
+    pull_only = ps.OpScript()
+    pull_only.pull([0], [rep.data_ptr()])
+    pg = srv.capture(pull_only)              # captured while the pull writes
+    with srv.capture(step) as graph:
+        graph.launch()
+        graph.launch()
+        srv.sync()
+        w = w0.cpu().numpy().astype(np.float32)
+        p = np.float32(np.float32(0.01) * np.float32(0.5))
+        for _ in range(2):
+            w = (w - p).astype(np.float32)
+        assert parity.bitwise(parity.np_bits(rep), w.view(np.uint32))
+        pulls = srv.stats().pulls
+        with pytest.raises(ps.PSError) as e:
+            pg.launch()                      # the replica is current: skipped now
+        assert e.value.code == ps.PS_ESTATE
+        assert srv.timestamp == 2 and srv.stats().pulls == pulls
+    pg.close()
+    graph.close()
+    with pytest.raises(ps.PSError):
+        graph.launch()
+    srv.close()
+
+
 def test_graph_launch_checks_the_plan(torch):
     """A replay runs only if the calls would launch exactly the captured
     kernels: a pull written at capture that would now be skipped refuses the
