@@ -423,7 +423,9 @@ int ps_run(ps_server *ps, const ps_op *ops, int count, int *done);
  *
  * Both need a server stream other than the legacy null stream
  * (ps_set_stream), ordered pulls (no ps_set_pull_stream) and an empty queue
- * (PS_ESTATE otherwise); scripts start from an empty queue. PS_EINVAL for a
+ * (PS_ESTATE otherwise); scripts start from an empty queue. While
+ * ps_graph_create runs, no other thread may enqueue work on that stream
+ * (it is being captured). PS_EINVAL for a
  * bad script, a script that launches nothing, or a graph of another
  * server. Destroy graphs before their server; a graph is launched only on
  * the server it was created for. ps_graph_destroy waits for the graph's
