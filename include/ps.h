@@ -191,9 +191,10 @@ int ps_apply_pull(ps_server *ps, int n, const int *learner_ids, void *const *dst
 
 /* Largest replica count ps_apply_pull writes from the apply pass itself
  * (0..PS_MAX_REPLICAS), or -1 (default) to choose per call: one replica
- * always, up to 4 when the apply folds at most 16 gradients (measured faster
- * there; with more gradients or replicas the separate fan-out is). Results
- * are identical either way. PS_EINVAL for other values. */
+ * always, up to 4 when the apply folds at most 16 gradients, up to 6 when it
+ * folds at most 8 into a vector of fewer than 20M coordinates (measured
+ * faster there; with more gradients or replicas the separate fan-out is).
+ * Results are identical either way. PS_EINVAL for other values. */
 int ps_set_pull_fusion(ps_server *ps, int max_replicas);
 
 /* Use hip_stream (a hipStream_t; NULL = the null stream) for all later device

@@ -114,6 +114,8 @@ ApplyShape sync_shape(int k, bool momentum, bool bf16) {
     return {1, 0, 16};
 }
 
-bool fuse_replicas(int r, int k) { return r <= 1 || (r <= 4 && k <= 16); }
+bool fuse_replicas(int r, int k, size_t n) {
+    return r <= 1 || (r <= 4 && k <= 16) || (r <= 6 && k <= 8 && n < kSmallVector);
+}
 
 }  // namespace gadei

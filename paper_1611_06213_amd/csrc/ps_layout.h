@@ -90,8 +90,12 @@ ApplyShape apply_shape(int k, bool momentum, bool bf16, size_t n);
 ApplyShape sync_shape(int k, bool momentum, bool bf16);
 
 // Whether ps_apply_pull writes its r replicas from the apply pass over k
-// gradients (else the apply is followed by the tiled fan-out): one replica
-// always; up to 4 when at most 16 gradients are folded. Writing replicas from
+// gradients of an n-coordinate vector (else the apply is followed by the
+// tiled fan-out): one replica always; up to 4 when at most 16 gradients are
+// folded; up to 6 when at most 8 are folded into a vector of fewer than
+// kSmallVector coordinates (10M, k = 8: r = 5 0.100 vs 0.104 ms, r = 6 0.108
+// vs 0.110; at 30M and above 5 or 6 are even or slower, 138M r = 6 1.50 vs
+// 1.44 ms). Writing replicas from
 // the apply adds write streams to its read streams, which costs more than a
 // separate fan-out once there are many of either; for few of both it saves
 // the fan-out's launch and its second read of w. Measured from server rows
@@ -99,6 +103,6 @@ ApplyShape sync_shape(int k, bool momentum, bool bf16);
 // 0.079 vs 0.086 ms, 138M 1.07 vs 1.10 ms; k = 16, r = 2: 138M 1.89-1.90 vs
 // 1.93-1.94 ms; k = 16, r = 8: 138M 2.47 vs 2.42-2.43 ms; k = 32, r = 2:
 // 61M 1.55 vs 1.51 ms.
-bool fuse_replicas(int r, int k);
+bool fuse_replicas(int r, int k, size_t n);
 
 }  // namespace gadei

@@ -683,7 +683,7 @@ int ps_apply_pull(ps_server *ps, int n, const int *learner_ids, void *const *dst
         if (int rc = order_after_pulls(ps)) return rc;
     const int r = static_cast<int>(write.size());
     const bool fuse = ps->fuse_max_r >= 0 ? r <= ps->fuse_max_r
-                                           : gadei::fuse_replicas(r, static_cast<int>(b.items.size()));
+                                           : gadei::fuse_replicas(r, static_cast<int>(b.items.size()), ps->n);
     if (fuse) {
         if (int rc = launch_batch(ps, b.items, dst_dtype, dsts, write)) return rc;
     } else {

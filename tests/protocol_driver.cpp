@@ -16,7 +16,8 @@
 //   shape K M B [N]       launch shape of a K-gradient apply (M = 1: momentum; B = 1: bf16)
 //                         over N coordinates (default 138,357,544)
 //   sync_shape K M B      the same for a synchronous step over K learners
-//   fuse R K              1 if ps_apply_pull writes R replicas from the apply of K gradients
+//   fuse R K [N]          1 if ps_apply_pull writes R replicas from the apply of K gradients
+//                         over N coordinates (default 138,357,544)
 #include <cstdio>
 #include <iostream>
 #include <sstream>
@@ -160,8 +161,11 @@ int main() {
                         gadei::velocity_offset(bytes));
         } else if (cmd == "fuse") {
             long r, k;
+            size_t n = 138357544;
             in >> r >> k;
-            std::printf("fuse %d", gadei::fuse_replicas(static_cast<int>(r), static_cast<int>(k)) ? 1 : 0);
+            if (!(in >> n)) n = 138357544;
+            std::printf("fuse %d",
+                        gadei::fuse_replicas(static_cast<int>(r), static_cast<int>(k), n) ? 1 : 0);
         } else if (cmd == "shape" || cmd == "sync_shape") {
             long k, m, b = 0;
             size_t n = 138357544;

@@ -285,12 +285,18 @@ def test_apply_shape_table(driver):
 
 def test_replica_fusion_rule(driver):
     """ps_apply_pull writes one replica from the apply pass always, up to 4
-    when the apply folds at most 16 gradients, and otherwise leaves the
-    replicas to the tiled fan-out (the measured rule)."""
+    when the apply folds at most 16 gradients, up to 6 when it folds at most 8
+    into a vector under 20M coordinates, and otherwise leaves the replicas to
+    the tiled fan-out (the measured rule)."""
     cases = {(1, 1): 1, (1, 64): 1, (2, 8): 1, (4, 16): 1, (5, 8): 0, (2, 17): 0, (4, 32): 0,
              (8, 8): 0, (0, 32): 1}
     got = run_driver(driver, [f"fuse {r} {k}" for (r, k) in cases])
     assert got == [f"fuse {v}" for v in cases.values()]
+    small = {(5, 8, 10_000_000): 1, (6, 8, 19_999_999): 1, (7, 8, 10_000_000): 0,
+             (5, 9, 10_000_000): 0, (6, 8, 20_000_000): 0, (4, 16, 10_000_000): 1,
+             (5, 16, 10_000_000): 0}
+    got = run_driver(driver, [f"fuse {r} {k} {n}" for (r, k, n) in small])
+    assert got == [f"fuse {v}" for v in small.values()]
 
 
 # (K, momentum, bf16) -> (blocks per CU, fronts log2, group)
