@@ -32,6 +32,8 @@
 // relative of the sequential result.
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "ps_kernels.h"
 
 #ifdef PS_FP_CONTRACT
@@ -53,7 +55,37 @@ namespace {
 #define PS_NT_WV 1
 #endif
 
-constexpr int kBlock = PS_BLOCK;      // threads per block (waves of 64 lanes)
+constexpr int kBlock = PS_BLOCK;
+
+// Compact kernel argument blocks for launches of at most kCompact gradients
+// and kCompact replicas: the fields of ApplyArgs / PullArgs with 8-entry
+// pointer arrays (176 and 88 bytes instead of 1064 and 536). The host
+// enqueues a launch faster the smaller its argument segment (back-to-back
+// launches of an empty kernel: 4.5 us with a 1 KiB argument, 2.9 us with 64
+// bytes, each beside the runtime's implicit arguments), and that cost sets
+// the rate of launch-bound loops such as one gradient and one replica per
+// step. The kernels are the same templates over either block.
+constexpr int kCompact = 8;
+struct ApplyArgsC {
+    float *w;
+    float *v;
+    uint64_t n;
+    float lr;
+    float m;
+    int k;
+    int r;
+    int fronts_log2;
+    const void *g[kCompact];
+    void *dst[kCompact];
+};
+struct PullArgsC {
+    const float *w;
+    uint64_t n;
+    int r;
+    void *dst[kCompact];
+};
+template <class A>
+constexpr bool kCompactArgs = std::is_same_v<A, ApplyArgsC>;      // threads per block (waves of 64 lanes)
 // Gradients whose loads are issued together: the vector kernels take the
 // group size their launcher chooses (4, 8, 12, 16, 24 or 32 for the apply,
 // up to 16 for the synchronous step); the scalar paths take kGroup. Full
@@ -255,8 +287,8 @@ __device__ __forceinline__ void step(float (&w)[E], float (&v)[E], const float (
 // compiler from pulling the updates (and the bf16 widening) up between the
 // loads, which would make the later loads of a group wait for the earlier
 // ones to arrive.
-template <bool MOM, int GDT, int E, int G>
-__device__ __forceinline__ void apply_group(const ApplyArgs &a, int k0, uint64_t i, float (&w)[E],
+template <bool MOM, int GDT, int E, int G, class A>
+__device__ __forceinline__ void apply_group(const A &a, int k0, uint64_t i, float (&w)[E],
                                             float (&v)[E], float lr, float m) {
     GradBits<GDT, E> r[G];
 #pragma unroll
@@ -275,8 +307,8 @@ __device__ __forceinline__ void apply_group(const ApplyArgs &a, int k0, uint64_t
 // before entering the loop). The remainder after the full groups (and one
 // group of 8) is one straight-line group of its exact size: loads under
 // per-gradient conditions would each wait for the memory in turn.
-template <bool MOM, int GDT, int PDT, int E, int G>
-__device__ __forceinline__ void apply_chunk(const ApplyArgs &a, uint64_t i) {
+template <bool MOM, int GDT, int PDT, int E, int G, class A>
+__device__ __forceinline__ void apply_chunk(const A &a, uint64_t i) {
     static_assert(G >= 1 && G <= 32, "gradient group size must be 1..32");
     float w[E], v[E];
     ld_f32<E, nt_wv_ld<E>()>(w, a.w + i);
@@ -325,8 +357,8 @@ __device__ __forceinline__ void apply_chunk(const ApplyArgs &a, uint64_t i) {
 // and gradient groups as the apply, loaded and waited for as the compiler
 // schedules them (the apply's load arrangement measured no faster here), the
 // remainder as one predicated group.
-template <int GDT, int E, int G>
-__device__ __forceinline__ void sum_group(const ApplyArgs &a, int k0, uint64_t i, float (&s)[E]) {
+template <int GDT, int E, int G, class A>
+__device__ __forceinline__ void sum_group(const A &a, int k0, uint64_t i, float (&s)[E]) {
     float g[G][E];
 #pragma unroll
     for (int j = 0; j < G; ++j) ld_grad<GDT, E>(g[j], a.g[k0 + j], i);
@@ -336,8 +368,8 @@ __device__ __forceinline__ void sum_group(const ApplyArgs &a, int k0, uint64_t i
         for (int e = 0; e < E; ++e) s[e] = s[e] + g[j][e];
 }
 
-template <bool MOM, int GDT, int E, int G>
-__device__ __forceinline__ void sync_chunk(const ApplyArgs &a, uint64_t i) {
+template <bool MOM, int GDT, int E, int G, class A>
+__device__ __forceinline__ void sync_chunk(const A &a, uint64_t i) {
     static_assert(G >= 1 && G <= 16, "gradient group size must be 1..16");
     float w[E], v[E], s[E];
     ld_f32<E, nt_wv_ld<E>()>(w, a.w + i);
@@ -384,8 +416,8 @@ __device__ __forceinline__ uint64_t front_block(unsigned b, unsigned nb, int f) 
     return b;
 }
 
-template <bool MOM, int GDT, int E, int G>
-__global__ void __launch_bounds__(kBlock) sync_vec(const ApplyArgs a) {
+template <bool MOM, int GDT, int E, int G, class A>
+__global__ void __launch_bounds__(kBlock) sync_vec(const A a) {
     const uint64_t chunks = a.n / E;
     const uint64_t tid = static_cast<uint64_t>(blockIdx.x) * kBlock + threadIdx.x;
     const uint64_t vtid = front_block(blockIdx.x, gridDim.x, a.fronts_log2) * kBlock + threadIdx.x;
@@ -397,8 +429,8 @@ __global__ void __launch_bounds__(kBlock) sync_vec(const ApplyArgs a) {
 // Vector path: lane t of the grid owns E-coordinate chunks t', t' + stride,
 // ... where t' is t with its block renumbered by front_block. The n mod E
 // trailing coordinates go to the first lanes of the grid.
-template <bool MOM, int GDT, int PDT, int E, int G>
-__global__ void __launch_bounds__(kBlock) apply_vec(const ApplyArgs a) {
+template <bool MOM, int GDT, int PDT, int E, int G, class A>
+__global__ void __launch_bounds__(kBlock) apply_vec(const A a) {
     const uint64_t chunks = a.n / E;
     const uint64_t tid = static_cast<uint64_t>(blockIdx.x) * kBlock + threadIdx.x;
     const uint64_t vtid = front_block(blockIdx.x, gridDim.x, a.fronts_log2) * kBlock + threadIdx.x;
@@ -408,8 +440,8 @@ __global__ void __launch_bounds__(kBlock) apply_vec(const ApplyArgs a) {
 }
 
 // Scalar path for buffers without vector alignment: one coordinate per lane.
-template <bool MOM, int GDT, int PDT>
-__global__ void __launch_bounds__(kBlock) apply_scalar(const ApplyArgs a) {
+template <bool MOM, int GDT, int PDT, class A>
+__global__ void __launch_bounds__(kBlock) apply_scalar(const A a) {
     const uint64_t tid = static_cast<uint64_t>(blockIdx.x) * kBlock + threadIdx.x;
     const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kBlock;
     for (uint64_t i = tid; i < a.n; i += stride) apply_chunk<MOM, GDT, PDT, 1, kGroup>(a, i);
@@ -417,8 +449,8 @@ __global__ void __launch_bounds__(kBlock) apply_scalar(const ApplyArgs a) {
 
 // ---------------------------------------------------------------- pull
 
-template <int PDT, int E, bool NT>
-__device__ __forceinline__ void pull_chunk(const PullArgs &a, uint64_t i) {
+template <int PDT, int E, bool NT, class P>
+__device__ __forceinline__ void pull_chunk(const P &a, uint64_t i) {
     float w[E];
     ld_f32<E, NT>(w, a.w + i);
     for (int r = 0; r < a.r; ++r) st_dst<PDT, E>(a.dst[r], i, w);
@@ -426,8 +458,8 @@ __device__ __forceinline__ void pull_chunk(const PullArgs &a, uint64_t i) {
 
 // One pass: each lane reads its chunk of w once and writes it to every
 // replica. Used for a single replica (a plain streaming copy).
-template <int PDT>
-__global__ void __launch_bounds__(kBlock) pull_vec(const PullArgs a) {
+template <int PDT, class P>
+__global__ void __launch_bounds__(kBlock) pull_vec(const P a) {
     const uint64_t chunks = a.n >> 2;
     const uint64_t tid = static_cast<uint64_t>(blockIdx.x) * kBlock + threadIdx.x;
     const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kBlock;
@@ -457,8 +489,8 @@ __global__ void __launch_bounds__(kBlock) pull_vec(const PullArgs a) {
 constexpr uint64_t kTiledCoords = uint64_t(4) << 20;
 constexpr unsigned kTileBlocks = 4096;      // most blocks per (tile, replica)
 
-template <int PDT, int E>
-__global__ void __launch_bounds__(kBlock) pull_tiled(const PullArgs a, unsigned bpt) {
+template <int PDT, int E, class P>
+__global__ void __launch_bounds__(kBlock) pull_tiled(const P a, unsigned bpt) {
     constexpr uint64_t kTileChunksE = kTiledCoords / E;
     const uint64_t chunks = a.n / E;
     const unsigned b0 = blockIdx.x % bpt;
@@ -496,8 +528,8 @@ __global__ void __launch_bounds__(kBlock) pull_tiled(const PullArgs a, unsigned 
 // 0.172 vs 0.185 ms).
 constexpr uint64_t kSliceTileCoords = uint64_t(2) << 20;
 
-template <int PDT, int E>
-__global__ void __launch_bounds__(kBlock) pull_slices(const PullArgs a) {
+template <int PDT, int E, class P>
+__global__ void __launch_bounds__(kBlock) pull_slices(const P a) {
     constexpr uint64_t kTileChunksE = kSliceTileCoords / E;
     const uint64_t chunks = a.n / E;
     const unsigned b = blockIdx.x;
@@ -529,8 +561,8 @@ __global__ void __launch_bounds__(kBlock) pull_slices(const PullArgs a) {
 }
 
 // Scalar path for replicas without vector alignment.
-template <int PDT>
-__global__ void __launch_bounds__(kBlock) pull_scalar(const PullArgs a) {
+template <int PDT, class P>
+__global__ void __launch_bounds__(kBlock) pull_scalar(const P a) {
     const uint64_t tid = static_cast<uint64_t>(blockIdx.x) * kBlock + threadIdx.x;
     const uint64_t stride = static_cast<uint64_t>(gridDim.x) * kBlock;
     for (uint64_t i = tid; i < a.n; i += stride) pull_chunk<PDT, 1, false>(a, i);
@@ -552,32 +584,40 @@ unsigned grid_for(uint64_t items, const Geometry &geo) {
     return static_cast<unsigned>(blocks < cap ? blocks : cap);
 }
 
-template <bool MOM, int GDT, int PDT, int E, int G>
-hipError_t launch_vec(const ApplyArgs &a, unsigned lds, const Geometry &geo, hipStream_t s) {
-    hipLaunchKernelGGL((apply_vec<MOM, GDT, PDT, E, G>), dim3(grid_for(a.n / E, geo)), dim3(kBlock),
-                       lds, s, a);
+template <bool MOM, int GDT, int PDT, int E, int G, class A>
+hipError_t launch_vec(const A &a, unsigned lds, const Geometry &geo, hipStream_t s) {
+    hipLaunchKernelGGL((apply_vec<MOM, GDT, PDT, E, G, A>), dim3(grid_for(a.n / E, geo)),
+                       dim3(kBlock), lds, s, a);
     return hipGetLastError();
 }
 
-template <bool MOM, int GDT, int PDT, int E>
-hipError_t launch_vec_g(const ApplyArgs &a, int group, unsigned lds, const Geometry &geo,
+template <bool MOM, int GDT, int PDT, int E, class A>
+hipError_t launch_vec_g(const A &a, int group, unsigned lds, const Geometry &geo,
                         hipStream_t s) {
-    switch (group) {
-        case 4: return launch_vec<MOM, GDT, PDT, E, 4>(a, lds, geo, s);
-        case 8: return launch_vec<MOM, GDT, PDT, E, 8>(a, lds, geo, s);
-        case 12: return launch_vec<MOM, GDT, PDT, E, 12>(a, lds, geo, s);
-        case 24: return launch_vec<MOM, GDT, PDT, E, 24>(a, lds, geo, s);
-        case 32: return launch_vec<MOM, GDT, PDT, E, 32>(a, lds, geo, s);
-        default: return launch_vec<MOM, GDT, PDT, E, 16>(a, lds, geo, s);
+    if constexpr (kCompactArgs<A>) {
+        // at most kCompact gradients: groups above 8 all take one group of 8
+        // and the exact remainder, so 16 stands for 12, 24 and 32
+        if (group == 4) return launch_vec<MOM, GDT, PDT, E, 4>(a, lds, geo, s);
+        if (group == 8) return launch_vec<MOM, GDT, PDT, E, 8>(a, lds, geo, s);
+        return launch_vec<MOM, GDT, PDT, E, 16>(a, lds, geo, s);
+    } else {
+        switch (group) {
+            case 4: return launch_vec<MOM, GDT, PDT, E, 4>(a, lds, geo, s);
+            case 8: return launch_vec<MOM, GDT, PDT, E, 8>(a, lds, geo, s);
+            case 12: return launch_vec<MOM, GDT, PDT, E, 12>(a, lds, geo, s);
+            case 24: return launch_vec<MOM, GDT, PDT, E, 24>(a, lds, geo, s);
+            case 32: return launch_vec<MOM, GDT, PDT, E, 32>(a, lds, geo, s);
+            default: return launch_vec<MOM, GDT, PDT, E, 16>(a, lds, geo, s);
+        }
     }
 }
 
-template <bool MOM, int GDT, int PDT>
-hipError_t go_apply(const ApplyArgs &a, int level, const Shape &sh, const Geometry &geo,
+template <bool MOM, int GDT, int PDT, class A>
+hipError_t go_apply(const A &a, int level, const Shape &sh, const Geometry &geo,
                     hipStream_t s) {
     if (level == 0) {
-        hipLaunchKernelGGL((apply_scalar<MOM, GDT, PDT>), dim3(grid_for(a.n, geo)), dim3(kBlock),
-                           0, s, a);
+        hipLaunchKernelGGL((apply_scalar<MOM, GDT, PDT, A>), dim3(grid_for(a.n, geo)),
+                           dim3(kBlock), 0, s, a);
         return hipGetLastError();
     }
     // Residency as the caller asks (apply_shape, ps_layout.h), reserved via
@@ -594,8 +634,8 @@ hipError_t go_apply(const ApplyArgs &a, int level, const Shape &sh, const Geomet
 
 template <bool MOM, int GDT, int E, int G>
 hipError_t launch_sync_vec(const ApplyArgs &a, unsigned lds, const Geometry &geo, hipStream_t s) {
-    hipLaunchKernelGGL((sync_vec<MOM, GDT, E, G>), dim3(grid_for(a.n / E, geo)), dim3(kBlock), lds,
-                       s, a);
+    hipLaunchKernelGGL((sync_vec<MOM, GDT, E, G, ApplyArgs>), dim3(grid_for(a.n / E, geo)),
+                       dim3(kBlock), lds, s, a);
     return hipGetLastError();
 }
 
@@ -622,16 +662,16 @@ hipError_t go_sync(const ApplyArgs &a, int level, const Shape &sh, const Geometr
     return launch_sync_g<MOM, GDT, 4>(a, sh.group, lds, geo, s);
 }
 
-template <bool MOM, int GDT>
-hipError_t go_apply_p(const ApplyArgs &a, int pdt, int level, const Shape &sh, const Geometry &geo,
+template <bool MOM, int GDT, class A>
+hipError_t go_apply_p(const A &a, int pdt, int level, const Shape &sh, const Geometry &geo,
                       hipStream_t s) {
     if (pdt == PS_F32) return go_apply<MOM, GDT, PS_F32>(a, level, sh, geo, s);
     if (pdt == PS_BF16) return go_apply<MOM, GDT, PS_BF16>(a, level, sh, geo, s);
     return go_apply<MOM, GDT, -1>(a, level, sh, geo, s);
 }
 
-template <bool MOM>
-hipError_t go_apply_g(const ApplyArgs &a, int gdt, int pdt, int level, const Shape &sh,
+template <bool MOM, class A>
+hipError_t go_apply_g(const A &a, int gdt, int pdt, int level, const Shape &sh,
                       const Geometry &geo, hipStream_t s) {
     if (gdt == PS_BF16) return go_apply_p<MOM, PS_BF16>(a, pdt, level, sh, geo, s);
     return go_apply_p<MOM, PS_F32>(a, pdt, level, sh, geo, s);
@@ -642,12 +682,29 @@ hipError_t go_apply_g(const ApplyArgs &a, int gdt, int pdt, int level, const Sha
 hipError_t launch_apply(const ApplyArgs &a, int grad_dtype, int pull_dtype, int level,
                         const Shape &shape, const Geometry &geo, hipStream_t s) {
     if (a.r == 0) pull_dtype = -1;
+    if (a.k <= kCompact && a.r <= kCompact) {
+        ApplyArgsC c;
+        c.w = a.w;
+        c.v = a.v;
+        c.n = a.n;
+        c.lr = a.lr;
+        c.m = a.m;
+        c.k = a.k;
+        c.r = a.r;
+        c.fronts_log2 = a.fronts_log2;
+        for (int j = 0; j < kCompact; ++j) {
+            c.g[j] = j < a.k ? a.g[j] : nullptr;
+            c.dst[j] = j < a.r ? a.dst[j] : nullptr;
+        }
+        if (c.v != nullptr) return go_apply_g<true>(c, grad_dtype, pull_dtype, level, shape, geo, s);
+        return go_apply_g<false>(c, grad_dtype, pull_dtype, level, shape, geo, s);
+    }
     if (a.v != nullptr) return go_apply_g<true>(a, grad_dtype, pull_dtype, level, shape, geo, s);
     return go_apply_g<false>(a, grad_dtype, pull_dtype, level, shape, geo, s);
 }
 
-template <int PDT, int E>
-void go_pull_tiled(const PullArgs &a, const Geometry &geo, hipStream_t s) {
+template <int PDT, int E, class P>
+void go_pull_tiled(const P &a, const Geometry &geo, hipStream_t s) {
     const uint64_t chunks = a.n / E;
     const bool one_d = PDT == PS_F32 && chunks / (kTiledCoords / E) >= 8;
     if (!one_d) {
@@ -660,7 +717,7 @@ void go_pull_tiled(const PullArgs &a, const Geometry &geo, hipStream_t s) {
         if (bx < 1) bx = 1;
         if (bx > 8) bx = (bx + 7) / 8 * 8;
         if (tiles <= 65535 && bx * tiles * static_cast<uint64_t>(a.r) <= kMaxBlocks) {
-            hipLaunchKernelGGL((pull_slices<PDT, E>),
+            hipLaunchKernelGGL((pull_slices<PDT, E, P>),
                                dim3(static_cast<unsigned>(bx), static_cast<unsigned>(a.r),
                                     static_cast<unsigned>(tiles)),
                                dim3(kBlock), 0, s, a);
@@ -678,19 +735,21 @@ void go_pull_tiled(const PullArgs &a, const Geometry &geo, hipStream_t s) {
     if (groups * bpt > kMaxBlocks) bpt = kMaxBlocks / groups;   // lanes stride further
     if (bpt < 1) {
         // more (tile, replica) pairs than a grid can hold: one pass per lane
-        hipLaunchKernelGGL(pull_vec<PDT>, dim3(grid_for(a.n >> 2, geo)), dim3(kBlock), 0, s, a);
+        hipLaunchKernelGGL((pull_vec<PDT, P>), dim3(grid_for(a.n >> 2, geo)), dim3(kBlock), 0, s,
+                           a);
         return;
     }
-    hipLaunchKernelGGL((pull_tiled<PDT, E>), dim3(static_cast<unsigned>(groups * bpt)),
+    hipLaunchKernelGGL((pull_tiled<PDT, E, P>), dim3(static_cast<unsigned>(groups * bpt)),
                        dim3(kBlock), 0, s, a, static_cast<unsigned>(bpt));
 }
 
-template <int PDT>
-void go_pull(const PullArgs &a, int level, const Geometry &geo, hipStream_t s) {
+template <int PDT, class P>
+void go_pull(const P &a, int level, const Geometry &geo, hipStream_t s) {
     if (level == 0) {
-        hipLaunchKernelGGL(pull_scalar<PDT>, dim3(grid_for(a.n, geo)), dim3(kBlock), 0, s, a);
+        hipLaunchKernelGGL((pull_scalar<PDT, P>), dim3(grid_for(a.n, geo)), dim3(kBlock), 0, s, a);
     } else if (a.r == 1) {
-        hipLaunchKernelGGL(pull_vec<PDT>, dim3(grid_for(a.n >> 2, geo)), dim3(kBlock), 0, s, a);
+        hipLaunchKernelGGL((pull_vec<PDT, P>), dim3(grid_for(a.n >> 2, geo)), dim3(kBlock), 0, s,
+                           a);
     } else if (PDT == PS_BF16 && level == 2) {
         go_pull_tiled<PDT, 8>(a, geo, s);
     } else {
@@ -710,6 +769,16 @@ hipError_t launch_sync(const ApplyArgs &a, int grad_dtype, int level, const Shap
 
 hipError_t launch_pull(const PullArgs &a, int pull_dtype, int level, const Geometry &geo,
                        hipStream_t s) {
+    if (a.r <= kCompact) {
+        PullArgsC c;
+        c.w = a.w;
+        c.n = a.n;
+        c.r = a.r;
+        for (int j = 0; j < kCompact; ++j) c.dst[j] = j < a.r ? a.dst[j] : nullptr;
+        if (pull_dtype == PS_BF16) go_pull<PS_BF16>(c, level, geo, s);
+        else go_pull<PS_F32>(c, level, geo, s);
+        return hipGetLastError();
+    }
     if (pull_dtype == PS_BF16) go_pull<PS_BF16>(a, level, geo, s);
     else go_pull<PS_F32>(a, level, geo, s);
     return hipGetLastError();

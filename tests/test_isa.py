@@ -5,6 +5,11 @@
   multiply-add instructions: every product and sum is rounded on its own
   (the binary32 reading of Eq. "gd"), and packed fp32 stays disabled.
 * No kernel uses private (scratch) memory: registers hold every value.
+* Launches of at most 8 gradients and 8 replicas take kernels over a compact
+  argument block; the others a full one (64 pointers per array). With the
+  runtime's implicit arguments the compact segments stay under 448 bytes and
+  the full ones at 536 or more: the host enqueues a launch faster the smaller its
+  argument segment.
 * The fused applies of the VGG-16 shape (fp32 gradients, one group of 32)
   and of the Mixed shape (bf16 gradients, groups of 24) issue each group's
   gradient loads back to back, non-temporal, before waiting for the first:
@@ -23,8 +28,8 @@ import pytest
 from paper_1611_06213_amd import build as B
 
 KERNELS = os.path.join(B.CSRC, "ps_kernels.hip")
-VGG16_APPLY = "_ZN5gadei12_GLOBAL__N_19apply_vecILb1ELi0ELin1ELi4ELi32EEEvNS_9ApplyArgsE"
-MIXED_APPLY = "_ZN5gadei12_GLOBAL__N_19apply_vecILb1ELi1ELin1ELi8ELi24EEEvNS_9ApplyArgsE"
+VGG16_APPLY = "_ZN5gadei12_GLOBAL__N_19apply_vecILb1ELi0ELin1ELi4ELi32ENS_9ApplyArgsEEEvT4_"
+MIXED_APPLY = "_ZN5gadei12_GLOBAL__N_19apply_vecILb1ELi1ELin1ELi8ELi24ENS_9ApplyArgsEEEvT4_"
 
 
 @pytest.fixture(scope="module")
@@ -72,6 +77,22 @@ def test_no_kernel_uses_scratch(asm):
     for name, (_, meta) in ks.items():
         m = re.search(r"\.amdhsa_private_segment_fixed_size (\d+)", meta)
         assert m and int(m.group(1)) == 0, name
+
+
+def test_compact_argument_blocks(asm):
+    ks = kernels(asm)
+    compact = full = 0
+    for name, (_, meta) in ks.items():
+        if not re.search(r"apply_vec|apply_scalar|pull_", name):
+            continue
+        size = int(re.search(r"\.amdhsa_kernarg_size (\d+)", meta).group(1))
+        if "ArgsC" in name:
+            compact += 1
+            assert size <= 448, (name, size)
+        else:
+            full += 1
+            assert size >= 536, (name, size)
+    assert compact >= 60 and full >= 60, (compact, full)
 
 
 @pytest.mark.parametrize("name,group,wv", [(VGG16_APPLY, 32, 2), (MIXED_APPLY, 24, 4)],
