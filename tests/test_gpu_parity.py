@@ -1473,6 +1473,50 @@ def test_fronts_give_identical_bits(torch, layout, gdt):
     free(torch)
 
 
+@pytest.mark.parametrize("rdt", ["f32", "bf16"])
+def test_argument_block_boundary(torch, rdt):
+    """Launches of at most 8 gradients and 8 replicas run over the compact
+    argument block, larger ones over the full one: at K = 7, 8, 9 and 16
+    gradients and R = 7, 8, 9 and 16 replicas, ps_apply_pull with the
+    replicas written from the apply pass, and the same apply followed by
+    ps_pull_many, give the oracle's w, v and replica bits."""
+    n, lr, m = 4 * 8192 + 3, 0.01, 0.9
+    say(f"[case] argument block boundary replicas={rdt} n={n}")
+    tdt = torch.bfloat16 if rdt == "bf16" else torch.float32
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(43)
+    w0 = (torch.rand(n, generator=gen, device="cuda") - 0.5) * 0.1
+    grads = [torch.randn(n, generator=gen, device="cuda") * 1e-3 for _ in range(16)]
+    host = [g.cpu().numpy() for g in grads]
+    srv = ps.ParameterServer(n, lr, m, queue_depth=16)
+    for k in (7, 8, 9, 16):
+        o = orc.OracleServer(w0.cpu().numpy(), lr, m, depth=16)
+        for j in range(k):
+            assert o.push(j, host[j]) == orc.OK
+        o.apply_pending()
+        want_w, want_v = o.w.view(np.uint32).copy(), o.v.view(np.uint32).copy()
+        want_r = want_w.view(np.float32) if rdt == "f32" else orc.f32_to_bf16(want_w.view(np.float32))
+        for r in (7, 8, 9, 16):
+            for fused in (True, False):
+                reps = [torch.full((n,), float("nan"), dtype=tdt, device="cuda") for _ in range(r)]
+                srv.set_weights(w0)
+                for j in range(k):
+                    assert srv.push(j, grads[j])
+                if fused:
+                    srv.set_pull_fusion(64)
+                    srv.apply_pull(list(range(r)), reps)
+                    srv.set_pull_fusion(-1)
+                else:
+                    srv.apply_pending()
+                    srv.pull_many(list(range(r)), reps)
+                assert parity.bitwise(parity.np_bits(srv.weights_copy()), want_w), (k, r, fused)
+                assert parity.bitwise(parity.np_bits(srv.velocity_copy()), want_v), (k, r, fused)
+                for rep in reps:
+                    assert parity.bitwise(parity.np_bits(rep), want_r), (k, r, fused)
+    srv.close()
+    free(torch)
+
+
 @pytest.mark.parametrize("m", [0.0, 0.9])
 @pytest.mark.parametrize("gdt", ["f32", "bf16"])
 def test_every_group_and_remainder(torch, gdt, m):
